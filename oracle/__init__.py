@@ -1,0 +1,15 @@
+"""Oracle for the exact FP4-GEMM integer product (test infrastructure only).
+
+This package is a plain, slow, CPU-only restatement of what the method
+computes, written from the paper and independent of the HIP library: it shares
+no code, table, header or constant generator with ``paper_2609_24519_amd``,
+and neither imports the other.  Only ``tests/``, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py`` may import or execute it.
+
+* ``gemm``    -- the plain definition C = A B (and C mod m), a C triple loop
+                 with a 64-bit accumulator, loaded through ctypes.
+* ``schemes`` -- the paper's encodings (storable set, limb tables, planes,
+                 reconstruction coefficients, coverage, K*), the scheme
+                 identity and the run-time procedure in plain numpy int64.
+* ``modm``    -- the congruence (mod m) schemes and their tables.
+"""

@@ -1,0 +1,107 @@
+/*
+ * Oracle (test infrastructure only): the plain definition of the integer
+ * matrix product that the FP4 method must reproduce exactly.
+ *
+ * The method's whole contract is that its output equals the error-free
+ * integer product C = A B (Sec. 1, the definition of an error-free matrix
+ * product; Alg. 1, its postcondition), or that product reduced modulo m
+ * (Sec. 5.3, the congruence relaxation).  So the oracle is that definition
+ * written out: a triple loop with a 64-bit integer accumulator.  It shares no
+ * code, table or header with the HIP library.  Only tests/, the package's
+ * smoke entry and the CPU-baseline leg of the benchmark may load it.
+ *
+ * Layouts: A is M x K row-major with leading dimension lda (A[i*lda + k]);
+ * B is K x N row-major with leading dimension ldb (B[k*ldb + j]); C is M x N
+ * row-major with leading dimension ldc.  OpenMP splits the rows of C; each
+ * thread runs the same plain loop over its rows.
+ */
+#include <stdint.h>
+
+/* C = A B exactly, int8 inputs (an int4 operand arrives in an int8 container). */
+void oracle_gemm_i8_i64(int64_t M, int64_t N, int64_t K,
+                        const int8_t* A, int64_t lda,
+                        const int8_t* B, int64_t ldb,
+                        int64_t* C, int64_t ldc)
+{
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < M; ++i) {
+        int64_t* c = C + i * ldc;
+        for (int64_t j = 0; j < N; ++j) c[j] = 0;
+        for (int64_t k = 0; k < K; ++k) {
+            const int64_t a = A[i * lda + k];
+            const int8_t* b = B + k * ldb;
+            for (int64_t j = 0; j < N; ++j) c[j] += a * (int64_t)b[j];
+        }
+    }
+}
+
+/* The same product restricted to the listed rows and columns of C:
+   C[r*nc + c] = sum_k A[rows[r], k] * B[k, cols[c]].  Used to check sampled
+   output tiles of products too large to form in full on the host. */
+void oracle_gemm_i8_i64_sampled(int64_t nr, const int64_t* rows,
+                                int64_t nc, const int64_t* cols, int64_t K,
+                                const int8_t* A, int64_t lda,
+                                const int8_t* B, int64_t ldb,
+                                int64_t* C)
+{
+    #pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < nr; ++r) {
+        const int8_t* a = A + rows[r] * lda;
+        for (int64_t c = 0; c < nc; ++c) {
+            int64_t acc = 0;
+            for (int64_t k = 0; k < K; ++k) acc += (int64_t)a[k] * (int64_t)B[k * ldb + cols[c]];
+            C[r * nc + c] = acc;
+        }
+    }
+}
+
+/* (A B) mod m for residue operands, as the non-negative residue in [0, m). */
+void oracle_gemm_u8_mod(int64_t m, int64_t M, int64_t N, int64_t K,
+                        const uint8_t* A, int64_t lda,
+                        const uint8_t* B, int64_t ldb,
+                        int32_t* C, int64_t ldc)
+{
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < M; ++i) {
+        for (int64_t j = 0; j < N; ++j) {
+            int64_t acc = 0;
+            for (int64_t k = 0; k < K; ++k) acc += (int64_t)A[i * lda + k] * (int64_t)B[k * ldb + j];
+            C[i * ldc + j] = (int32_t)(((acc % m) + m) % m);
+        }
+    }
+}
+
+/* Sampled variant of the residue product. */
+void oracle_gemm_u8_mod_sampled(int64_t m, int64_t nr, const int64_t* rows,
+                                int64_t nc, const int64_t* cols, int64_t K,
+                                const uint8_t* A, int64_t lda,
+                                const uint8_t* B, int64_t ldb,
+                                int32_t* C)
+{
+    #pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < nr; ++r) {
+        const uint8_t* a = A + rows[r] * lda;
+        for (int64_t c = 0; c < nc; ++c) {
+            int64_t acc = 0;
+            for (int64_t k = 0; k < K; ++k) acc += (int64_t)a[k] * (int64_t)B[k * ldb + cols[c]];
+            C[r * nc + c] = (int32_t)(((acc % m) + m) % m);
+        }
+    }
+}
+
+/* Number of OpenMP threads the loops above will use (reported with timings). */
+int oracle_num_threads(void)
+{
+    int n = 1;
+    #pragma omp parallel
+    {
+        #pragma omp single
+        {
+#ifdef _OPENMP
+            extern int omp_get_num_threads(void);
+            n = omp_get_num_threads();
+#endif
+        }
+    }
+    return n;
+}

@@ -1,0 +1,178 @@
+"""Pins for the oracle's encodings (CPU only).
+
+Each check ties the oracle's scheme code to something the paper or the
+mathematics fixes: the printed coverages, K* values and coefficients
+(tests/golden/paper_values.txt, each line citing its passage), the E2M1 format
+definition, exact rational re-solving of the reconstruction coefficients, and
+brute force over every input pair.  The mutation tests plant a mistake in a
+copy of a scheme and require the pins to catch it.
+"""
+import copy
+
+import numpy as np
+import pytest
+
+from oracle import schemes as sc
+
+
+def test_storable_set(paper):
+    assert sorted(sc.S) == sorted(paper["storable_set"])
+    # S is the E2M1 value set doubled (format definition, sign-magnitude codes 0..15)
+    doubled = {int(2 * sc.e2m1_value(c)) for c in range(16)}
+    assert doubled == set(sc.S)
+    assert [sc.e2m1_value(c) for c in range(8)] == list(sc.E2M1_VALUES)
+
+
+def test_b13_positional(paper):
+    assert list(sc.b13().w) == paper["b13.weights"]
+    assert [sc.x_carry(L) for L in (1, 2, 3)] == paper["b13.xcarry"]
+    # X_carry(L) = (13^L - 1) / 3 (App. B closed form)
+    assert all(sc.x_carry(L) == (13 ** L - 1) // 3 for L in range(1, 7))
+    limbs3 = sc.admissible([(1, 0, 0), (0, 1, 0), (0, 0, 1)], 3, 12)
+    assert sc.coverage((1, 13, 169), limbs3) == paper["b13.xcarry"][2]
+    limbs2 = sc.admissible([(1, 0), (0, 1)], 2, 12)
+    assert sc.coverage((1, 13), limbs2) == paper["b13.xcarry"][1]
+    assert sc.b13().r == paper["b13.products"][0]
+    for x in range(-128, 128):
+        d = sc.b13_digits(x)
+        assert sum(a * 13 ** i for i, a in enumerate(d)) == x
+        assert all(a in sc.S_SET for a in d)
+        assert d[2] in (-1, 0, 1)
+    # the INT8 side of the ternary x INT8 construction has K* = 2^24 / (1 * 8): largest limb 8
+    assert sc.stored_cap(sc.b13(), "a") == 8
+    assert sc.k_star(1, 1, 8) == paper["kstar.ternary_int8"][0]
+
+
+def test_awe6_printed(paper):
+    s = sc.awe6()
+    assert list(s.w) == paper["awe6.w"] and list(s.v) == paper["awe6.w"]
+    assert [l for _, _, l in s.products] == paper["awe6.ell"]
+    assert s.r == paper["awe6.products"][0]
+    # re-solve the coefficients from planes and weights alone (independent verification)
+    assert [f for f in sc.solve_ell(s)] == paper["awe6.ell"]
+    assert sc.coefficient_identity_holds(s)
+    cap6 = sc.admissible(s.planes_a, 3, 6)
+    assert sc.coverage(s.w, cap6) == paper["awe6.coverage_cap6"][0]
+    assert sc.coverage(s.w, sc.admissible(s.planes_a, 3, 12)) >= 127
+    assert sc.stored_cap(s, "a") == 6 and sc.stored_cap(s, "b") == 6
+    assert sc.k_star(1, 6, 6) == paper["awe6.kstar_cap6"][0]
+    assert sc.k_star(1, 12, 12) == paper["awe6.kstar_fullS"][0]
+
+
+def test_awe6_alt_printed(paper):
+    s = sc.awe6_alt()
+    assert list(s.w) == paper["awe6_alt.w"]
+    assert [l for _, _, l in s.products] == paper["awe6_alt.ell"]
+    assert [f for f in sc.solve_ell(s)] == paper["awe6_alt.ell"]
+    full = sc.admissible(s.planes_a, 3, 12)
+    assert sc.coverage(s.w, full) == paper["awe6_alt.coverage"][0]
+
+
+def test_awe4_printed(paper):
+    s = sc.awe4()
+    assert list(s.w) == paper["awe4.w"] and list(s.v) == paper["awe4.v"]
+    assert [l for _, _, l in s.products] == paper["awe4.ell"]
+    assert s.D == paper["awe4.D"][0]
+    lam = sc.solve_ell(s)
+    assert [f * s.D for f in lam] == paper["awe4.ell"]
+    assert sc.coefficient_identity_holds(s)
+    assert [sc.stored_cap(s, "a"), sc.stored_cap(s, "b")] == paper["awe4.cap"]
+    assert sc.k_star(1, *paper["awe4.cap"]) == paper["awe4.kstar"][0]
+
+
+def test_kstar_formula(paper):
+    assert sc.k_star(1, 127, 127) == paper["kstar.bf16_int8"][0]
+    assert sc.k_star(1, 127, 1) == paper["kstar.bf16_ternary"][0]
+    assert sc.k_star(1, 14, 14) == paper["kstar.fp8fp4"][0]
+
+
+@pytest.mark.parametrize("name", ["b13", "awe6", "awe6_alt", "awe4"])
+def test_round_trip_and_storability(name):
+    s = sc.PAPER_SCHEMES[name]()
+    for side in ("a", "b"):
+        lo, hi = s.range_a if side == "a" else s.range_b
+        w = s.w if side == "a" else s.v
+        planes = s.planes_a if side == "a" else s.planes_b
+        cap = s.cap_a if side == "a" else s.cap_b
+        limbs = sc.limb_table(s, side)
+        for x in range(lo, hi + 1):
+            a = limbs[x]
+            assert sc.dot(w, a) == x
+            assert all(l in sc.S_SET for l in a)
+            for c in planes:
+                assert sc.dot(c, a) in sc.S_SET and abs(sc.dot(c, a)) <= cap
+
+
+@pytest.mark.parametrize("name", ["b13", "awe6", "awe6_alt", "awe4"])
+def test_brute_force_all_pairs(name):
+    assert sc.brute_force_pairs(sc.PAPER_SCHEMES[name]())
+
+
+@pytest.mark.parametrize("name", ["awe6", "awe6_alt", "awe4"])
+def test_identity_all_admissible(name):
+    assert sc.identity_all_admissible(sc.PAPER_SCHEMES[name]())
+
+
+def test_scheme_gemm_equals_plain_product():
+    rng = np.random.default_rng(0)
+    A = rng.integers(-128, 127, (13, 40), endpoint=True)
+    B = rng.integers(-128, 127, (40, 9), endpoint=True)
+    A4 = rng.integers(-8, 7, (13, 40), endpoint=True)
+    for name in ("b13", "awe6", "awe6_alt"):
+        assert np.array_equal(sc.scheme_gemm(sc.PAPER_SCHEMES[name](), A, B), A @ B)
+    assert np.array_equal(sc.scheme_gemm(sc.awe4(), A4, B), A4 @ B)
+
+
+def test_endpoints_are_covered():
+    # the two's-complement endpoints -128 and -8 are encodable although the paper's
+    # symmetric width convention does not require them
+    for name in ("b13", "awe6", "awe6_alt"):
+        assert -128 in sc.limb_table(sc.PAPER_SCHEMES[name](), "a")
+    assert -8 in sc.limb_table(sc.awe4(), "a")
+
+
+# ---- planted mistakes: the pins must fail ---------------------------------
+def _mutate_ell(s, k, new):
+    t = copy.deepcopy(s)
+    a, b, _ = t.products[k]
+    t.products[k] = (a, b, new)
+    return t
+
+
+@pytest.mark.parametrize("k", range(6))
+def test_mutation_sign_flip_caught(k):
+    s = sc.awe6()
+    bad = _mutate_ell(s, k, -s.products[k][2])
+    assert not sc.coefficient_identity_holds(bad)
+    assert not sc.brute_force_pairs(bad)
+
+
+def test_mutation_dropped_term_caught():
+    s = sc.awe6()
+    bad = copy.deepcopy(s)
+    bad.products = bad.products[:-1]
+    assert not sc.coefficient_identity_holds(bad)
+    assert not sc.brute_force_pairs(bad)
+
+
+def test_mutation_wrong_plane_caught():
+    s = sc.awe4()
+    bad = copy.deepcopy(s)
+    a, b, l = bad.products[1]
+    bad.products[1] = (a, (0, -1, 1), l)  # b2 - b1 instead of b1 - b2
+    bad.planes_b[bad.planes_b.index(b)] = (0, -1, 1)
+    assert not sc.coefficient_identity_holds(bad)
+    assert not sc.brute_force_pairs(bad)
+
+
+def test_mutation_wrong_weight_caught():
+    s = sc.awe6()
+    bad = copy.deepcopy(s)
+    bad.w = (1, 29, 38)
+    bad.v = (1, 29, 38)
+    assert not sc.coefficient_identity_holds(bad)
+    try:
+        ok = sc.brute_force_pairs(bad)
+    except ValueError:  # the weights may no longer cover the int8 range
+        ok = False
+    assert not ok

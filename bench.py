@@ -1,0 +1,174 @@
+"""Benchmark of the exact INT8 x INT8 product as 6 FP4 GEMMs (AWE) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+One step is the whole hot path on one batch of resident synthetic input:
+encode A, encode B, the r FP4 products with their fused reconstruction
+(the calls awe_encode, awe_encode, awe_gemm_planes, i.e. awe_gemm_exact).
+The workload is M = N = K = 8192 with int8 entries uniform in [-128, 127]
+(seed 0) and int32 C.  Printed: one JSON line with the end-to-end exact TOPS
+as ``value``, the roofline of the dominant kernel (the GEMM) from HIP events
+on its stream, the 9-product base-13 baseline and the native INT8 MFMA GEMM
+(hipBLASLt through torch._int_mm) timed in the same run as context, and the
+oracle timed on the host's cores on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "exact INT8xINT8 GEMM TOPS at 8192^3 (6 FP4 GEMMs) + % of FP4 MFMA peak"
+FP4_PEAK_TFLOPS = 10100.0  # MI355X dense MXFP4 MFMA
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--size", type=int, default=8192)
+    p.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
+    p.add_argument("--no-context", action="store_true", help="skip base-13 and INT8 context")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2609_24519_amd import awe, inputs
+
+    if not os.path.exists(awe.LIB_PATH):
+        from paper_2609_24519_amd import build as hip_build
+        hip_build.build()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    M = N = K = args.size
+    A_h, B_h = inputs.int8_pair(M, N, K, seed=0)
+    A = torch.from_numpy(A_h).to(dev)
+    B = torch.from_numpy(B_h).to(dev)
+    C = torch.empty((M, N), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def setup(enc):
+        info = awe.get_encoding_info(enc)
+        pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, M, K), dtype=torch.uint8, device=dev)
+        pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, N, K), dtype=torch.uint8, device=dev)
+        return info, pa, pb
+
+    def step(enc, pa, pb, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        awe.encode(enc, 0, awe.SIDE_A, A, M, K, K, pa, None, stream)
+        awe.encode(enc, 0, awe.SIDE_B, B, N, K, N, pb, None, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I32, 0, stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    def run(enc, steps, warmup):
+        info, pa, pb = setup(enc)
+        for _ in range(warmup):
+            step(enc, pa, pb)
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        t0 = time.perf_counter()
+        for s in range(steps):
+            step(enc, pa, pb, evs[s])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        enc_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / steps
+        gemm_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / steps
+        return info, wall, enc_ms, gemm_ms
+
+    info, wall, enc_ms, gemm_ms = run(awe.ENC_AWE6, args.steps, args.warmup)
+    ms_step = wall / args.steps * 1e3
+    ops = 2.0 * M * N * K
+    r = info["r"]
+    gemm_tflops = r * ops / (gemm_ms * 1e-3) / 1e12
+    enc_bytes = (M * K + N * K) * (1 + info["planes_a"] / 2.0)
+    line = {
+        "metric": METRIC,
+        "value": round(ops / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "e2m1",
+        "data": "synthetic",
+        "config": {"workload": "AWE 6-product exact INT8xINT8 GEMM, M=N=K=%d, int8 uniform "
+                               "[-128,127] seed 0, int32 C (encode A + encode B + GEMM)" % M,
+                   "M": M, "N": N, "K": K, "encoding": "awe6", "products": r},
+        "gemm_only": {"ms": round(gemm_ms, 4), "exact_TOPS": round(ops / (gemm_ms * 1e-3) / 1e12, 2),
+                      "fp4_TFLOPs": round(gemm_tflops, 1),
+                      "fp4_peak_frac": round(gemm_tflops / FP4_PEAK_TFLOPS, 4)},
+        "encode": {"ms": round(enc_ms, 4), "GB_s": round(enc_bytes / (enc_ms * 1e-3) / 1e9, 1)},
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": FP4_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / FP4_PEAK_TFLOPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_context:
+        binfo, bwall, benc_ms, bgemm_ms = run(awe.ENC_B13, max(3, args.steps // 2), 2)
+        line["base13_9_products"] = {
+            "ms_per_step": round(bwall / max(3, args.steps // 2) * 1e3, 4),
+            "gemm_ms": round(bgemm_ms, 4),
+            "gemm_exact_TOPS": round(ops / (bgemm_ms * 1e-3) / 1e12, 2),
+            "fp4_peak_frac": round(binfo["r"] * ops / (bgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
+        try:
+            Ci = torch._int_mm(A, B)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(5):
+                Ci = torch._int_mm(A, B)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ims = e0.elapsed_time(e1) / 5
+            line["int8_mfma_context"] = {"library": "hipBLASLt via torch._int_mm", "ms": round(ims, 4),
+                                         "TOPS": round(ops / (ims * 1e-3) / 1e12, 1)}
+            # both products are exact, so the last AWE result must equal the INT8 GEMM bit for bit
+            line["int8_mfma_context"]["equal_to_exact_C"] = bool(torch.equal(Ci, C))
+        except Exception as ex:  # noqa: BLE001 - context only
+            line["int8_mfma_context"] = {"error": str(ex)[:200]}
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(A_h, B_h)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(A_h, B_h, rows=48):
+    """The oracle (plain int64 triple loop, OpenMP over rows) on a bounded sample:
+    ``rows`` rows of C over the full N and K, scaled to exact TOPS."""
+    import numpy as np
+
+    from oracle import gemm as og
+
+    if not os.path.exists(os.path.join(ROOT, "oracle", "liboracle_gemm.so")):
+        og.build()
+    K, N = B_h.shape
+    sub = np.ascontiguousarray(A_h[:rows])
+    t0 = time.perf_counter()
+    og.gemm_i64(sub, B_h)
+    dt = time.perf_counter() - t0
+    macs = rows * N * K
+    return {"value": round(2.0 * macs / dt / 1e12, 6), "unit": "TOPS", "cores": og.num_threads(),
+            "kind": "oracle",
+            "sample": "%d of %d rows of C (%d x %d x %d MACs), %.1f s" % (rows, A_h.shape[0], rows, N, K, dt)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,175 @@
+/*
+ * awe.h -- exact integer matrix products as a few FP4 (E2M1) GEMMs on MI355X.
+ *
+ * The method (Adaptive Weight Encoding, arXiv 2609.24519): each integer
+ * operand entry is split into limbs in the storable set
+ * S = {0, +-1, +-2, +-3, +-4, +-6, +-8, +-12} (the E2M1 values doubled,
+ * Sec. 3.1), with integer weights w (A side) and v (B side).  Stored "planes"
+ * are linear combinations of limbs (Definition 4.1).  Product k multiplies
+ * plane alpha_k of A by plane beta_k of B on the FP4 matrix unit with FP32
+ * accumulation, which is exact while the reduction length stays below
+ * K* = 2^24 / (n_g c_A c_B) (Sec. 3.4).  The exact result is
+ * C = (sum_k ell_k P_k) / D with D a power of two (Alg. 1).  Relaxed to a
+ * congruence with integer coefficients, the same procedure gives C mod m for
+ * the residues of Ozaki scheme II (Sec. 5.3).
+ *
+ * Conventions for every entry point below:
+ *  - Pointers are DEVICE pointers unless marked host.  The caller allocates
+ *    and owns every buffer; the library keeps only its constant tables (host
+ *    memory) and allocates no device memory.
+ *  - Device work is enqueued asynchronously on `stream` (0 = the null
+ *    stream).  Argument errors are detected on the host before anything is
+ *    enqueued and returned as a status; nothing is written then.  No C++
+ *    exception crosses this interface.  awe_last_error() gives detail.
+ *  - Results are bit-exact and do not depend on the launch configuration.
+ *  - Matrices are row-major: A is M x K (A[i*lda + k]), B is K x N
+ *    (B[k*ldb + j]), C is M x N (C[i*ldc + j]).  Leading dimensions must be
+ *    at least the row length.  Empty problems (M or N zero) succeed and write
+ *    nothing; K = 0 writes zeros.
+ *
+ * Stored plane layout (the output of awe_encode, the input of
+ * awe_gemm_planes).  One side holds P planes back to back; plane p starts at
+ * byte p * stride, stride = ceil(rows/32) * (Kp/64) * 1024 with
+ * Kp = K rounded up to a multiple of 128.  A plane is a grid of 1024-byte
+ * bricks, brick (rb, ks) at byte (rb * Kp/64 + ks) * 1024, covering rows
+ * (A: rows of A; B: columns of B) rb*32 .. rb*32+31 and reduction indices
+ * ks*64 .. ks*64+63.  Inside a brick, lane L = 32*h + t (h in {0,1},
+ * t in 0..31) owns bytes L*16 .. L*16+15, which hold row rb*32 + t at
+ * reduction indices ks*64 + 32*h + j, j = 0..31, element j in the low nibble
+ * of byte L*16 + j/2 when j is even and in the high nibble when j is odd.
+ * This is the operand order of one lane of the 32x32x64 scaled FP4 MFMA, so
+ * a brick is one wave's operand fragment.  Each nibble is the E2M1 code of
+ * the stored value s/2 (s in S): bit 3 the sign, bits 2..0 the magnitude
+ * index of |s| in (0, 1, 2, 3, 4, 6, 8, 12).  Padding rows and reduction
+ * indices hold code 0 (value 0), so they add nothing to any product.
+ */
+#ifndef AWE_H
+#define AWE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum awe_status {
+  AWE_OK = 0,
+  AWE_ERR_INVALID_VALUE = 1, /* bad pointer, size, leading dimension, enum or modulus */
+  AWE_ERR_UNSUPPORTED = 2,   /* no scheme for this modulus, or a size past what the kernels handle */
+  AWE_ERR_OVERFLOW = 3,      /* int32 C requested but max|A| max|B| K exceeds 2^31 - 1 */
+  AWE_ERR_WORKSPACE = 4,     /* workspace missing or smaller than awe_workspace_bytes */
+  AWE_ERR_HIP = 5,           /* a HIP runtime call failed */
+  AWE_ERR_TABLE = 6          /* an encoding table failed its self-check */
+} awe_status;
+
+typedef enum awe_encoding {
+  AWE_ENC_B13 = 1,     /* INT8 x INT8, base-13 positional limbs (1, 13, 169), all 9 limb pairs
+                          (Sec. 3.2; Table 1 baseline).  Equal coefficients share an accumulator. */
+  AWE_ENC_AWE6 = 2,    /* INT8 x INT8 in 6 products, w = v = (1, 29, 37), planes a_i and a_i + a_j,
+                          stored values capped at 6 (Sec. 4.3; App. A) */
+  AWE_ENC_AWE6ALT = 3, /* INT8 x INT8 in 6 products, w = v = (1, 11, 39) (Sec. 4.3; App. A) */
+  AWE_ENC_AWE4 = 4,    /* INT4 x INT8 in 4 products, A = 3a0 + 5a1, B = 5b0 + 3b1 + 42b2, D = 2
+                          (App. A).  The int4 operand is stored one value per int8 byte. */
+  AWE_ENC_MOD = 5      /* residues modulo m (Sec. 5.3); needs the modulus argument */
+} awe_encoding;
+
+typedef enum awe_side { AWE_SIDE_A = 0, AWE_SIDE_B = 1 } awe_side;
+typedef enum awe_dtype { AWE_I32 = 0, AWE_I64 = 1 } awe_dtype;
+
+#define AWE_MAX_LIMBS 4
+#define AWE_MAX_PLANES 8
+#define AWE_MAX_PRODUCTS 16
+
+/* A configuration record (Alg. 1 input): weights, planes, reconstruction and bounds. */
+typedef struct awe_encoding_info {
+  int32_t r;                      /* number of FP4 products */
+  int32_t limbs_a, limbs_b;       /* p and q of the cell (p, q) */
+  int32_t planes_a, planes_b;     /* distinct stored planes per side */
+  int32_t log2_D;                 /* reconstruction denominator D = 2^log2_D */
+  int32_t c_a, c_b;               /* largest |stored value| the tables use */
+  int32_t n_g;                    /* most products sharing one accumulator */
+  int32_t modulus;                /* 0 for an exact scheme */
+  int32_t xmin_a, xmax_a;         /* accepted input range, A side */
+  int32_t xmin_b, xmax_b;         /* accepted input range, B side */
+  int32_t coverage_a, coverage_b; /* contiguous half-width of w.a (v.b) over the table's tuples; exact schemes */
+  int32_t w[AWE_MAX_LIMBS];       /* limb weights, A side */
+  int32_t v[AWE_MAX_LIMBS];       /* limb weights, B side */
+  int32_t alpha[AWE_MAX_PLANES][AWE_MAX_LIMBS]; /* A-side plane coefficient vectors */
+  int32_t beta[AWE_MAX_PLANES][AWE_MAX_LIMBS];  /* B-side plane coefficient vectors */
+  int32_t pair_a[AWE_MAX_PRODUCTS];             /* A plane used by product k */
+  int32_t pair_b[AWE_MAX_PRODUCTS];             /* B plane used by product k */
+  int64_t ell[AWE_MAX_PRODUCTS];  /* reconstruction numerators ell_k (mod m: balanced residues) */
+  int32_t group[AWE_MAX_PRODUCTS];/* accumulator shared by product k (equal ell_k) */
+  int64_t k_star;                 /* floor(2^24 / (n_g c_a c_b)), Sec. 3.4 */
+  int64_t k_seg;                  /* default fold segment of the GEMM (<= k_star), multiple of 128 */
+} awe_encoding_info;
+
+/* Host.  The configuration record of an encoding (for AWE_ENC_MOD, of modulus m; the
+   modulus argument is ignored otherwise).  AWE_ERR_UNSUPPORTED when no scheme exists. */
+awe_status awe_get_encoding_info(awe_encoding enc, int32_t modulus, awe_encoding_info* out);
+
+/* Host.  The encoding table (Alg. 1, "decompose each entry by table lookup"): for every
+   input x in [xmin, xmax] of `side`, values[(x - xmin) * planes + p] = stored value of plane p
+   (a doubled integer in S).  n_values must be at least (xmax - xmin + 1) * planes. */
+awe_status awe_get_plane_table(awe_encoding enc, int32_t modulus, awe_side side,
+                               int32_t* values, int64_t n_values);
+
+/* Host.  Bytes of all stored planes of one side for `rows` x K (layout above). */
+awe_status awe_plane_bytes(awe_encoding enc, int32_t modulus, awe_side side,
+                           int64_t rows, int64_t K, size_t* bytes);
+
+/* Encode one operand into its stored planes (Alg. 1, first two loops).
+   side A: x is rows x K, x[i*ld + k];  side B: x is K x rows, x[k*ld + j] (rows = N).
+   x holds int8 (exact encodings; int4 values for the A side of AWE_ENC_AWE4) or uint8
+   residues (AWE_ENC_MOD).  planes receives awe_plane_bytes bytes.  A value outside the
+   encoding's range is stored as 0 and, when d_range_flag is not NULL, sets *d_range_flag
+   to a nonzero value (the flag is never cleared by the library). */
+awe_status awe_encode(awe_encoding enc, int32_t modulus, awe_side side,
+                      const void* x, int64_t rows, int64_t K, int64_t ld,
+                      void* planes, int32_t* d_range_flag, hipStream_t stream);
+
+/* The r FP4 products and the reconstruction on stored planes (Alg. 1, last two steps):
+   C = (sum_k ell_k P_k) / D exactly, or (sum_k lambda_k P_k) mod m in [0, m) for
+   AWE_ENC_MOD (then c_type must be AWE_I32).  planes_a / planes_b come from awe_encode
+   with the same M, N, K.  k_seg: fold segment length (0 = the encoding's default;
+   otherwise a positive multiple of 128 no larger than the default): every FP32 partial
+   covers at most k_seg reduction indices and is then added to an integer accumulator. */
+awe_status awe_gemm_planes(awe_encoding enc, int32_t modulus, int64_t M, int64_t N, int64_t K,
+                           const void* planes_a, const void* planes_b,
+                           void* C, int64_t ldc, awe_dtype c_type, int64_t k_seg,
+                           hipStream_t stream);
+
+/* Host.  Workspace awe_gemm_exact / awe_gemm_mod need (both sides' planes). */
+awe_status awe_workspace_bytes(awe_encoding enc, int32_t modulus, int64_t M, int64_t N,
+                               int64_t K, size_t* bytes);
+
+/* C = A B exactly (Alg. 1 end to end): encode A, encode B, products, reconstruction.
+   enc is one of the exact encodings.  int8 A (int4 values for AWE_ENC_AWE4) and int8 B.
+   c_type AWE_I32 requires max|A| max|B| K <= 2^31 - 1 (else AWE_ERR_OVERFLOW). */
+awe_status awe_gemm_exact(awe_encoding enc, int64_t M, int64_t N, int64_t K,
+                          const int8_t* A, int64_t lda, const int8_t* B, int64_t ldb,
+                          void* C, int64_t ldc, awe_dtype c_type,
+                          void* workspace, size_t ws_bytes, int32_t* d_range_flag,
+                          hipStream_t stream);
+
+/* C = (A B) mod m in [0, m), residue operands in [0, m) as uint8 (Sec. 5.3). */
+awe_status awe_gemm_mod(int32_t m, int64_t M, int64_t N, int64_t K,
+                        const uint8_t* A, int64_t lda, const uint8_t* B, int64_t ldb,
+                        int32_t* C, int64_t ldc,
+                        void* workspace, size_t ws_bytes, int32_t* d_range_flag,
+                        hipStream_t stream);
+
+/* Host.  Static description of a status code. */
+const char* awe_status_string(awe_status s);
+
+/* Host.  Detail of the last error returned on the calling thread ("" if none). */
+const char* awe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AWE_H */

@@ -1,0 +1,318 @@
+// The C ABI (include/awe.h): argument checks on the host, reduction-length
+// splitting, and the launches of the encoder and GEMM kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <string>
+
+#include "awe_internal.h"
+
+namespace awe {
+
+namespace {
+thread_local std::string g_last_error;
+
+awe_status fail(awe_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+int64_t max_abs_input(const Scheme& s, bool sideA) {
+  int32_t lo = sideA ? s.xmin_a : s.xmin_b, hi = sideA ? s.xmax_a : s.xmax_b;
+  return std::max<int64_t>(std::abs((int64_t)lo), std::abs((int64_t)hi));
+}
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+const Scheme* scheme_or_fail(awe_encoding enc, int32_t modulus, awe_status* st) {
+  std::string msg;
+  const Scheme* s = get_scheme(enc, modulus, st, &msg);
+  if (!s) g_last_error = msg;
+  return s;
+}
+
+size_t side_bytes(const Scheme& s, bool sideA, int64_t rows, int64_t K) {
+  return (size_t)(sideA ? s.na : s.nb) * (size_t)plane_stride_bytes(rows, K);
+}
+
+// Largest reduction length (multiple of 128) one GEMM launch may cover so that
+// the int32 accumulator's true value fits: |D C| <= D max|A| max|B| K for an
+// exact scheme, |sum lambda_k P_k| <= sum|lambda_k| c_A c_B K for a congruence.
+int64_t launch_k_limit(const Scheme& s) {
+  const int64_t lim = 0x7fffffffLL;
+  int64_t per_k;
+  if (s.modulus) {
+    int64_t sum = 0;
+    for (int k = 0; k < s.r; ++k) sum += std::abs(s.ell[k]);
+    per_k = sum * s.c_a * s.c_b;
+  } else {
+    per_k = (int64_t(1) << s.log2D) * max_abs_input(s, true) * max_abs_input(s, false);
+  }
+  return std::max<int64_t>(lim / per_k / kKPad * kKPad, kKPad);
+}
+
+awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, const void* pa,
+                            const void* pb, void* C, int64_t ldc, awe_dtype c_type, int64_t k_seg,
+                            hipStream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  if (c_type != AWE_I32 && c_type != AWE_I64) return fail(AWE_ERR_INVALID_VALUE, "bad c_type");
+  if (s.modulus && c_type != AWE_I32) return fail(AWE_ERR_INVALID_VALUE, "residues are written as int32");
+  if (M == 0 || N == 0) return AWE_OK;
+  if (C == nullptr) return fail(AWE_ERR_INVALID_VALUE, "C is NULL");
+  if (ldc < N) return fail(AWE_ERR_INVALID_VALUE, "ldc < N");
+  if (K > 0 && (pa == nullptr || pb == nullptr)) return fail(AWE_ERR_INVALID_VALUE, "planes are NULL");
+  if (M > 0x7fffff00LL || N > 0x7fffff00LL) return fail(AWE_ERR_UNSUPPORTED, "M or N too large");
+  if (round_up(K, kKPad) / kKPad > 0x7fffffffLL) return fail(AWE_ERR_UNSUPPORTED, "K too large");
+  if (!s.modulus && c_type == AWE_I32 &&
+      max_abs_input(s, true) * max_abs_input(s, false) * K > 0x7fffffffLL)
+    return fail(AWE_ERR_OVERFLOW, "int32 C cannot hold max|A| max|B| K");
+  if (k_seg == 0) k_seg = s.k_seg;
+  if (k_seg < 0 || k_seg % kKPad != 0 || k_seg > s.k_seg)
+    return fail(AWE_ERR_INVALID_VALUE,
+                "k_seg must be a positive multiple of 128 no larger than " + std::to_string(s.k_seg));
+
+  GemmLaunch L{};
+  L.planes_a = reinterpret_cast<const uint8_t*>(pa);
+  L.planes_b = reinterpret_cast<const uint8_t*>(pb);
+  L.stride_a = plane_stride_bytes(M, K);
+  L.stride_b = plane_stride_bytes(N, K);
+  L.M = M;
+  L.N = N;
+  L.K = K;
+  L.r = s.r;
+  L.fold_mask = 0;
+  for (int k = 0; k < s.r; ++k) {
+    L.pa[k] = s.pa[k];
+    L.pb[k] = s.pb[k];
+    L.fold_ell[k] = (int32_t)s.ell[k];
+    if (k == s.r - 1 || s.group[k + 1] != s.group[k]) L.fold_mask |= 1u << k;
+  }
+  L.k_seg = k_seg;
+  L.C = C;
+  L.ldc = ldc;
+  L.c_type = c_type;
+  L.log2D = s.log2D;
+  L.modulus = s.modulus;
+  const int64_t kp = round_up(K, kKPad);
+  const int64_t step = launch_k_limit(s);
+  if (kp == 0) {
+    L.k_begin = L.k_end = 0;
+    L.accumulate = false;
+    return launch_gemm(L, stream);
+  }
+  for (int64_t k0 = 0; k0 < kp; k0 += step) {
+    L.k_begin = k0;
+    L.k_end = std::min(kp, k0 + step);
+    L.accumulate = k0 > 0;
+    awe_status st = launch_gemm(L, stream);
+    if (st != AWE_OK) return st;
+  }
+  return AWE_OK;
+}
+
+awe_status encode_impl(const Scheme& s, awe_side side, const void* x, int64_t rows, int64_t K,
+                       int64_t ld, void* planes, int32_t* flag, hipStream_t stream) {
+  if (side != AWE_SIDE_A && side != AWE_SIDE_B) return fail(AWE_ERR_INVALID_VALUE, "bad side");
+  if (rows < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  if (rows == 0 || K == 0) {
+    if (rows > 0 && K == 0) return AWE_OK;  // no bricks: Kp = 0
+    return AWE_OK;
+  }
+  if (x == nullptr || planes == nullptr) return fail(AWE_ERR_INVALID_VALUE, "NULL pointer");
+  const bool sideA = side == AWE_SIDE_A;
+  if (sideA ? ld < K : ld < rows) return fail(AWE_ERR_INVALID_VALUE, "leading dimension too small");
+  EncodeLaunch e{};
+  e.x = x;
+  e.rows = rows;
+  e.K = K;
+  e.ld = ld;
+  e.transposed = !sideA;
+  e.is_unsigned = sideA ? s.a_unsigned : s.b_unsigned;
+  e.nplanes = sideA ? s.na : s.nb;
+  e.planes = reinterpret_cast<uint8_t*>(planes);
+  e.plane_stride = plane_stride_bytes(rows, K);
+  e.flag = flag;
+  e.lut = sideA ? s.lut_a : s.lut_b;
+  return launch_encode(e, stream);
+}
+
+awe_status exact_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                      const void* B, int64_t ldb, void* C, int64_t ldc, awe_dtype c_type,
+                      void* ws, size_t ws_bytes, int32_t* flag, hipStream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  if (M == 0 || N == 0) return AWE_OK;
+  if (K > 0 && (A == nullptr || B == nullptr)) return fail(AWE_ERR_INVALID_VALUE, "A or B is NULL");
+  if (K > 0 && (lda < K || ldb < N)) return fail(AWE_ERR_INVALID_VALUE, "leading dimension too small");
+  if (C == nullptr || ldc < N) return fail(AWE_ERR_INVALID_VALUE, "bad C or ldc");
+  if (c_type != AWE_I32 && c_type != AWE_I64) return fail(AWE_ERR_INVALID_VALUE, "bad c_type");
+  if (!s.modulus && c_type == AWE_I32 &&
+      max_abs_input(s, true) * max_abs_input(s, false) * K > 0x7fffffffLL)
+    return fail(AWE_ERR_OVERFLOW, "int32 C cannot hold max|A| max|B| K");
+  const size_t ba = round_up((int64_t)side_bytes(s, true, M, K), 256);
+  const size_t bb = side_bytes(s, false, N, K);
+  if (ba + bb > 0 && (ws == nullptr || ws_bytes < ba + bb))
+    return fail(AWE_ERR_WORKSPACE, "workspace smaller than awe_workspace_bytes");
+  uint8_t* pa = reinterpret_cast<uint8_t*>(ws);
+  uint8_t* pb = pa + ba;
+  awe_status st = AWE_OK;
+  if (K > 0) {
+    st = encode_impl(s, AWE_SIDE_A, A, M, K, lda, pa, flag, stream);
+    if (st != AWE_OK) return st;
+    st = encode_impl(s, AWE_SIDE_B, B, N, K, ldb, pb, flag, stream);
+    if (st != AWE_OK) return st;
+  }
+  return gemm_planes_impl(s, M, N, K, pa, pb, C, ldc, c_type, 0, stream);
+}
+
+}  // namespace
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+}  // namespace awe
+
+using namespace awe;
+
+extern "C" {
+
+awe_status awe_get_encoding_info(awe_encoding enc, int32_t modulus, awe_encoding_info* out) {
+  if (out == nullptr) return fail(AWE_ERR_INVALID_VALUE, "out is NULL");
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, modulus, &st);
+  if (!s) return st;
+  awe_encoding_info info;
+  std::memset(&info, 0, sizeof(info));
+  info.r = s->r;
+  info.limbs_a = s->p;
+  info.limbs_b = s->q;
+  info.planes_a = s->na;
+  info.planes_b = s->nb;
+  info.log2_D = s->log2D;
+  info.c_a = s->c_a;
+  info.c_b = s->c_b;
+  info.n_g = s->n_g;
+  info.modulus = s->modulus;
+  info.xmin_a = s->xmin_a;
+  info.xmax_a = s->xmax_a;
+  info.xmin_b = s->xmin_b;
+  info.xmax_b = s->xmax_b;
+  info.coverage_a = s->coverage_a;
+  info.coverage_b = s->coverage_b;
+  for (int i = 0; i < AWE_MAX_LIMBS; ++i) {
+    info.w[i] = s->w[i];
+    info.v[i] = s->v[i];
+  }
+  for (int k = 0; k < AWE_MAX_PLANES; ++k)
+    for (int i = 0; i < AWE_MAX_LIMBS; ++i) {
+      info.alpha[k][i] = s->alpha[k][i];
+      info.beta[k][i] = s->beta[k][i];
+    }
+  for (int k = 0; k < s->r; ++k) {
+    info.pair_a[k] = s->pa[k];
+    info.pair_b[k] = s->pb[k];
+    info.ell[k] = s->ell[k];
+    info.group[k] = s->group[k];
+  }
+  info.k_star = s->k_star;
+  info.k_seg = s->k_seg;
+  *out = info;
+  return AWE_OK;
+}
+
+awe_status awe_get_plane_table(awe_encoding enc, int32_t modulus, awe_side side, int32_t* values,
+                               int64_t n_values) {
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, modulus, &st);
+  if (!s) return st;
+  if (side != AWE_SIDE_A && side != AWE_SIDE_B) return fail(AWE_ERR_INVALID_VALUE, "bad side");
+  const bool a = side == AWE_SIDE_A;
+  const int lo = a ? s->xmin_a : s->xmin_b, hi = a ? s->xmax_a : s->xmax_b;
+  const int np = a ? s->na : s->nb;
+  const bool uns = a ? s->a_unsigned : s->b_unsigned;
+  if (values == nullptr || n_values < (int64_t)(hi - lo + 1) * np)
+    return fail(AWE_ERR_INVALID_VALUE, "values too small");
+  for (int x = lo; x <= hi; ++x) {
+    const int b = uns ? x : (int)(uint8_t)(int8_t)x;
+    for (int k = 0; k < np; ++k) values[(int64_t)(x - lo) * np + k] = (a ? s->val_a : s->val_b)[b][k];
+  }
+  return AWE_OK;
+}
+
+awe_status awe_plane_bytes(awe_encoding enc, int32_t modulus, awe_side side, int64_t rows, int64_t K,
+                           size_t* bytes) {
+  if (bytes == nullptr) return fail(AWE_ERR_INVALID_VALUE, "bytes is NULL");
+  if (rows < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  if (side != AWE_SIDE_A && side != AWE_SIDE_B) return fail(AWE_ERR_INVALID_VALUE, "bad side");
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, modulus, &st);
+  if (!s) return st;
+  *bytes = side_bytes(*s, side == AWE_SIDE_A, rows, K);
+  return AWE_OK;
+}
+
+awe_status awe_encode(awe_encoding enc, int32_t modulus, awe_side side, const void* x, int64_t rows,
+                      int64_t K, int64_t ld, void* planes, int32_t* d_range_flag, hipStream_t stream) {
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, modulus, &st);
+  if (!s) return st;
+  return encode_impl(*s, side, x, rows, K, ld, planes, d_range_flag, stream);
+}
+
+awe_status awe_gemm_planes(awe_encoding enc, int32_t modulus, int64_t M, int64_t N, int64_t K,
+                           const void* planes_a, const void* planes_b, void* C, int64_t ldc,
+                           awe_dtype c_type, int64_t k_seg, hipStream_t stream) {
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, modulus, &st);
+  if (!s) return st;
+  return gemm_planes_impl(*s, M, N, K, planes_a, planes_b, C, ldc, c_type, k_seg, stream);
+}
+
+awe_status awe_workspace_bytes(awe_encoding enc, int32_t modulus, int64_t M, int64_t N, int64_t K,
+                               size_t* bytes) {
+  if (bytes == nullptr) return fail(AWE_ERR_INVALID_VALUE, "bytes is NULL");
+  if (M < 0 || N < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, modulus, &st);
+  if (!s) return st;
+  *bytes = (size_t)round_up((int64_t)side_bytes(*s, true, M, K), 256) + side_bytes(*s, false, N, K);
+  return AWE_OK;
+}
+
+awe_status awe_gemm_exact(awe_encoding enc, int64_t M, int64_t N, int64_t K, const int8_t* A,
+                          int64_t lda, const int8_t* B, int64_t ldb, void* C, int64_t ldc,
+                          awe_dtype c_type, void* workspace, size_t ws_bytes, int32_t* d_range_flag,
+                          hipStream_t stream) {
+  if (enc == AWE_ENC_MOD) return fail(AWE_ERR_INVALID_VALUE, "use awe_gemm_mod for residues");
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, 0, &st);
+  if (!s) return st;
+  return exact_impl(*s, M, N, K, A, lda, B, ldb, C, ldc, c_type, workspace, ws_bytes, d_range_flag,
+                    stream);
+}
+
+awe_status awe_gemm_mod(int32_t m, int64_t M, int64_t N, int64_t K, const uint8_t* A, int64_t lda,
+                        const uint8_t* B, int64_t ldb, int32_t* C, int64_t ldc, void* workspace,
+                        size_t ws_bytes, int32_t* d_range_flag, hipStream_t stream) {
+  awe_status st;
+  const Scheme* s = scheme_or_fail(AWE_ENC_MOD, m, &st);
+  if (!s) return st;
+  return exact_impl(*s, M, N, K, A, lda, B, ldb, C, ldc, AWE_I32, workspace, ws_bytes, d_range_flag,
+                    stream);
+}
+
+const char* awe_status_string(awe_status s) {
+  switch (s) {
+    case AWE_OK: return "success";
+    case AWE_ERR_INVALID_VALUE: return "invalid argument";
+    case AWE_ERR_UNSUPPORTED: return "unsupported modulus or size";
+    case AWE_ERR_OVERFLOW: return "int32 output would overflow";
+    case AWE_ERR_WORKSPACE: return "workspace too small";
+    case AWE_ERR_HIP: return "HIP runtime error";
+    case AWE_ERR_TABLE: return "encoding table failed its self-check";
+  }
+  return "unknown status";
+}
+
+const char* awe_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,97 @@
+// Internal declarations shared by the host table code, the kernels and the C ABI.
+#pragma once
+#include <cstdint>
+#include <string>
+
+#include "../../include/awe.h"
+
+namespace awe {
+
+constexpr int kMaxLimbs = AWE_MAX_LIMBS;
+constexpr int kMaxPlanes = AWE_MAX_PLANES;
+constexpr int kMaxProducts = AWE_MAX_PRODUCTS;
+
+// Plane layout constants (the MFMA fragment "brick", see include/awe.h).
+constexpr int kBrickRows = 32;     // rows (A) or columns (B) per brick
+constexpr int kBrickK = 64;        // reduction indices per brick
+constexpr int kBrickBytes = 1024;  // 32 x 64 E2M1 codes, 2 per byte
+constexpr int kKPad = 128;         // the reduction length is padded to this multiple
+
+// LUT entry flag: the input byte is outside the encoding's range.
+constexpr uint32_t kLutInvalid = 0x80000000u;
+
+// One scheme (Definition 4.1 of the paper, or its mod-m congruence form)
+// together with the encoding tables derived from it.
+struct Scheme {
+  awe_encoding enc = AWE_ENC_AWE6;
+  int32_t modulus = 0;  // 0: exact scheme
+  int p = 0, q = 0;     // limbs on the A and B side
+  int32_t w[kMaxLimbs] = {}, v[kMaxLimbs] = {};
+  int na = 0, nb = 0;   // stored planes per side
+  int32_t alpha[kMaxPlanes][kMaxLimbs] = {};
+  int32_t beta[kMaxPlanes][kMaxLimbs] = {};
+  int r = 0;
+  int32_t pa[kMaxProducts] = {}, pb[kMaxProducts] = {};
+  int64_t ell[kMaxProducts] = {};
+  int32_t group[kMaxProducts] = {};  // products with equal ell that share an accumulator
+  int log2D = 0;
+  int cap_a = 12, cap_b = 12;        // bound on |stored value| the tables may use
+  int32_t xmin_a = 0, xmax_a = 0, xmin_b = 0, xmax_b = 0;
+  bool positional13 = false;          // base-13 digits with carries instead of the choice rule
+  bool a_unsigned = false, b_unsigned = false;  // residues arrive as uint8
+
+  // derived by build_tables()
+  int c_a = 0, c_b = 0, n_g = 1;
+  int32_t coverage_a = 0, coverage_b = 0;
+  int64_t k_star = 0, k_seg = 0;
+  int32_t val_a[256][kMaxPlanes] = {};  // plane values per input byte (index: byte value)
+  int32_t val_b[256][kMaxPlanes] = {};
+  uint32_t lut_a[256] = {}, lut_b[256] = {};  // packed E2M1 codes per input byte
+};
+
+// Builds (once, thread-safe) and returns the scheme; nullptr with a message on failure.
+const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std::string* msg);
+
+// E2M1 code of a doubled integer in S (sign bit 3, magnitude code 0..7), or -1.
+int e2m1_code(int s);
+
+// Bytes of one plane of `rows` x `K`.
+int64_t plane_stride_bytes(int64_t rows, int64_t K);
+
+// ---- kernel launchers (awe_kernels.hip) ----
+struct EncodeLaunch {
+  const void* x;
+  int64_t rows, K, ld;
+  bool transposed;  // B side: x[k * ld + row]
+  bool is_unsigned;
+  int nplanes;
+  uint8_t* planes;
+  int64_t plane_stride;
+  int32_t* flag;
+  const uint32_t* lut;  // 256 entries (host memory; passed by value to the kernel)
+};
+awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream);
+
+struct GemmLaunch {
+  const uint8_t* planes_a;
+  const uint8_t* planes_b;
+  int64_t stride_a, stride_b;
+  int64_t M, N, K;
+  int r;
+  int32_t pa[kMaxProducts], pb[kMaxProducts];
+  int32_t fold_ell[kMaxProducts];  // coefficient applied when the accumulator is folded after product k
+  uint32_t fold_mask;              // bit k: fold after product k
+  int64_t k_seg;                   // fold segment length (multiple of kKPad)
+  int64_t k_begin, k_end;          // reduction range of this launch (multiples of kKPad)
+  void* C;
+  int64_t ldc;
+  awe_dtype c_type;
+  bool accumulate;
+  int log2D;
+  int32_t modulus;
+};
+awe_status launch_gemm(const GemmLaunch& g, hipStream_t stream);
+
+void set_error(const std::string& msg);
+
+}  // namespace awe

@@ -1,0 +1,396 @@
+// HIP kernels for gfx950: the plane encoder and the multi-plane FP4 GEMM with
+// its fused integer reconstruction (Alg. 1 of the paper).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "awe_internal.h"
+
+namespace awe {
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+struct LutArg {
+  uint32_t v[256];
+};
+
+// ---------------------------------------------------------------------------
+// Encoder (Alg. 1, table lookup and plane formation).  One wave per 1 KiB
+// brick: lane L = 32 h + t turns the 32 inputs of row rb*32 + t at reduction
+// indices ks*64 + 32 h + j into one 16-byte fragment per stored plane.  The
+// plane values (combinations of limbs included) come from one 256-entry table
+// of packed E2M1 codes, so forming a combination plane costs nothing here.
+// ---------------------------------------------------------------------------
+template <bool kTransposed>
+__global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__ x, int64_t rows,
+                                                     int64_t K, int64_t ld, int64_t KS,
+                                                     int64_t nbricks, int nplanes,
+                                                     uint8_t* __restrict__ planes,
+                                                     int64_t plane_stride, int32_t* flag,
+                                                     LutArg lut) {
+  __shared__ uint32_t slut[256];
+  slut[threadIdx.x] = lut.v[threadIdx.x];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int64_t brick = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (brick >= nbricks) return;
+  const int64_t rb = brick / KS, ks = brick - rb * KS;
+  const int64_t row = rb * kBrickRows + (lane & 31);
+  const int64_t k0 = ks * kBrickK + (lane >> 5) * 32;
+  const bool row_ok = row < rows;
+
+  uint32_t e[32];
+  if (!kTransposed) {
+    const uint8_t* src = x + row * ld + k0;
+    if (row_ok && k0 + 32 <= K && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+      const uint4 lo = *reinterpret_cast<const uint4*>(src);
+      const uint4 hi = *reinterpret_cast<const uint4*>(src + 16);
+      const uint32_t w[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+      for (int j = 0; j < 32; ++j) e[j] = slut[(w[j >> 2] >> (8 * (j & 3))) & 0xff];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? slut[src[j]] : 0u;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? slut[x[(k0 + j) * ld + row]] : 0u;
+  }
+  uint32_t bad = 0;
+#pragma unroll
+  for (int j = 0; j < 32; ++j) bad |= e[j];
+  if ((bad & kLutInvalid) && flag != nullptr) atomicOr(flag, 1);
+
+  uint8_t* dst = planes + brick * kBrickBytes + lane * 16;
+  for (int p = 0; p < nplanes; ++p) {
+    uint32_t d[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 32; ++j) d[j >> 3] |= ((e[j] >> (4 * p)) & 0xfu) << (4 * (j & 7));
+    *reinterpret_cast<uint4*>(dst + p * plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Multi-plane FP4 GEMM (Alg. 1, the r products and the reconstruction).
+//
+// Tile 256 x 128 of C per workgroup of 4 waves; each wave owns 128 x 64 as
+// 4 x 2 blocks of the 32x32x64 scaled FP4 MFMA.  The reduction runs as one
+// stream of k-tiles (128 indices = 2 bricks per row block) in the order
+// segment -> product -> k-tile: a wave accumulates one product in FP32 for a
+// whole fold segment, then folds that partial into an int32 accumulator with
+// its reconstruction coefficient (cvt + 24-bit multiply-add) and restarts the
+// FP32 accumulator.  Every FP32 partial is an exact integer below 2^23 by the
+// segment length (Sec. 3.4 with a factor 2 of margin for the 24-bit multiply),
+// and the int32 sum is exact modulo 2^32; the host splits the reduction into
+// launches so that the true value of each launch fits in int32.
+//
+// Both E8M0 block scales are 2^1 (byte 128): the stored E2M1 values are s/2
+// for the doubled integers s of S, so each product of codes is s_a s_b
+// exactly and the FP32 accumulators hold the integer plane products.
+// ---------------------------------------------------------------------------
+constexpr int BM = 256, BN = 128;
+constexpr int A_BRICKS = (BM / kBrickRows) * 2;  // per stage: 8 row blocks x 2 k-steps
+constexpr int B_BRICKS = (BN / kBrickRows) * 2;
+constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * kBrickBytes;  // 24 KiB
+constexpr int BRICKS_PER_WAVE = (A_BRICKS + B_BRICKS) / 4;        // 6
+constexpr int NSTAGE = 4;                                         // LDS ring depth
+constexpr int GEMM_LDS_BYTES = NSTAGE * STAGE_BYTES;
+constexpr uint32_t kScale2 = 0x80808080u;                         // E8M0 2^1 in every byte
+
+struct GemmArgs {
+  const uint8_t* pa;
+  const uint8_t* pb;
+  int64_t stride_a, stride_b;
+  int32_t rba, rbb;  // row blocks of the A and B planes
+  int32_t KS;        // bricks along K per row block
+  int32_t t_begin, t_end;
+  int32_t ts;        // fold segment in k-tiles
+  int32_t r;
+  int32_t pidx_a[kMaxProducts], pidx_b[kMaxProducts];
+  int32_t fold_ell[kMaxProducts];
+  uint32_t fold_mask;
+  void* C;
+  int64_t ldc;
+  int32_t M, N;
+  int32_t c64, accumulate, log2D, modulus;
+  int32_t tiles_n;
+};
+
+// Position in the reduction stream: product p, k-tile t, current fold segment [cs, ce).
+struct Cursor {
+  int p, t, cs, ce;
+};
+
+__device__ __forceinline__ void cursor_next(Cursor& c, const GemmArgs& g) {
+  if (++c.t == c.ce) {
+    c.t = c.cs;
+    if (++c.p == g.r) {
+      c.p = 0;
+      c.cs = c.ce;
+      c.ce = min(c.cs + g.ts, g.t_end);
+      c.t = c.cs;
+    }
+  }
+}
+
+// One 16-byte-per-lane global -> LDS copy: the wave's 64 lanes fill the 1 KiB
+// at LDS byte address `lds` (wave-uniform, in M0) from their own global
+// addresses.  Issued as inline assembly so that the compiler does not
+// serialise the copies; completion is awaited explicitly with vmcnt.
+__device__ __forceinline__ void dma_brick(const uint8_t* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds)
+               : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
+                                           int tm, int tn, int wave, int lane) {
+  const uint8_t* pa = g.pa + (int64_t)g.pidx_a[c.p] * g.stride_a;
+  const uint8_t* pb = g.pb + (int64_t)g.pidx_b[c.p] * g.stride_b;
+#pragma unroll
+  for (int i = 0; i < BRICKS_PER_WAVE; ++i) {
+    const int id = wave * BRICKS_PER_WAVE + i;  // wave-uniform
+    const uint8_t* src;
+    if (id < A_BRICKS) {
+      const int rb = min(tm * (BM / kBrickRows) + (id >> 1), g.rba - 1);
+      src = pa + ((int64_t)rb * g.KS + c.t * 2 + (id & 1)) * kBrickBytes;
+    } else {
+      const int idb = id - A_BRICKS;
+      const int cb = min(tn * (BN / kBrickRows) + (idb >> 1), g.rbb - 1);
+      src = pb + ((int64_t)cb * g.KS + c.t * 2 + (idb & 1)) * kBrickBytes;
+    }
+    dma_brick(src + lane * 16, stage_lds + id * kBrickBytes);
+  }
+}
+
+__device__ __forceinline__ v8i frag(const uint8_t* p) {
+  const int4 x = *reinterpret_cast<const int4*>(p);
+  v8i v = {x.x, x.y, x.z, x.w, 0, 0, 0, 0};
+  return v;
+}
+
+__device__ __forceinline__ void compute_stage(const uint8_t* stage, int wm, int wn, int lane,
+                                              v16f (&acc)[4][2]) {
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    v8i a[4], b[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = frag(stage + ((wm * 4 + i) * 2 + ks) * kBrickBytes + lane * 16);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      b[j] = frag(stage + (A_BRICKS + (wn * 2 + j) * 2 + ks) * kBrickBytes + lane * 16);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[i], b[j], acc[i][j], 4, 4, 0,
+                                                                     kScale2, 0, kScale2);
+  }
+}
+
+__global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x - (blockIdx.x / g.tiles_n) * g.tiles_n;
+  const int wm = wave >> 1, wn = wave & 1;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+
+  v16f acc[4][2];
+  int32_t iacc[4][2][16];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        acc[i][j][v] = 0.0f;
+        iacc[i][j][v] = 0;
+      }
+
+  const int nt = g.t_end - g.t_begin;
+  const int S = g.r * nt;
+  Cursor cur{0, g.t_begin, g.t_begin, min(g.t_begin + g.ts, g.t_end)};
+  Cursor nxt = cur;
+  // prologue: stages 0 .. NSTAGE-2 in flight
+#pragma unroll
+  for (int i = 0; i < NSTAGE - 1; ++i) {
+    if (i < S) {
+      load_stage(g, nxt, lds0 + i * STAGE_BYTES, tm, tn, wave, lane);
+      cursor_next(nxt, g);
+    }
+  }
+  int buf = 0;
+  for (int s = 0; s < S; ++s) {
+    // stage s has landed once at most the NSTAGE-2 younger stages are outstanding
+    if (s + NSTAGE - 2 < S)
+      wait_vmcnt<BRICKS_PER_WAVE * (NSTAGE - 2)>();
+    else
+      wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();  // every wave's copies of stage s are visible; stage s-1 is consumed
+    if (s + NSTAGE - 1 < S) {
+      int nb = buf + NSTAGE - 1;
+      if (nb >= NSTAGE) nb -= NSTAGE;
+      load_stage(g, nxt, lds0 + nb * STAGE_BYTES, tm, tn, wave, lane);
+      cursor_next(nxt, g);
+    }
+    compute_stage(smem + buf * STAGE_BYTES, wm, wn, lane, acc);
+    if (cur.t == cur.ce - 1 && ((g.fold_mask >> cur.p) & 1u)) {
+      const int32_t l = g.fold_ell[cur.p];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
+            acc[i][j][v] = 0.0f;
+          }
+    }
+    cursor_next(cur, g);
+    if (++buf == NSTAGE) buf = 0;
+  }
+
+  // Epilogue: exact shift by log2 D, or the non-negative residue mod m.
+  const int row0 = tm * BM + wm * 128 + 4 * (lane >> 5);
+  const int col0 = tn * BN + wn * 64 + (lane & 31);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
+        const int col = col0 + j * 32;
+        if (row >= g.M || col >= g.N) continue;
+        const int64_t off = (int64_t)row * g.ldc + col;
+        int32_t val = iacc[i][j][v];
+        if (g.modulus) {
+          const int32_t m = g.modulus;
+          int32_t rr = val % m;
+          if (rr < 0) rr += m;
+          int32_t* C = reinterpret_cast<int32_t*>(g.C);
+          if (g.accumulate) rr = (C[off] + rr) % m;
+          C[off] = rr;
+        } else {
+          val >>= g.log2D;
+          if (g.c64) {
+            int64_t* C = reinterpret_cast<int64_t*>(g.C);
+            C[off] = g.accumulate ? C[off] + (int64_t)val : (int64_t)val;
+          } else {
+            int32_t* C = reinterpret_cast<int32_t*>(g.C);
+            C[off] = g.accumulate ? (int32_t)((uint32_t)C[off] + (uint32_t)val) : val;
+          }
+        }
+      }
+}
+
+__global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
+  const int64_t total = rows * row_bytes;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / row_bytes, c = i - r * row_bytes;
+    C[r * ld_bytes + c] = 0;
+  }
+}
+
+}  // namespace
+
+awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
+  const int64_t rb = (e.rows + kBrickRows - 1) / kBrickRows;
+  const int64_t kp = (e.K + kKPad - 1) / kKPad * kKPad;
+  const int64_t KS = kp / kBrickK;
+  const int64_t nbricks = rb * KS;
+  if (nbricks == 0) return AWE_OK;
+  LutArg lut;
+  for (int i = 0; i < 256; ++i) lut.v[i] = e.lut[i];
+  const int64_t blocks = (nbricks + 3) / 4;
+  if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;
+  if (e.transposed)
+    hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, nbricks,
+                       e.nplanes, e.planes, e.plane_stride, e.flag, lut);
+  else
+    hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, nbricks,
+                       e.nplanes, e.planes, e.plane_stride, e.flag, lut);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) {
+    set_error(std::string("encode launch: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  return AWE_OK;
+}
+
+awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
+  if (L.M == 0 || L.N == 0) return AWE_OK;
+  const int64_t esize = L.c_type == AWE_I64 ? 8 : 4;
+  if (L.k_end <= L.k_begin) {
+    if (L.accumulate) return AWE_OK;
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(1024), dim3(256), 0, stream,
+                       reinterpret_cast<uint8_t*>(L.C), L.M, L.N * esize, L.ldc * esize);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) {
+      set_error(std::string("fill launch: ") + hipGetErrorString(err));
+      return AWE_ERR_HIP;
+    }
+    return AWE_OK;
+  }
+  GemmArgs g{};
+  g.pa = L.planes_a;
+  g.pb = L.planes_b;
+  g.stride_a = L.stride_a;
+  g.stride_b = L.stride_b;
+  g.rba = (int32_t)((L.M + kBrickRows - 1) / kBrickRows);
+  g.rbb = (int32_t)((L.N + kBrickRows - 1) / kBrickRows);
+  const int64_t kp = (L.K + kKPad - 1) / kKPad * kKPad;
+  g.KS = (int32_t)(kp / kBrickK);
+  g.t_begin = (int32_t)(L.k_begin / kKPad);
+  g.t_end = (int32_t)(L.k_end / kKPad);
+  g.ts = (int32_t)(L.k_seg / kKPad);
+  g.r = L.r;
+  for (int k = 0; k < L.r; ++k) {
+    g.pidx_a[k] = L.pa[k];
+    g.pidx_b[k] = L.pb[k];
+    g.fold_ell[k] = L.fold_ell[k];
+  }
+  g.fold_mask = L.fold_mask;
+  g.C = L.C;
+  g.ldc = L.ldc;
+  g.M = (int32_t)L.M;
+  g.N = (int32_t)L.N;
+  g.c64 = L.c_type == AWE_I64;
+  g.accumulate = L.accumulate;
+  g.log2D = L.log2D;
+  g.modulus = L.modulus;
+  const int64_t tiles_m = (L.M + BM - 1) / BM, tiles_n = (L.N + BN - 1) / BN;
+  g.tiles_n = (int32_t)tiles_n;
+  const int64_t blocks = tiles_m * tiles_n;
+  if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, GEMM_LDS_BYTES);
+    if (e != hipSuccess) {
+      set_error(std::string("gemm LDS attribute: ") + hipGetErrorString(e));
+      return AWE_ERR_HIP;
+    }
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(gemm_kernel, dim3((unsigned)blocks), dim3(256), GEMM_LDS_BYTES, stream, g);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) {
+    set_error(std::string("gemm launch: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  return AWE_OK;
+}
+
+}  // namespace awe

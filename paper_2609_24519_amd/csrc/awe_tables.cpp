@@ -1,0 +1,514 @@
+// Host-side encoding tables: the schemes of the paper, the limb-tuple choice,
+// the packed E2M1 lookup tables the encoder kernel uses, and a self-check of
+// every table before it is used (the verifier of Sec. 4.7 applied to the
+// tables actually shipped to the GPU).
+#include <algorithm>
+#include <climits>
+#include <cstdio>
+#include <cstdlib>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <numeric>
+#include <tuple>
+#include <vector>
+
+#include "awe_internal.h"
+
+namespace awe {
+namespace {
+
+// Sec. 3.1: the doubled E2M1 values.
+constexpr int kS[15] = {0, 1, -1, 2, -2, 3, -3, 4, -4, 6, -6, 8, -8, 12, -12};
+constexpr int kMag[8] = {0, 1, 2, 3, 4, 6, 8, 12};
+
+bool in_S(int x) {
+  for (int s : kS)
+    if (s == x) return true;
+  return false;
+}
+
+int64_t pmod(int64_t x, int64_t m) {
+  int64_t r = x % m;
+  return r < 0 ? r + m : r;
+}
+
+int64_t balanced(int64_t x, int64_t m) {
+  int64_t r = pmod(x, m);
+  return r > m / 2 ? r - m : r;
+}
+
+void set_plane(int32_t (&pl)[kMaxPlanes][kMaxLimbs], int k, std::initializer_list<int> c) {
+  int i = 0;
+  for (int x : c) pl[k][i++] = x;
+}
+
+// ---- scheme definitions -------------------------------------------------
+// INT8 x INT8 in 6 products (Sec. 4.3, App. A): planes a0, a1, a2, a0+a1,
+// a0+a2, a1+a2 on both sides, product k pairs plane k with plane k.
+void define_awe6(Scheme& s, bool alt) {
+  s.p = s.q = 3;
+  const int32_t w0[3] = {1, 29, 37}, w1[3] = {1, 11, 39};
+  const int64_t l0[6] = {-65, -261, 259, 29, 37, 1073};
+  const int64_t l1[6] = {-49, -319, 1053, 11, 39, 429};
+  for (int i = 0; i < 3; ++i) s.w[i] = s.v[i] = alt ? w1[i] : w0[i];
+  s.na = s.nb = 6;
+  const int comb[6][3] = {{1, 0, 0}, {0, 1, 0}, {0, 0, 1}, {1, 1, 0}, {1, 0, 1}, {0, 1, 1}};
+  for (int k = 0; k < 6; ++k)
+    for (int i = 0; i < 3; ++i) s.alpha[k][i] = s.beta[k][i] = comb[k][i];
+  s.r = 6;
+  for (int k = 0; k < 6; ++k) {
+    s.pa[k] = s.pb[k] = k;
+    s.ell[k] = alt ? l1[k] : l0[k];
+  }
+  // App. A: capping every stored value at 6 keeps coverage 148 for (1, 29, 37);
+  // the (1, 11, 39) solution needs the full set for its coverage 134.
+  s.cap_a = s.cap_b = alt ? 12 : 6;
+  s.xmin_a = s.xmin_b = -128;
+  s.xmax_a = s.xmax_b = 127;
+}
+
+// INT4 x INT8 in 4 products (App. A).
+void define_awe4(Scheme& s) {
+  s.p = 2;
+  s.q = 3;
+  s.w[0] = 3; s.w[1] = 5;
+  s.v[0] = 5; s.v[1] = 3; s.v[2] = 42;
+  s.na = s.nb = 4;
+  set_plane(s.alpha, 0, {0, 1});
+  set_plane(s.alpha, 1, {1, 0});
+  set_plane(s.alpha, 2, {1, 2});
+  set_plane(s.alpha, 3, {2, 1});
+  set_plane(s.beta, 0, {1, 0, 0});
+  set_plane(s.beta, 1, {0, 1, -1});
+  set_plane(s.beta, 2, {0, 0, 1});
+  set_plane(s.beta, 3, {1, 2, 0});
+  s.r = 4;
+  const int64_t l[4] = {35, -42, 210, 15};
+  for (int k = 0; k < 4; ++k) {
+    s.pa[k] = s.pb[k] = k;
+    s.ell[k] = l[k];
+  }
+  s.log2D = 1;
+  s.cap_a = 3;
+  s.cap_b = 8;
+  s.xmin_a = -8; s.xmax_a = 7;
+  s.xmin_b = -128; s.xmax_b = 127;
+}
+
+// Base-13 positional limbs (Sec. 3.2), all 9 limb pairs, ordered so that the
+// pairs with equal coefficient 13^(i+j) are adjacent and share an accumulator.
+void define_b13(Scheme& s) {
+  s.p = s.q = 3;
+  s.w[0] = s.v[0] = 1; s.w[1] = s.v[1] = 13; s.w[2] = s.v[2] = 169;
+  s.na = s.nb = 3;
+  for (int k = 0; k < 3; ++k) s.alpha[k][k] = s.beta[k][k] = 1;
+  s.r = 0;
+  int64_t pw = 1;
+  for (int d = 0; d <= 4; ++d, pw *= 13)
+    for (int i = 0; i < 3; ++i) {
+      int j = d - i;
+      if (j < 0 || j > 2) continue;
+      s.pa[s.r] = i;
+      s.pb[s.r] = j;
+      s.ell[s.r] = pw;
+      ++s.r;
+    }
+  s.positional13 = true;
+  s.cap_a = s.cap_b = 12;
+  s.xmin_a = s.xmin_b = -128;
+  s.xmax_a = s.xmax_b = 127;
+}
+
+// ---- limb tuples ----------------------------------------------------------
+struct Tuple {
+  int a[kMaxLimbs];
+};
+
+int plane_value(const int32_t* c, const int* a, int p) {
+  int x = 0;
+  for (int i = 0; i < p; ++i) x += c[i] * a[i];
+  return x;
+}
+
+// Enumerate S^p; call f(a) for every tuple whose plane values all lie in S
+// within |cap| (the admissible tuples of Definition 4.1 under a cap).
+template <class F>
+void for_admissible(int p, const int32_t (*planes)[kMaxLimbs], int nplanes, int cap, F f) {
+  int idx[kMaxLimbs] = {0, 0, 0, 0};
+  int a[kMaxLimbs] = {0, 0, 0, 0};
+  for (;;) {
+    for (int i = 0; i < p; ++i) a[i] = kS[idx[i]];
+    bool ok = true;
+    for (int k = 0; k < nplanes && ok; ++k) {
+      int x = plane_value(planes[k], a, p);
+      ok = in_S(x) && std::abs(x) <= cap;
+    }
+    if (ok) f(a);
+    int i = 0;
+    while (i < p && ++idx[i] == 15) idx[i++] = 0;
+    if (i == p) break;
+  }
+}
+
+// Choice among several admissible tuples for one input (the paper leaves it to
+// "table lookup"): smallest largest |plane value|, then smallest sum of |limb|,
+// then the limb tuple read from the top limb down, ascending.
+bool better(const int* a, const int* b, int p, const int32_t (*planes)[kMaxLimbs], int nplanes) {
+  int ma = 0, mb = 0, sa = 0, sb = 0;
+  for (int k = 0; k < nplanes; ++k) {
+    ma = std::max(ma, std::abs(plane_value(planes[k], a, p)));
+    mb = std::max(mb, std::abs(plane_value(planes[k], b, p)));
+  }
+  if (ma != mb) return ma < mb;
+  for (int i = 0; i < p; ++i) {
+    sa += std::abs(a[i]);
+    sb += std::abs(b[i]);
+  }
+  if (sa != sb) return sa < sb;
+  for (int i = p - 1; i >= 0; --i)
+    if (a[i] != b[i]) return a[i] < b[i];
+  return false;
+}
+
+// Least-magnitude element of S in each residue class mod 13 (S holds a full
+// residue system mod 13, Sec. 3.2).
+void base13_digits(int x, int* out) {
+  int rep[13];
+  for (int r = 0; r < 13; ++r) rep[r] = INT_MAX;
+  for (int s : kS) {
+    int r = (int)pmod(s, 13);
+    if (rep[r] == INT_MAX || std::abs(s) < std::abs(rep[r])) rep[r] = s;
+  }
+  for (int i = 0; i < 3; ++i) {
+    int d = rep[pmod(x, 13)];
+    out[i] = d;
+    x = (x - d) / 13;
+  }
+  if (x != 0) out[0] = INT_MAX;  // not representable in 3 limbs (never for int8)
+}
+
+// Builds the limb table of one side: for every input byte, the chosen limbs.
+// Returns false with a message if an input of the range has no tuple.
+bool build_side(Scheme& s, bool sideA, std::string* msg) {
+  const int p = sideA ? s.p : s.q;
+  const int np = sideA ? s.na : s.nb;
+  const int32_t* wts = sideA ? s.w : s.v;
+  const int32_t(*planes)[kMaxLimbs] = sideA ? s.alpha : s.beta;
+  const int cap = sideA ? s.cap_a : s.cap_b;
+  const int xmin = sideA ? s.xmin_a : s.xmin_b;
+  const int xmax = sideA ? s.xmax_a : s.xmax_b;
+  const bool uns = sideA ? s.a_unsigned : s.b_unsigned;
+  int32_t(*val)[kMaxPlanes] = sideA ? s.val_a : s.val_b;
+  uint32_t* lut = sideA ? s.lut_a : s.lut_b;
+  const int nx = xmax - xmin + 1;
+
+  std::vector<Tuple> best(nx);
+  std::vector<char> have(nx, 0);
+  std::vector<char> hit(4096, 0);  // values of w.a seen (exact schemes; for the coverage)
+  if (s.modulus == 0) {
+    // values of w.a over the admissible tuples, for the coverage (Sec. 4.2)
+    for_admissible(p, planes, np, cap, [&](const int* a) {
+      int64_t x = 0;
+      for (int i = 0; i < p; ++i) x += (int64_t)wts[i] * a[i];
+      if (x >= -2047 && x <= 2048) hit[x + 2047] = 1;
+    });
+    int X = 0;
+    while (X < 2047 && hit[X + 1 + 2047] && hit[-(X + 1) + 2047]) ++X;
+    (sideA ? s.coverage_a : s.coverage_b) = X;
+  }
+  if (s.positional13) {
+    for (int x = xmin; x <= xmax; ++x) {
+      int d[3];
+      base13_digits(x, d);
+      if (d[0] == INT_MAX) continue;
+      Tuple t{};
+      for (int i = 0; i < 3; ++i) t.a[i] = d[i];
+      best[x - xmin] = t;
+      have[x - xmin] = 1;
+    }
+  } else {
+    for_admissible(p, planes, np, cap, [&](const int* a) {
+      int64_t x = 0;
+      for (int i = 0; i < p; ++i) x += (int64_t)wts[i] * a[i];
+      if (s.modulus) x = pmod(x, s.modulus);
+      if (x < xmin || x > xmax) return;
+      int ix = (int)x - xmin;
+      if (!have[ix] || better(a, best[ix].a, p, planes, np)) {
+        for (int i = 0; i < kMaxLimbs; ++i) best[ix].a[i] = i < p ? a[i] : 0;
+        have[ix] = 1;
+      }
+    });
+  }
+  for (int ix = 0; ix < nx; ++ix)
+    if (!have[ix]) {
+      *msg = "encoding table misses input " + std::to_string(ix + xmin);
+      return false;
+    }
+
+  int cmax = 0;
+  for (int b = 0; b < 256; ++b) {
+    int x = uns ? b : (int)(int8_t)(uint8_t)b;
+    for (int k = 0; k < kMaxPlanes; ++k) val[b][k] = 0;
+    if (x < xmin || x > xmax) {
+      lut[b] = kLutInvalid;
+      continue;
+    }
+    const int* a = best[x - xmin].a;
+    uint32_t packed = 0;
+    for (int k = 0; k < np; ++k) {
+      int pv = plane_value(planes[k], a, p);
+      val[b][k] = pv;
+      cmax = std::max(cmax, std::abs(pv));
+      int code = e2m1_code(pv);
+      if (code < 0 || std::abs(pv) > cap) {
+        *msg = "stored value outside S or above the cap";
+        return false;
+      }
+      packed |= (uint32_t)code << (4 * k);
+    }
+    // round trip: the limbs reproduce the input (Sec. 3.2), or its residue (Sec. 5.3)
+    int64_t back = 0;
+    for (int i = 0; i < p; ++i) {
+      if (!in_S(a[i])) {
+        *msg = "limb outside S";
+        return false;
+      }
+      back += (int64_t)wts[i] * a[i];
+    }
+    if (s.modulus ? pmod(back - x, s.modulus) != 0 : back != x) {
+      *msg = "limb table does not reproduce its input";
+      return false;
+    }
+    lut[b] = packed;
+  }
+  (sideA ? s.c_a : s.c_b) = cmax;
+  return true;
+}
+
+// Definition 4.1 identity (or its congruence) on every pair of table inputs.
+bool check_identity(const Scheme& s, std::string* msg) {
+  for (int ba = 0; ba < 256; ++ba) {
+    if (s.lut_a[ba] & kLutInvalid) continue;
+    int x = s.a_unsigned ? ba : (int)(int8_t)(uint8_t)ba;
+    for (int bb = 0; bb < 256; ++bb) {
+      if (s.lut_b[bb] & kLutInvalid) continue;
+      int y = s.b_unsigned ? bb : (int)(int8_t)(uint8_t)bb;
+      int64_t acc = 0;
+      for (int k = 0; k < s.r; ++k) acc += s.ell[k] * s.val_a[ba][s.pa[k]] * s.val_b[bb][s.pb[k]];
+      bool ok = s.modulus ? pmod(acc - (int64_t)x * y, s.modulus) == 0
+                          : acc == ((int64_t)x * y) * (int64_t(1) << s.log2D);
+      if (!ok) {
+        *msg = "scheme identity fails at x=" + std::to_string(x) + " y=" + std::to_string(y);
+        return false;
+      }
+    }
+  }
+  return true;
+}
+
+void derive_bounds(Scheme& s) {
+  // products with equal coefficients that are adjacent share one accumulator (n_g, Sec. 3.4)
+  int g = -1, run = 0;
+  s.n_g = 1;
+  for (int k = 0; k < s.r; ++k) {
+    if (k == 0 || s.ell[k] != s.ell[k - 1]) {
+      ++g;
+      run = 0;
+    }
+    s.group[k] = g;
+    s.n_g = std::max(s.n_g, ++run);
+  }
+  const int64_t denom = (int64_t)s.n_g * s.c_a * s.c_b;
+  s.k_star = (int64_t(1) << 24) / denom;
+  // The fold multiplies each FP32 partial by its coefficient with a signed
+  // 24-bit multiply, so a partial must stay within 2^23 - 1 in magnitude.
+  int64_t seg = ((int64_t(1) << 23) - 1) / denom;
+  s.k_seg = seg / kKPad * kKPad;
+}
+
+bool finish(Scheme& s, std::string* msg) {
+  if (!build_side(s, true, msg) || !build_side(s, false, msg)) return false;
+  if (!check_identity(s, msg)) return false;
+  derive_bounds(s);
+  if (s.k_seg < kKPad) {
+    *msg = "fold segment below one k-tile";
+    return false;
+  }
+  return true;
+}
+
+// ---- mod-m schemes (Sec. 5.3) ----------------------------------------------
+bool residues_cover(int m, int W, int pp, int uu) {
+  std::vector<char> seen(m, 0);
+  int count = 0;
+  for (int a0 : kS)
+    for (int a1 : kS) {
+      if (pp != 0 && !in_S(pp * a0 + uu * a1)) continue;
+      int r = (int)pmod(a0 + (int64_t)W * a1, m);
+      if (!seen[r]) {
+        seen[r] = 1;
+        ++count;
+      }
+    }
+  return count == m;
+}
+
+int64_t inv_mod(int64_t a, int64_t m) {
+  int64_t t = 0, nt = 1, r = m, nr = pmod(a, m);
+  while (nr) {
+    int64_t q = r / nr;
+    std::tie(t, nt) = std::make_pair(nt, t - q * nt);
+    std::tie(r, nr) = std::make_pair(nr, r - q * nr);
+  }
+  return r == 1 ? pmod(t, m) : -1;
+}
+
+// Families, tried in order: one limb (S a complete residue system mod m);
+// one Karatsuba-type step with the plane p a0 + u a1 on both sides; two limbs
+// with all four pairs.  Weights w = v = (1, W), W as small as possible.
+bool define_mod(Scheme& s, int m, std::string* msg) {
+  s.modulus = m;
+  s.a_unsigned = s.b_unsigned = true;
+  s.xmin_a = s.xmin_b = 0;
+  s.xmax_a = s.xmax_b = m - 1;
+  s.cap_a = s.cap_b = 12;
+  {
+    std::vector<char> seen(m, 0);
+    int count = 0;
+    for (int x : kS)
+      if (!seen[pmod(x, m)]) {
+        seen[pmod(x, m)] = 1;
+        ++count;
+      }
+    if (count == m) {
+      s.p = s.q = 1;
+      s.w[0] = s.v[0] = 1;
+      s.na = s.nb = 1;
+      s.alpha[0][0] = s.beta[0][0] = 1;
+      s.r = 1;
+      s.ell[0] = 1;
+      return true;
+    }
+  }
+  static const int kPlanes[6][2] = {{1, 1}, {1, -1}, {1, 2}, {1, -2}, {2, 1}, {2, -1}};
+  for (const auto& pu : kPlanes) {
+    const int pp = pu[0], uu = pu[1];
+    int64_t inv = inv_mod(pp * uu, m);
+    if (inv < 0) continue;
+    for (int W = 2; W < m; ++W) {
+      if (!residues_cover(m, W, pp, uu)) continue;
+      // coefficients of a0b0, a0b1 + a1b0 and a1b1 matched modulo m
+      int64_t t = pmod((int64_t)W * inv, m);
+      s.p = s.q = 2;
+      s.w[0] = s.v[0] = 1;
+      s.w[1] = s.v[1] = W;
+      s.na = s.nb = 3;
+      set_plane(s.alpha, 0, {1, 0});
+      set_plane(s.alpha, 1, {0, 1});
+      set_plane(s.alpha, 2, {pp, uu});
+      for (int k = 0; k < 3; ++k)
+        for (int i = 0; i < 2; ++i) s.beta[k][i] = s.alpha[k][i];
+      s.r = 3;
+      for (int k = 0; k < 3; ++k) s.pa[k] = s.pb[k] = k;
+      s.ell[0] = balanced(1 - t * pp * pp, m);
+      s.ell[1] = balanced((int64_t)W * W - t * uu * uu, m);
+      s.ell[2] = balanced(t, m);
+      return true;
+    }
+  }
+  for (int W = 2; W < m; ++W) {
+    if (!residues_cover(m, W, 0, 0)) continue;
+    s.p = s.q = 2;
+    s.w[0] = s.v[0] = 1;
+    s.w[1] = s.v[1] = W;
+    s.na = s.nb = 2;
+    set_plane(s.alpha, 0, {1, 0});
+    set_plane(s.alpha, 1, {0, 1});
+    set_plane(s.beta, 0, {1, 0});
+    set_plane(s.beta, 1, {0, 1});
+    s.r = 4;
+    const int pr[4][2] = {{0, 0}, {0, 1}, {1, 0}, {1, 1}};
+    for (int k = 0; k < 4; ++k) {
+      s.pa[k] = pr[k][0];
+      s.pb[k] = pr[k][1];
+    }
+    s.ell[0] = balanced(1, m);
+    s.ell[1] = s.ell[2] = balanced(W, m);
+    s.ell[3] = balanced((int64_t)W * W, m);
+    return true;
+  }
+  *msg = "no single, Karatsuba-type or two-limb scheme for modulus " + std::to_string(m);
+  return false;
+}
+
+std::mutex g_mu;
+std::map<std::pair<int, int>, std::unique_ptr<Scheme>> g_cache;
+std::map<std::pair<int, int>, std::string> g_fail;
+
+}  // namespace
+
+int e2m1_code(int s) {
+  int a = std::abs(s);
+  for (int i = 0; i < 8; ++i)
+    if (kMag[i] == a) return (s < 0 ? 8 : 0) | i;
+  return -1;
+}
+
+int64_t plane_stride_bytes(int64_t rows, int64_t K) {
+  int64_t rb = (rows + kBrickRows - 1) / kBrickRows;
+  int64_t kp = (K + kKPad - 1) / kKPad * kKPad;
+  return rb * (kp / kBrickK) * kBrickBytes;
+}
+
+const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std::string* msg) {
+  if (enc < AWE_ENC_B13 || enc > AWE_ENC_MOD) {
+    *st = AWE_ERR_INVALID_VALUE;
+    *msg = "unknown encoding";
+    return nullptr;
+  }
+  int key_m = enc == AWE_ENC_MOD ? modulus : 0;
+  if (enc == AWE_ENC_MOD && (modulus < 2 || modulus > 256)) {
+    *st = modulus < 2 ? AWE_ERR_INVALID_VALUE : AWE_ERR_UNSUPPORTED;
+    *msg = "modulus must lie in [2, 256] (residues are stored as uint8)";
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto key = std::make_pair((int)enc, key_m);
+  auto it = g_cache.find(key);
+  if (it != g_cache.end()) return it->second.get();
+  auto f = g_fail.find(key);
+  if (f != g_fail.end()) {
+    *st = enc == AWE_ENC_MOD ? AWE_ERR_UNSUPPORTED : AWE_ERR_TABLE;
+    *msg = f->second;
+    return nullptr;
+  }
+  auto s = std::make_unique<Scheme>();
+  s->enc = enc;
+  bool ok = true;
+  std::string m;
+  awe_status fail = AWE_ERR_TABLE;
+  switch (enc) {
+    case AWE_ENC_B13: define_b13(*s); break;
+    case AWE_ENC_AWE6: define_awe6(*s, false); break;
+    case AWE_ENC_AWE6ALT: define_awe6(*s, true); break;
+    case AWE_ENC_AWE4: define_awe4(*s); break;
+    case AWE_ENC_MOD:
+      ok = define_mod(*s, modulus, &m);
+      if (!ok) fail = AWE_ERR_UNSUPPORTED;
+      break;
+  }
+  if (ok) ok = finish(*s, &m);
+  if (!ok) {
+    g_fail[key] = m;
+    *st = fail;
+    *msg = m;
+    return nullptr;
+  }
+  const Scheme* out = s.get();
+  g_cache[key] = std::move(s);
+  *st = AWE_OK;
+  return out;
+}
+
+}  // namespace awe

@@ -1,0 +1,159 @@
+"""GPU parity of the exact product against the oracle's plain int64 GEMM (bit-exact).
+
+Small and ragged shapes that span several 256 x 128 tiles and a ragged tail,
+every encoding, both output types, forced small fold segments, reduction
+lengths that need several launches, the FP32 partial near its 2^23 bound,
+and the degenerate sizes.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import gemm as og
+from paper_2609_24519_amd import awe, inputs
+from tests.gpu_helpers import to_dev
+
+pytestmark = pytest.mark.gpu
+
+EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4]
+
+
+def _run_exact(enc, A, B, out=torch.int32):
+    Ad, Bd = to_dev(A), to_dev(B)
+    C = awe.matmul_exact(Ad, Bd, enc, out)
+    torch.cuda.synchronize()
+    return C.cpu().numpy()
+
+
+def _operands(enc, M, N, K, seed):
+    a_range = (-8, 7) if enc == awe.ENC_AWE4 else (-128, 127)
+    return inputs.int8_pair(M, N, K, seed, a_range=a_range)
+
+
+def test_config1_256_cubed():
+    A, B = inputs.int8_pair(256, 256, 256, seed=0)
+    ref = og.gemm_i64(A, B)
+    for enc in (awe.ENC_B13, awe.ENC_AWE6):
+        C = _run_exact(enc, A, B)
+        assert C.dtype == np.int32
+        assert np.array_equal(C.astype(np.int64), ref), enc
+
+
+@pytest.mark.parametrize("enc", EXACT)
+@pytest.mark.parametrize("M,N,K", [(1, 1, 1), (33, 65, 129), (300, 200, 333), (513, 129, 1000),
+                                   (64, 256, 64), (31, 17, 4097)])
+def test_ragged_shapes(enc, M, N, K):
+    A, B = _operands(enc, M, N, K, seed=M + N + K)
+    C = _run_exact(enc, A, B)
+    assert np.array_equal(C.astype(np.int64), og.gemm_i64(A, B))
+
+
+@pytest.mark.parametrize("enc", EXACT)
+def test_int64_output(enc):
+    A, B = _operands(enc, 97, 300, 700, seed=5)
+    C = _run_exact(enc, A, B, torch.int64)
+    assert C.dtype == np.int64 and np.array_equal(C, og.gemm_i64(A, B))
+
+
+def test_extremes():
+    # every entry at an end of the int8 range; the two's-complement end -128 included
+    M, N, K = 64, 96, 2048
+    A, B = inputs.stress_operands(M, N, K, seed=3)
+    ref = og.gemm_i64(A, B)
+    for enc in (awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT):
+        assert np.array_equal(_run_exact(enc, A, B).astype(np.int64), ref), enc
+    A4 = np.where(A < 0, -8, 7).astype(np.int8)
+    assert np.array_equal(_run_exact(awe.ENC_AWE4, A4, B).astype(np.int64), og.gemm_i64(A4, B))
+
+
+def test_zero_k_and_empty():
+    A = np.zeros((40, 0), np.int8)
+    B = np.zeros((0, 50), np.int8)
+    C = _run_exact(awe.ENC_AWE6, A, B)
+    assert C.shape == (40, 50) and not C.any()
+    C = awe.matmul_exact(to_dev(np.zeros((0, 8), np.int8)), to_dev(np.zeros((8, 5), np.int8)))
+    assert tuple(C.shape) == (0, 5)
+
+
+def _planes(enc, m, A, B):
+    M, K = A.shape
+    N = B.shape[1]
+    pa = torch.empty(max(awe.plane_bytes(enc, m, awe.SIDE_A, M, K), 1), dtype=torch.uint8, device="cuda")
+    pb = torch.empty(max(awe.plane_bytes(enc, m, awe.SIDE_B, N, K), 1), dtype=torch.uint8, device="cuda")
+    Ad, Bd = to_dev(A), to_dev(B)
+    awe.encode(enc, m, awe.SIDE_A, Ad, M, K, K, pa)
+    awe.encode(enc, m, awe.SIDE_B, Bd, N, K, N, pb)
+    return pa, pb
+
+
+@pytest.mark.parametrize("enc", EXACT)
+@pytest.mark.parametrize("kseg", [128, 384, 1024])
+def test_forced_fold_segments(enc, kseg):
+    M, N, K = 130, 260, 2000
+    A, B = _operands(enc, M, N, K, seed=11)
+    pa, pb = _planes(enc, 0, A, B)
+    C = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I32, kseg)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy().astype(np.int64), og.gemm_i64(A, B))
+
+
+def test_ldc_larger_than_n():
+    M, N, K = 70, 50, 300
+    A, B = inputs.int8_pair(M, N, K, seed=2)
+    pa, pb = _planes(awe.ENC_AWE6, 0, A, B)
+    C = torch.full((M, 64), -7, dtype=torch.int32, device="cuda")
+    awe.gemm_planes(awe.ENC_AWE6, 0, M, N, K, pa, pb, C, 64, awe.I32)
+    torch.cuda.synchronize()
+    Cn = C.cpu().numpy()
+    assert np.array_equal(Cn[:, :N].astype(np.int64), og.gemm_i64(A, B))
+    assert (Cn[:, N:] == -7).all()
+
+
+def test_multi_launch_reduction():
+    # K beyond what one launch's int32 accumulator may hold (130944 for int8 x int8): the
+    # host splits the reduction and the launches add into the int64 output
+    M, N, K = 40, 72, 300_000
+    A, B = inputs.int8_pair(M, N, K, seed=9)
+    C = _run_exact(awe.ENC_AWE6, A, B, torch.int64)
+    assert np.array_equal(C, og.gemm_i64(A, B))
+
+
+def test_fp32_partial_near_bound():
+    # AWE4: c_A c_B = 24, fold segment 349440, so one FP32 partial reaches 24 * 349440 = 8386560,
+    # just below 2^23; constant operands put every product at its largest magnitude
+    info = awe.get_encoding_info(awe.ENC_AWE4)
+    K = info["k_seg"]
+    loa, TA = awe.get_plane_table(awe.ENC_AWE4, 0, awe.SIDE_A)
+    lob, TB = awe.get_plane_table(awe.ENC_AWE4, 0, awe.SIDE_B)
+    xs = [x for x in range(loa, loa + TA.shape[0]) if np.abs(TA[x - loa]).max() == 3]
+    ys = [y for y in range(lob, lob + TB.shape[0]) if np.abs(TB[y - lob]).max() == 8]
+    M = N = 32
+    A = np.empty((M, K), np.int8)
+    B = np.empty((K, N), np.int8)
+    for i in range(M):
+        A[i] = xs[i % len(xs)]
+    for j in range(N):
+        B[:, j] = ys[(7 * j) % len(ys)]
+    C = _run_exact(awe.ENC_AWE4, A, B, torch.int64)
+    ref = np.outer(A[:, 0].astype(np.int64), B[0].astype(np.int64)) * K
+    assert np.array_equal(C, ref)
+
+
+@pytest.mark.parametrize("m", [2, 9, 13, 31, 53, 89, 149, 157])
+def test_mod_parity(m):
+    A, B = inputs.residue_pair(190, 140, 777, m)
+    Ad, Bd = to_dev(A), to_dev(B)
+    C = awe.matmul_mod(m, Ad, Bd)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
+
+
+def test_mod_forced_segments():
+    m = 157
+    A, B = inputs.residue_pair(64, 200, 3000, m)
+    pa, pb = _planes(awe.ENC_MOD, m, A, B)
+    C = torch.empty((64, 200), dtype=torch.int32, device="cuda")
+    awe.gemm_planes(awe.ENC_MOD, m, 64, 200, 3000, pa, pb, C, 200, awe.I32, 256)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))

@@ -31,9 +31,10 @@
  * awe_gemm_planes).  One side holds P planes back to back; plane p starts at
  * byte p * stride, stride = ceil(rows/32) * (Kp/64) * 1024 with
  * Kp = K rounded up to a multiple of 128.  A plane is a grid of 1024-byte
- * bricks, brick (rb, ks) at byte (rb * Kp/64 + ks) * 1024, covering rows
- * (A: rows of A; B: columns of B) rb*32 .. rb*32+31 and reduction indices
- * ks*64 .. ks*64+63.  Inside a brick, lane L = 32*h + t (h in {0,1},
+ * bricks, brick (rb, ks) at byte (ks * ceil(rows/32) + rb) * 1024 (k-step
+ * major: the bricks of one k-step for consecutive row blocks are adjacent),
+ * covering rows (A: rows of A; B: columns of B) rb*32 .. rb*32+31 and
+ * reduction indices ks*64 .. ks*64+63.  Inside a brick, lane L = 32*h + t (h in {0,1},
  * t in 0..31) owns bytes L*16 .. L*16+15, which hold row rb*32 + t at
  * reduction indices ks*64 + 32*h + j, j = 0..31, element j in the low nibble
  * of byte L*16 + j/2 when j is even and in the high nibble when j is odd.

@@ -26,7 +26,7 @@ struct LutArg {
 template <bool kTransposed>
 __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__ x, int64_t rows,
                                                      int64_t K, int64_t ld, int64_t KS,
-                                                     int64_t nbricks, int nplanes,
+                                                     int64_t R32, int64_t nbricks, int nplanes,
                                                      uint8_t* __restrict__ planes,
                                                      int64_t plane_stride, int32_t* flag,
                                                      LutArg lut) {
@@ -63,7 +63,7 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
   for (int j = 0; j < 32; ++j) bad |= e[j];
   if ((bad & kLutInvalid) && flag != nullptr) atomicOr(flag, 1);
 
-  uint8_t* dst = planes + brick * kBrickBytes + lane * 16;
+  uint8_t* dst = planes + (ks * R32 + rb) * kBrickBytes + lane * 16;
   for (int p = 0; p < nplanes; ++p) {
     uint32_t d[4] = {0, 0, 0, 0};
 #pragma unroll
@@ -94,8 +94,11 @@ constexpr int BM = 256, BN = 128;
 constexpr int A_BRICKS = (BM / kBrickRows) * 2;  // per stage: 8 row blocks x 2 k-steps
 constexpr int B_BRICKS = (BN / kBrickRows) * 2;
 constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * kBrickBytes;  // 24 KiB
-constexpr int BRICKS_PER_WAVE = (A_BRICKS + B_BRICKS) / 4;        // 6
-constexpr int NSTAGE = 4;                                         // LDS ring depth
+constexpr int BRICKS_PER_WAVE = (A_BRICKS + B_BRICKS) / 4;        // 6 per wave per stage
+#ifndef AWE_GEMM_NSTAGE
+#define AWE_GEMM_NSTAGE 4
+#endif
+constexpr int NSTAGE = AWE_GEMM_NSTAGE;                           // LDS ring depth
 constexpr int GEMM_LDS_BYTES = NSTAGE * STAGE_BYTES;
 constexpr uint32_t kScale2 = 0x80808080u;                         // E8M0 2^1 in every byte
 
@@ -108,14 +111,14 @@ struct GemmArgs {
   int32_t t_begin, t_end;
   int32_t ts;        // fold segment in k-tiles
   int32_t r;
-  int32_t pidx_a[kMaxProducts], pidx_b[kMaxProducts];
+  uint64_t pidx_a, pidx_b;  // plane of product k in bits 4k .. 4k+3 (kept in SGPRs: no loads in the loop)
   int32_t fold_ell[kMaxProducts];
   uint32_t fold_mask;
   void* C;
   int64_t ldc;
   int32_t M, N;
   int32_t c64, accumulate, log2D, modulus;
-  int32_t tiles_n;
+  int32_t tiles_m, tiles_n;
 };
 
 // Position in the reduction stream: product p, k-tile t, current fold segment [cs, ce).
@@ -123,16 +126,21 @@ struct Cursor {
   int p, t, cs, ce;
 };
 
+// Advance to the next stage; saturates on the last stage of the launch (the
+// copies issued past the end re-read that stage into a buffer nobody reads,
+// which keeps the number of copies in flight the same for every stage).
 __device__ __forceinline__ void cursor_next(Cursor& c, const GemmArgs& g) {
-  if (++c.t == c.ce) {
-    c.t = c.cs;
-    if (++c.p == g.r) {
-      c.p = 0;
-      c.cs = c.ce;
-      c.ce = min(c.cs + g.ts, g.t_end);
-      c.t = c.cs;
-    }
-  }
+  const int t1 = c.t + 1;
+  const bool end_t = t1 == c.ce;
+  const int p1 = c.p + (end_t ? 1 : 0);
+  const bool end_p = end_t && p1 == g.r;
+  const bool end_all = end_p && c.ce == g.t_end;
+  const int ncs = end_p ? c.ce : c.cs;
+  const int nce = end_p ? min(c.ce + g.ts, g.t_end) : c.ce;
+  c.t = end_all ? c.t : (end_t ? ncs : t1);
+  c.p = end_all ? c.p : (end_p ? 0 : p1);
+  c.cs = end_all ? c.cs : ncs;
+  c.ce = end_all ? c.ce : nce;
 }
 
 // One 16-byte-per-lane global -> LDS copy: the wave's 64 lanes fill the 1 KiB
@@ -150,23 +158,34 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Workgroup barrier that is also a compiler memory barrier: no LDS access may
+// move across it.  The caller has already waited for its own copies (vmcnt)
+// and LDS reads (lgkmcnt) as the protocol needs.
+__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Wave w copies A bricks 4w .. 4w+3 (row blocks 2w, 2w+1, both k-steps) and
+// B bricks 2w, 2w+1 (column block w) of the stage at cursor c.
 __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
                                            int tm, int tn, int wave, int lane) {
-  const uint8_t* pa = g.pa + (int64_t)g.pidx_a[c.p] * g.stride_a;
-  const uint8_t* pb = g.pb + (int64_t)g.pidx_b[c.p] * g.stride_b;
+  const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u), kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
+  // k-step major planes: the bricks of one k-step for consecutive row blocks are adjacent
+  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * 2 * g.rba * kBrickBytes;
+  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * 2 * g.rbb * kBrickBytes;
 #pragma unroll
-  for (int i = 0; i < BRICKS_PER_WAVE; ++i) {
-    const int id = wave * BRICKS_PER_WAVE + i;  // wave-uniform
-    const uint8_t* src;
-    if (id < A_BRICKS) {
-      const int rb = min(tm * (BM / kBrickRows) + (id >> 1), g.rba - 1);
-      src = pa + ((int64_t)rb * g.KS + c.t * 2 + (id & 1)) * kBrickBytes;
-    } else {
-      const int idb = id - A_BRICKS;
-      const int cb = min(tn * (BN / kBrickRows) + (idb >> 1), g.rbb - 1);
-      src = pb + ((int64_t)cb * g.KS + c.t * 2 + (idb & 1)) * kBrickBytes;
-    }
-    dma_brick(src + lane * 16, stage_lds + id * kBrickBytes);
+  for (int i = 0; i < 4; ++i) {
+    const int id = wave * 4 + i;
+    const int rb = min(tm * (BM / kBrickRows) + (id >> 1), g.rba - 1);
+    dma_brick(pa + ((int64_t)(id & 1) * g.rba + rb) * kBrickBytes + lane * 16,
+              stage_lds + id * kBrickBytes);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int id = wave * 2 + i;
+    const int cb = min(tn * (BN / kBrickRows) + (id >> 1), g.rbb - 1);
+    dma_brick(pb + ((int64_t)(id & 1) * g.rbb + cb) * kBrickBytes + lane * 16,
+              stage_lds + (A_BRICKS + id) * kBrickBytes);
   }
 }
 
@@ -176,30 +195,51 @@ __device__ __forceinline__ v8i frag(const uint8_t* p) {
   return v;
 }
 
-__device__ __forceinline__ void compute_stage(const uint8_t* stage, int wm, int wn, int lane,
-                                              v16f (&acc)[4][2]) {
+// The wave's operand fragments for one k-step (64 reduction indices) of a stage.
+struct Frags {
+  v8i a[4], b[2];
+};
+
+__device__ __forceinline__ void read_frags(Frags& f, const uint8_t* stage, int ks, int wm, int wn,
+                                           int lane) {
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-    v8i a[4], b[2];
+  for (int i = 0; i < 4; ++i) f.a[i] = frag(stage + ((wm * 4 + i) * 2 + ks) * kBrickBytes + lane * 16);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = frag(stage + ((wm * 4 + i) * 2 + ks) * kBrickBytes + lane * 16);
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      b[j] = frag(stage + (A_BRICKS + (wn * 2 + j) * 2 + ks) * kBrickBytes + lane * 16);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[i], b[j], acc[i][j], 4, 4, 0,
-                                                                     kScale2, 0, kScale2);
-  }
+  for (int j = 0; j < 2; ++j)
+    f.b[j] = frag(stage + (A_BRICKS + (wn * 2 + j) * 2 + ks) * kBrickBytes + lane * 16);
+}
+
+__device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
+  acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 4, 4, 0, kScale2, 0, kScale2);
+}
+
+#ifndef AWE_GEMM_GROUP_M
+#define AWE_GEMM_GROUP_M 4
+#endif
+// Workgroup -> output tile.  Workgroups are dispatched round-robin over the 8
+// XCDs (each with its own L2): consecutive tiles of one XCD's share are taken
+// from a band of AWE_GEMM_GROUP_M tile rows, so the ~32 workgroups an XCD runs
+// at once cover a compact block of C and share their A rows and B columns in
+// that XCD's L2.
+__device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& tm, int& tn) {
+  const int nb = g.tiles_m * g.tiles_n;
+  int lin = bid;
+  if ((nb & 7) == 0) lin = (bid & 7) * (nb >> 3) + (bid >> 3);
+  const int per_group = AWE_GEMM_GROUP_M * g.tiles_n;
+  const int grp = lin / per_group;
+  const int first = grp * AWE_GEMM_GROUP_M;
+  const int gm = min(g.tiles_m - first, AWE_GEMM_GROUP_M);
+  const int in = lin - grp * per_group;
+  tm = first + in % gm;
+  tn = in / gm;
 }
 
 __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x - (blockIdx.x / g.tiles_n) * g.tiles_n;
+  int tm, tn;
+  tile_of_block(g, blockIdx.x, tm, tn);
   const int wm = wave >> 1, wn = wave & 1;
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
 
@@ -215,48 +255,66 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
         iacc[i][j][v] = 0;
       }
 
-  const int nt = g.t_end - g.t_begin;
-  const int S = g.r * nt;
-  Cursor cur{0, g.t_begin, g.t_begin, min(g.t_begin + g.ts, g.t_end)};
-  Cursor nxt = cur;
-  // prologue: stages 0 .. NSTAGE-2 in flight
+  Cursor nxt{0, g.t_begin, g.t_begin, min(g.t_begin + g.ts, g.t_end)};
+  // Prologue: stages 0 .. NSTAGE-1 fill the whole ring.
 #pragma unroll
-  for (int i = 0; i < NSTAGE - 1; ++i) {
-    if (i < S) {
-      load_stage(g, nxt, lds0 + i * STAGE_BYTES, tm, tn, wave, lane);
-      cursor_next(nxt, g);
-    }
+  for (int i = 0; i < NSTAGE; ++i) {
+    load_stage(g, nxt, lds0 + i * STAGE_BYTES, tm, tn, wave, lane);
+    cursor_next(nxt, g);
   }
+  wait_vmcnt<BRICKS_PER_WAVE * (NSTAGE - 1)>();
+  block_barrier();
+  Frags f0, f1;
+  read_frags(f0, smem, 0, wm, wn, lane);
+
+  // Stage s: F1 <- (s, k-step 1); MFMAs (s, 0) on F0; wait until stage s+1 has
+  // landed and this wave's reads of stage s are done; barrier; refill stage s's
+  // buffer with stage s+NSTAGE; F0 <- (s+1, 0); MFMAs (s, 1) on F1.  The
+  // barrier sits between two groups of MFMAs, and the next stage's first
+  // fragments are in flight while the second group executes.  The body has no
+  // branch, so the order below is the issue order.
   int buf = 0;
-  for (int s = 0; s < S; ++s) {
-    // stage s has landed once at most the NSTAGE-2 younger stages are outstanding
-    if (s + NSTAGE - 2 < S)
-      wait_vmcnt<BRICKS_PER_WAVE * (NSTAGE - 2)>();
-    else
-      wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();  // every wave's copies of stage s are visible; stage s-1 is consumed
-    if (s + NSTAGE - 1 < S) {
-      int nb = buf + NSTAGE - 1;
-      if (nb >= NSTAGE) nb -= NSTAGE;
-      load_stage(g, nxt, lds0 + nb * STAGE_BYTES, tm, tn, wave, lane);
-      cursor_next(nxt, g);
+  for (int cs = g.t_begin; cs < g.t_end; cs += g.ts) {
+    const int ce = min(cs + g.ts, g.t_end);
+    for (int p = 0; p < g.r; ++p) {
+      for (int t = cs; t < ce; ++t) {
+        const uint32_t cur_off = buf * STAGE_BYTES;
+        buf = buf + 1 == NSTAGE ? 0 : buf + 1;
+        read_frags(f1, smem + cur_off, 1, wm, wn, lane);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) mfma_block(acc[i][j], f0.a[i], f0.b[j]);
+        __builtin_amdgcn_sched_barrier(0);
+        wait_vmcnt<BRICKS_PER_WAVE * (NSTAGE - 2)>();
+        wait_lgkm0();
+        block_barrier();
+        load_stage(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
+        cursor_next(nxt, g);
+        read_frags(f0, smem + buf * STAGE_BYTES, 0, wm, wn, lane);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) mfma_block(acc[i][j], f1.a[i], f1.b[j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if ((g.fold_mask >> p) & 1u) {
+        const int32_t l = g.fold_ell[p];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
+              acc[i][j][v] = 0.0f;
+            }
+      }
     }
-    compute_stage(smem + buf * STAGE_BYTES, wm, wn, lane, acc);
-    if (cur.t == cur.ce - 1 && ((g.fold_mask >> cur.p) & 1u)) {
-      const int32_t l = g.fold_ell[cur.p];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
-            acc[i][j][v] = 0.0f;
-          }
-    }
-    cursor_next(cur, g);
-    if (++buf == NSTAGE) buf = 0;
   }
+  wait_vmcnt<0>();  // the saturated copies past the end must land before the wave exits
 
   // Epilogue: exact shift by log2 D, or the non-negative residue mod m.
   const int row0 = tm * BM + wm * 128 + 4 * (lane >> 5);
@@ -315,11 +373,11 @@ awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
   if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;
   if (e.transposed)
     hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, nbricks,
+                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,
                        e.nplanes, e.planes, e.plane_stride, e.flag, lut);
   else
     hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, nbricks,
+                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,
                        e.nplanes, e.planes, e.plane_stride, e.flag, lut);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) {
@@ -356,9 +414,10 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.t_end = (int32_t)(L.k_end / kKPad);
   g.ts = (int32_t)(L.k_seg / kKPad);
   g.r = L.r;
+  g.pidx_a = g.pidx_b = 0;
   for (int k = 0; k < L.r; ++k) {
-    g.pidx_a[k] = L.pa[k];
-    g.pidx_b[k] = L.pb[k];
+    g.pidx_a |= (uint64_t)(L.pa[k] & 15) << (4 * k);
+    g.pidx_b |= (uint64_t)(L.pb[k] & 15) << (4 * k);
     g.fold_ell[k] = L.fold_ell[k];
   }
   g.fold_mask = L.fold_mask;
@@ -371,6 +430,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.log2D = L.log2D;
   g.modulus = L.modulus;
   const int64_t tiles_m = (L.M + BM - 1) / BM, tiles_n = (L.N + BN - 1) / BN;
+  g.tiles_m = (int32_t)tiles_m;
   g.tiles_n = (int32_t)tiles_n;
   const int64_t blocks = tiles_m * tiles_n;
   if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;

@@ -27,7 +27,9 @@ def decode_planes(buf, nplanes, rows, K):
     Kp = -(-K // 128) * 128
     KS = Kp // 64
     stride = R32 * KS * 1024
-    raw = np.asarray(buf[: nplanes * stride], dtype=np.uint8).reshape(nplanes, R32, KS, 64, 16)
+    # k-step major: brick (rb, ks) at (ks * R32 + rb) * 1024
+    raw = np.asarray(buf[: nplanes * stride], dtype=np.uint8).reshape(nplanes, KS, R32, 64, 16)
+    raw = raw.transpose(0, 2, 1, 3, 4)
     nib = np.stack([raw & 0xF, raw >> 4], axis=-1).reshape(nplanes, R32, KS, 2, 32, 32)
     val = E2M1_MAG[nib & 7] * np.where(nib & 8, -1, 1)
     # [p, rb, ks, h, t, j] -> [p, rb, t, ks, h, j]

@@ -150,9 +150,10 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(A_h, B_h, rows=48):
-    """The oracle (plain int64 triple loop, OpenMP over rows) on a bounded sample:
-    ``rows`` rows of C over the full N and K, scaled to exact TOPS."""
+def cpu_baseline(A_h, B_h, target_s=10.0):
+    """The oracle (plain int64 triple loop, OpenMP over rows) on a bounded sample of
+    the same workload: a block of rows of C over the full N and K, sized from a short
+    calibration run to take about ``target_s`` seconds, scaled to exact TOPS."""
     import numpy as np
 
     from oracle import gemm as og
@@ -160,14 +161,22 @@ def cpu_baseline(A_h, B_h, rows=48):
     if not os.path.exists(os.path.join(ROOT, "oracle", "liboracle_gemm.so")):
         og.build()
     K, N = B_h.shape
+    threads = og.num_threads()
+    rows = max(threads, 16)
+    t0 = time.perf_counter()
+    og.gemm_i64(np.ascontiguousarray(A_h[:rows]), B_h)
+    dt = time.perf_counter() - t0
+    rows = int(min(A_h.shape[0], max(rows, rows * target_s / max(dt, 1e-3))))
+    rows = max(threads, rows // threads * threads)
     sub = np.ascontiguousarray(A_h[:rows])
     t0 = time.perf_counter()
     og.gemm_i64(sub, B_h)
     dt = time.perf_counter() - t0
     macs = rows * N * K
-    return {"value": round(2.0 * macs / dt / 1e12, 6), "unit": "TOPS", "cores": og.num_threads(),
+    return {"value": round(2.0 * macs / dt / 1e12, 6), "unit": "TOPS", "cores": threads,
             "kind": "oracle",
-            "sample": "%d of %d rows of C (%d x %d x %d MACs), %.1f s" % (rows, A_h.shape[0], rows, N, K, dt)}
+            "sample": "rows 0..%d of C over full N=%d, K=%d (%d MACs), %.1f s"
+                      % (rows - 1, N, K, macs, dt)}
 
 
 if __name__ == "__main__":

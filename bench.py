@@ -34,6 +34,8 @@ def parse():
     p.add_argument("--size", type=int, default=8192)
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
     p.add_argument("--no-context", action="store_true", help="skip base-13 and INT8 context")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="also run a plain 1 GiB device copy (the reference for rocprofv3 byte counters)")
     return p.parse_args()
 
 
@@ -120,7 +122,7 @@ def main():
         "encode": {"ms": round(enc_ms, 4), "GB_s": round(enc_bytes / (enc_ms * 1e-3) / 1e9, 1)},
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": FP4_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / FP4_PEAK_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": gemm_traffic()},
     }
     if not args.no_context:
         binfo, bwall, benc_ms, bgemm_ms = run(awe.ENC_B13, max(3, args.steps // 2), 2)
@@ -145,9 +147,33 @@ def main():
             line["int8_mfma_context"]["equal_to_exact_C"] = bool(torch.equal(Ci, C))
         except Exception as ex:  # noqa: BLE001 - context only
             line["int8_mfma_context"] = {"error": str(ex)[:200]}
+    if args.calibrate_copy:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(A_h, B_h)
     print(json.dumps(line), flush=True)
+
+
+def gemm_traffic():
+    """HBM bytes per GEMM dispatch from the committed rocprofv3 counter summary, or None
+    when that summary was taken on a different kernel source."""
+    from paper_2609_24519_amd import profiling
+
+    path = os.path.join(ROOT, "profiles", "traffic_gemm_awe6_int8_8192.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except OSError:
+        return None
+    if rec.get("kernel_source_sha") != profiling.kernel_source_hash():
+        return None
+    k = rec["kernels"].get("gemm_kernel")
+    return None if k is None else round(k["fetch_bytes"] + k["write_bytes"])
 
 
 def cpu_baseline(A_h, B_h, target_s=10.0):

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
+#include <string>
 
 #include "awe_internal.h"
 
@@ -75,32 +77,48 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
 // ---------------------------------------------------------------------------
 // Multi-plane FP4 GEMM (Alg. 1, the r products and the reconstruction).
 //
-// Tile 256 x 128 of C per workgroup of 4 waves; each wave owns 128 x 64 as
-// 4 x 2 blocks of the 32x32x64 scaled FP4 MFMA.  The reduction runs as one
-// stream of k-tiles (128 indices = 2 bricks per row block) in the order
-// segment -> product -> k-tile: a wave accumulates one product in FP32 for a
-// whole fold segment, then folds that partial into an int32 accumulator with
-// its reconstruction coefficient (cvt + 24-bit multiply-add) and restarts the
-// FP32 accumulator.  Every FP32 partial is an exact integer below 2^23 by the
-// segment length (Sec. 3.4 with a factor 2 of margin for the 24-bit multiply),
-// and the int32 sum is exact modulo 2^32; the host splits the reduction into
-// launches so that the true value of each launch fits in int32.
+// A workgroup of WM x WN waves computes a BM x BN tile of C; each wave owns
+// (32 BMW) x (32 BNW) as BMW x BNW blocks of the 32x32x64 scaled FP4 MFMA.
+// The reduction runs as one stream of k-tiles (128 indices = 2 bricks per row
+// block) in the order segment -> product -> k-tile: a wave accumulates one
+// product in FP32 for a whole fold segment, then folds that partial into an
+// int32 accumulator with its reconstruction coefficient (cvt + 24-bit
+// multiply-add) and restarts the FP32 accumulator.  Every FP32 partial is an
+// exact integer of magnitude at most 2^23 - 1 by the segment length (Sec. 3.4
+// with a factor 2 of margin for the 24-bit multiply), and the int32 sum is
+// exact modulo 2^32; the host splits the reduction into launches so that the
+// true value of each launch fits in int32.
 //
 // Both E8M0 block scales are 2^1 (byte 128): the stored E2M1 values are s/2
 // for the doubled integers s of S, so each product of codes is s_a s_b
 // exactly and the FP32 accumulators hold the integer plane products.
+//
+// A product-major stream needs one FP32 and one int32 accumulator per output
+// (8 bytes of registers), so the register file bounds the tile; the operand
+// bytes each CU must pull through its L1 per MFMA fall as the tile grows.
 // ---------------------------------------------------------------------------
-constexpr int BM = 256, BN = 128;
-constexpr int A_BRICKS = (BM / kBrickRows) * 2;  // per stage: 8 row blocks x 2 k-steps
-constexpr int B_BRICKS = (BN / kBrickRows) * 2;
-constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * kBrickBytes;  // 24 KiB
-constexpr int BRICKS_PER_WAVE = (A_BRICKS + B_BRICKS) / 4;        // 6 per wave per stage
 #ifndef AWE_GEMM_NSTAGE
 #define AWE_GEMM_NSTAGE 4
 #endif
-constexpr int NSTAGE = AWE_GEMM_NSTAGE;                           // LDS ring depth
-constexpr int GEMM_LDS_BYTES = NSTAGE * STAGE_BYTES;
-constexpr uint32_t kScale2 = 0x80808080u;                         // E8M0 2^1 in every byte
+constexpr int NSTAGE = AWE_GEMM_NSTAGE;  // LDS ring depth
+constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
+
+template <int WM_, int WN_, int BMW_, int BNW_>
+struct Cfg {
+  static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
+  static constexpr int NW = WM * WN;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int BM = WM * BMW * 32, BN = WN * BNW * 32;
+  static constexpr int A_BRICKS = (BM / kBrickRows) * 2;  // per stage: row blocks x 2 k-steps
+  static constexpr int B_BRICKS = (BN / kBrickRows) * 2;
+  static constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * kBrickBytes;
+  static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES;
+  // copies per wave and stage: A bricks evenly, B bricks round-robin (the first
+  // B_BRICKS % NW waves take one more)
+  static constexpr int A_PW = A_BRICKS / NW;
+  static constexpr int B_LO = B_BRICKS / NW, B_XTRA = B_BRICKS % NW;
+  static_assert(A_BRICKS % NW == 0, "A bricks must split evenly over the waves");
+};
 
 struct GemmArgs {
   const uint8_t* pa;
@@ -144,11 +162,12 @@ __device__ __forceinline__ void cursor_next(Cursor& c, const GemmArgs& g) {
 }
 
 // One 16-byte-per-lane global -> LDS copy: the wave's 64 lanes fill the 1 KiB
-// at LDS byte address `lds` (wave-uniform, in M0) from their own global
-// addresses.  Issued as inline assembly so that the compiler does not
-// serialise the copies; completion is awaited explicitly with vmcnt.
-__device__ __forceinline__ void dma_brick(const uint8_t* src, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds)
+// at LDS byte address `lds` (wave-uniform, in M0).  The brick's base address
+// is wave-uniform (SGPRs); every lane adds its own 16-byte offset `voff`.
+// Issued as inline assembly so that the compiler does not serialise the
+// copies; completion is awaited explicitly with vmcnt.
+__device__ __forceinline__ void dma_brick(const uint8_t* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "s"(lds)
                : "memory");
 }
 
@@ -158,6 +177,15 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Wait until at most `stages` younger stages of this wave's copies are in flight.
+template <class C, int STAGES>
+__device__ __forceinline__ void wait_stages(int wave) {
+  if (C::B_XTRA == 0 || wave < C::B_XTRA)
+    wait_vmcnt<(C::A_PW + C::B_LO + (C::B_XTRA ? 1 : 0)) * STAGES>();
+  else
+    wait_vmcnt<(C::A_PW + C::B_LO) * STAGES>();
+}
+
 // Workgroup barrier that is also a compiler memory barrier: no LDS access may
 // move across it.  The caller has already waited for its own copies (vmcnt)
 // and LDS reads (lgkmcnt) as the protocol needs.
@@ -165,27 +193,29 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 
 __device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// Wave w copies A bricks 4w .. 4w+3 (row blocks 2w, 2w+1, both k-steps) and
-// B bricks 2w, 2w+1 (column block w) of the stage at cursor c.
+// The copies of one stage: wave w takes A bricks A_PW w .. A_PW w + A_PW - 1
+// and B bricks w, w + NW, ... (brick id = 2 * row block + k-step).
+template <class C>
 __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
                                            int tm, int tn, int wave, int lane) {
   const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u), kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
   // k-step major planes: the bricks of one k-step for consecutive row blocks are adjacent
   const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * 2 * g.rba * kBrickBytes;
   const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * 2 * g.rbb * kBrickBytes;
+  const uint32_t voff = lane * 16;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int id = wave * 4 + i;
-    const int rb = min(tm * (BM / kBrickRows) + (id >> 1), g.rba - 1);
-    dma_brick(pa + ((int64_t)(id & 1) * g.rba + rb) * kBrickBytes + lane * 16,
-              stage_lds + id * kBrickBytes);
+  for (int i = 0; i < C::A_PW; ++i) {
+    const int id = wave * C::A_PW + i;
+    const int rb = min(tm * (C::BM / kBrickRows) + (id >> 1), g.rba - 1);
+    dma_brick(pa + ((int64_t)(id & 1) * g.rba + rb) * kBrickBytes, voff, stage_lds + id * kBrickBytes);
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int id = wave * 2 + i;
-    const int cb = min(tn * (BN / kBrickRows) + (id >> 1), g.rbb - 1);
-    dma_brick(pb + ((int64_t)(id & 1) * g.rbb + cb) * kBrickBytes + lane * 16,
-              stage_lds + (A_BRICKS + id) * kBrickBytes);
+  for (int i = 0; i < C::B_LO + (C::B_XTRA ? 1 : 0); ++i) {
+    const int id = wave + i * C::NW;
+    if (i == C::B_LO && wave >= C::B_XTRA) break;
+    const int cb = min(tn * (C::BN / kBrickRows) + (id >> 1), g.rbb - 1);
+    dma_brick(pb + ((int64_t)(id & 1) * g.rbb + cb) * kBrickBytes, voff,
+              stage_lds + (C::A_BRICKS + id) * kBrickBytes);
   }
 }
 
@@ -196,17 +226,20 @@ __device__ __forceinline__ v8i frag(const uint8_t* p) {
 }
 
 // The wave's operand fragments for one k-step (64 reduction indices) of a stage.
+template <class C>
 struct Frags {
-  v8i a[4], b[2];
+  v8i a[C::BMW], b[C::BNW];
 };
 
-__device__ __forceinline__ void read_frags(Frags& f, const uint8_t* stage, int ks, int wm, int wn,
-                                           int lane) {
+template <class C>
+__device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, int ks, int wm,
+                                           int wn, int lane) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) f.a[i] = frag(stage + ((wm * 4 + i) * 2 + ks) * kBrickBytes + lane * 16);
+  for (int i = 0; i < C::BMW; ++i)
+    f.a[i] = frag(stage + ((wm * C::BMW + i) * 2 + ks) * kBrickBytes + lane * 16);
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
-    f.b[j] = frag(stage + (A_BRICKS + (wn * 2 + j) * 2 + ks) * kBrickBytes + lane * 16);
+  for (int j = 0; j < C::BNW; ++j)
+    f.b[j] = frag(stage + (C::A_BRICKS + (wn * C::BNW + j) * 2 + ks) * kBrickBytes + lane * 16);
 }
 
 __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
@@ -218,8 +251,8 @@ __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b
 #endif
 // Workgroup -> output tile.  Workgroups are dispatched round-robin over the 8
 // XCDs (each with its own L2): consecutive tiles of one XCD's share are taken
-// from a band of AWE_GEMM_GROUP_M tile rows, so the ~32 workgroups an XCD runs
-// at once cover a compact block of C and share their A rows and B columns in
+// from a band of AWE_GEMM_GROUP_M tile rows, so the workgroups an XCD runs at
+// once cover a compact block of C and share their A rows and B columns in
 // that XCD's L2.
 __device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& tm, int& tn) {
   const int nb = g.tiles_m * g.tiles_n;
@@ -234,21 +267,22 @@ __device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& t
   tn = in / gm;
 }
 
-__global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
+template <class C>
+__global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int tm, tn;
   tile_of_block(g, blockIdx.x, tm, tn);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WN, wn = wave % C::WN;
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
 
-  v16f acc[4][2];
-  int32_t iacc[4][2][16];
+  v16f acc[C::BMW][C::BNW];
+  int32_t iacc[C::BMW][C::BNW][16];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < C::BNW; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         acc[i][j][v] = 0.0f;
@@ -259,70 +293,72 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
   // Prologue: stages 0 .. NSTAGE-1 fill the whole ring.
 #pragma unroll
   for (int i = 0; i < NSTAGE; ++i) {
-    load_stage(g, nxt, lds0 + i * STAGE_BYTES, tm, tn, wave, lane);
+    load_stage<C>(g, nxt, lds0 + i * C::STAGE_BYTES, tm, tn, wave, lane);
     cursor_next(nxt, g);
   }
-  wait_vmcnt<BRICKS_PER_WAVE * (NSTAGE - 1)>();
+  wait_stages<C, NSTAGE - 1>(wave);
   block_barrier();
-  Frags f0, f1;
-  read_frags(f0, smem, 0, wm, wn, lane);
+  Frags<C> f0, f1;
+  read_frags<C>(f0, smem, 0, wm, wn, lane);
 
   // Stage s: F1 <- (s, k-step 1); MFMAs (s, 0) on F0; wait until stage s+1 has
   // landed and this wave's reads of stage s are done; barrier; refill stage s's
   // buffer with stage s+NSTAGE; F0 <- (s+1, 0); MFMAs (s, 1) on F1.  The
   // barrier sits between two groups of MFMAs, and the next stage's first
-  // fragments are in flight while the second group executes.  The body has no
-  // branch, so the order below is the issue order.
+  // fragments are in flight while the second group executes.
   int buf = 0;
   for (int cs = g.t_begin; cs < g.t_end; cs += g.ts) {
     const int ce = min(cs + g.ts, g.t_end);
     for (int p = 0; p < g.r; ++p) {
       for (int t = cs; t < ce; ++t) {
-        const uint32_t cur_off = buf * STAGE_BYTES;
+        const uint32_t cur_off = buf * C::STAGE_BYTES;
         buf = buf + 1 == NSTAGE ? 0 : buf + 1;
-        read_frags(f1, smem + cur_off, 1, wm, wn, lane);
+        read_frags<C>(f1, smem + cur_off, 1, wm, wn, lane);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) mfma_block(acc[i][j], f0.a[i], f0.b[j]);
+          for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], f0.a[i], f0.b[j]);
         __builtin_amdgcn_sched_barrier(0);
-        wait_vmcnt<BRICKS_PER_WAVE * (NSTAGE - 2)>();
+        wait_stages<C, NSTAGE - 2>(wave);
         wait_lgkm0();
         block_barrier();
-        load_stage(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
+        load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
         cursor_next(nxt, g);
-        read_frags(f0, smem + buf * STAGE_BYTES, 0, wm, wn, lane);
+        read_frags<C>(f0, smem + buf * C::STAGE_BYTES, 0, wm, wn, lane);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) mfma_block(acc[i][j], f1.a[i], f1.b[j]);
+          for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], f1.a[i], f1.b[j]);
         __builtin_amdgcn_sched_barrier(0);
       }
       if ((g.fold_mask >> p) & 1u) {
         const int32_t l = g.fold_ell[p];
+        // one 32x32 block at a time keeps the temporaries of the fold small
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
+          for (int j = 0; j < C::BNW; ++j) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
               iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
               acc[i][j][v] = 0.0f;
             }
+            __builtin_amdgcn_sched_barrier(0);
+          }
       }
     }
   }
   wait_vmcnt<0>();  // the saturated copies past the end must land before the wave exits
 
   // Epilogue: exact shift by log2 D, or the non-negative residue mod m.
-  const int row0 = tm * BM + wm * 128 + 4 * (lane >> 5);
-  const int col0 = tn * BN + wn * 64 + (lane & 31);
+  const int row0 = tm * C::BM + wm * (32 * C::BMW) + 4 * (lane >> 5);
+  const int col0 = tn * C::BN + wn * (32 * C::BNW) + (lane & 31);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < C::BNW; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
@@ -334,21 +370,26 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(GemmArgs g) {
           const int32_t m = g.modulus;
           int32_t rr = val % m;
           if (rr < 0) rr += m;
-          int32_t* C = reinterpret_cast<int32_t*>(g.C);
-          if (g.accumulate) rr = (C[off] + rr) % m;
-          C[off] = rr;
+          int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
+          if (g.accumulate) rr = (Cp[off] + rr) % m;
+          Cp[off] = rr;
         } else {
           val >>= g.log2D;
           if (g.c64) {
-            int64_t* C = reinterpret_cast<int64_t*>(g.C);
-            C[off] = g.accumulate ? C[off] + (int64_t)val : (int64_t)val;
+            int64_t* Cp = reinterpret_cast<int64_t*>(g.C);
+            Cp[off] = g.accumulate ? Cp[off] + (int64_t)val : (int64_t)val;
           } else {
-            int32_t* C = reinterpret_cast<int32_t*>(g.C);
-            C[off] = g.accumulate ? (int32_t)((uint32_t)C[off] + (uint32_t)val) : val;
+            int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
+            Cp[off] = g.accumulate ? (int32_t)((uint32_t)Cp[off] + (uint32_t)val) : val;
           }
         }
       }
 }
+
+// The tile configurations the launcher chooses from.
+using Cfg4w128x64 = Cfg<2, 2, 4, 2>;  // 256 x 128, 4 waves (1 per SIMD)
+using Cfg8w64x64 = Cfg<4, 2, 2, 2>;   // 256 x 128, 8 waves (2 per SIMD)
+using Cfg8w64x96 = Cfg<4, 2, 2, 3>;   // 256 x 192, 8 waves (2 per SIMD)
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;
@@ -357,6 +398,52 @@ __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, in
     const int64_t r = i / row_bytes, c = i - r * row_bytes;
     C[r * ld_bytes + c] = 0;
   }
+}
+
+// Tile configuration for a problem.  AWE_GEMM_CFG (0: 256x128 with 4 waves,
+// 1: 256x128 with 8 waves, 2: 256x192 with 8 waves) overrides the choice;
+// otherwise the wider tile is taken unless its coarser tiles leave more of the
+// last round of workgroups idle.
+int choose_cfg(int64_t M, int64_t N) {
+  const char* e = getenv("AWE_GEMM_CFG");
+  const int forced = e ? atoi(e) : -1;
+  if (forced >= 0 && forced <= 2) return forced;
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      cus = v;
+  }
+  const int64_t tm = (M + 255) / 256;
+  const double t128 = (double)((tm * ((N + 127) / 128) + cus - 1) / cus) * 2.0;
+  const double t192 = (double)((tm * ((N + 191) / 192) + cus - 1) / cus) * 3.0 / 1.2;
+  return t192 < t128 ? 2 : 1;
+}
+
+template <class C>
+awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
+  const int64_t tiles_m = (L.M + C::BM - 1) / C::BM, tiles_n = (L.N + C::BN - 1) / C::BN;
+  g.tiles_m = (int32_t)tiles_m;
+  g.tiles_n = (int32_t)tiles_n;
+  const int64_t blocks = tiles_m * tiles_n;
+  if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<C>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+    if (e != hipSuccess) {
+      set_error(std::string("gemm LDS attribute: ") + hipGetErrorString(e));
+      return AWE_ERR_HIP;
+    }
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(gemm_kernel<C>, dim3((unsigned)blocks), dim3(C::THREADS), C::LDS_BYTES, stream, g);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) {
+    set_error(std::string("gemm launch: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  return AWE_OK;
 }
 
 }  // namespace
@@ -429,28 +516,11 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.accumulate = L.accumulate;
   g.log2D = L.log2D;
   g.modulus = L.modulus;
-  const int64_t tiles_m = (L.M + BM - 1) / BM, tiles_n = (L.N + BN - 1) / BN;
-  g.tiles_m = (int32_t)tiles_m;
-  g.tiles_n = (int32_t)tiles_n;
-  const int64_t blocks = tiles_m * tiles_n;
-  if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, GEMM_LDS_BYTES);
-    if (e != hipSuccess) {
-      set_error(std::string("gemm LDS attribute: ") + hipGetErrorString(e));
-      return AWE_ERR_HIP;
-    }
-    attr_set = true;
+  switch (choose_cfg(L.M, L.N)) {
+    case 0: return launch_tile<Cfg4w128x64>(g, L, stream);
+    case 2: return launch_tile<Cfg8w64x96>(g, L, stream);
+    default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
-  hipLaunchKernelGGL(gemm_kernel, dim3((unsigned)blocks), dim3(256), GEMM_LDS_BYTES, stream, g);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) {
-    set_error(std::string("gemm launch: ") + hipGetErrorString(err));
-    return AWE_ERR_HIP;
-  }
-  return AWE_OK;
 }
 
 }  // namespace awe

@@ -157,3 +157,20 @@ def test_mod_forced_segments():
     awe.gemm_planes(awe.ENC_MOD, m, 64, 200, 3000, pa, pb, C, 200, awe.I32, 256)
     torch.cuda.synchronize()
     assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
+
+
+@pytest.mark.parametrize("cfg", ["0", "1", "2"])
+@pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13])
+def test_every_tile_configuration(monkeypatch, cfg, enc):
+    # AWE_GEMM_CFG forces one of the GEMM's tile configurations (256x128 on 4 or 8
+    # waves, 256x192 on 8 waves); every one must give the exact product
+    monkeypatch.setenv("AWE_GEMM_CFG", cfg)
+    M, N, K = 300, 420, 1100
+    A, B = _operands(enc, M, N, K, seed=int(cfg) + 40)
+    C = _run_exact(enc, A, B)
+    assert np.array_equal(C.astype(np.int64), og.gemm_i64(A, B))
+    m = 89
+    Ar, Br = inputs.residue_pair(130, 270, 600, m)
+    Cm = awe.matmul_mod(m, to_dev(Ar), to_dev(Br))
+    torch.cuda.synchronize()
+    assert np.array_equal(Cm.cpu().numpy(), og.gemm_mod(m, Ar, Br))

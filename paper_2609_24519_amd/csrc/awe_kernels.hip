@@ -97,20 +97,19 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
 // (8 bytes of registers), so the register file bounds the tile; the operand
 // bytes each CU must pull through its L1 per MFMA fall as the tile grows.
 // ---------------------------------------------------------------------------
-#ifndef AWE_GEMM_NSTAGE
-#define AWE_GEMM_NSTAGE 4
-#endif
-constexpr int NSTAGE = AWE_GEMM_NSTAGE;  // LDS ring depth
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
-template <int WM_, int WN_, int BMW_, int BNW_>
+template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
+  static constexpr int KST = KST_;        // k-steps (64 reduction indices each) per stage
+  static constexpr int KT = 64 * KST;     // reduction indices per stage
+  static constexpr int NSTAGE = NSTAGE_;  // LDS ring depth
   static constexpr int NW = WM * WN;
   static constexpr int THREADS = 64 * NW;
   static constexpr int BM = WM * BMW * 32, BN = WN * BNW * 32;
-  static constexpr int A_BRICKS = (BM / kBrickRows) * 2;  // per stage: row blocks x 2 k-steps
-  static constexpr int B_BRICKS = (BN / kBrickRows) * 2;
+  static constexpr int A_BRICKS = (BM / kBrickRows) * KST;  // per stage: row blocks x k-steps
+  static constexpr int B_BRICKS = (BN / kBrickRows) * KST;
   static constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * kBrickBytes;
   static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES;
   // copies per wave and stage: A bricks evenly, B bricks round-robin (the first
@@ -118,6 +117,7 @@ struct Cfg {
   static constexpr int A_PW = A_BRICKS / NW;
   static constexpr int B_LO = B_BRICKS / NW, B_XTRA = B_BRICKS % NW;
   static_assert(A_BRICKS % NW == 0, "A bricks must split evenly over the waves");
+  static_assert(kKPad % KT == 0, "a stage must divide the reduction padding");
 };
 
 struct GemmArgs {
@@ -126,8 +126,8 @@ struct GemmArgs {
   int64_t stride_a, stride_b;
   int32_t rba, rbb;  // row blocks of the A and B planes
   int32_t KS;        // bricks along K per row block
-  int32_t t_begin, t_end;
-  int32_t ts;        // fold segment in k-tiles
+  int32_t t_begin, t_end;  // stage range of this launch (stages of KT reduction indices)
+  int32_t ts;        // fold segment in stages
   int32_t r;
   uint64_t pidx_a, pidx_b;  // plane of product k in bits 4k .. 4k+3 (kept in SGPRs: no loads in the loop)
   int32_t fold_ell[kMaxProducts];
@@ -194,27 +194,27 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 __device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // The copies of one stage: wave w takes A bricks A_PW w .. A_PW w + A_PW - 1
-// and B bricks w, w + NW, ... (brick id = 2 * row block + k-step).
+// and B bricks w, w + NW, ... (brick id = KST * row block + k-step).
 template <class C>
 __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
                                            int tm, int tn, int wave, int lane) {
   const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u), kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
   // k-step major planes: the bricks of one k-step for consecutive row blocks are adjacent
-  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * 2 * g.rba * kBrickBytes;
-  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * 2 * g.rbb * kBrickBytes;
+  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * C::KST * g.rba * kBrickBytes;
+  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KST * g.rbb * kBrickBytes;
   const uint32_t voff = lane * 16;
 #pragma unroll
   for (int i = 0; i < C::A_PW; ++i) {
     const int id = wave * C::A_PW + i;
-    const int rb = min(tm * (C::BM / kBrickRows) + (id >> 1), g.rba - 1);
-    dma_brick(pa + ((int64_t)(id & 1) * g.rba + rb) * kBrickBytes, voff, stage_lds + id * kBrickBytes);
+    const int rb = min(tm * (C::BM / kBrickRows) + id / C::KST, g.rba - 1);
+    dma_brick(pa + ((int64_t)(id % C::KST) * g.rba + rb) * kBrickBytes, voff, stage_lds + id * kBrickBytes);
   }
 #pragma unroll
   for (int i = 0; i < C::B_LO + (C::B_XTRA ? 1 : 0); ++i) {
     const int id = wave + i * C::NW;
     if (i == C::B_LO && wave >= C::B_XTRA) break;
-    const int cb = min(tn * (C::BN / kBrickRows) + (id >> 1), g.rbb - 1);
-    dma_brick(pb + ((int64_t)(id & 1) * g.rbb + cb) * kBrickBytes, voff,
+    const int cb = min(tn * (C::BN / kBrickRows) + id / C::KST, g.rbb - 1);
+    dma_brick(pb + ((int64_t)(id % C::KST) * g.rbb + cb) * kBrickBytes, voff,
               stage_lds + (C::A_BRICKS + id) * kBrickBytes);
   }
 }
@@ -236,10 +236,10 @@ __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, in
                                            int wn, int lane) {
 #pragma unroll
   for (int i = 0; i < C::BMW; ++i)
-    f.a[i] = frag(stage + ((wm * C::BMW + i) * 2 + ks) * kBrickBytes + lane * 16);
+    f.a[i] = frag(stage + ((wm * C::BMW + i) * C::KST + ks) * kBrickBytes + lane * 16);
 #pragma unroll
   for (int j = 0; j < C::BNW; ++j)
-    f.b[j] = frag(stage + (C::A_BRICKS + (wn * C::BNW + j) * 2 + ks) * kBrickBytes + lane * 16);
+    f.b[j] = frag(stage + (C::A_BRICKS + (wn * C::BNW + j) * C::KST + ks) * kBrickBytes + lane * 16);
 }
 
 __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
@@ -289,6 +289,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
         iacc[i][j][v] = 0;
       }
 
+  constexpr int NSTAGE = C::NSTAGE;
   Cursor nxt{0, g.t_begin, g.t_begin, min(g.t_begin + g.ts, g.t_end)};
   // Prologue: stages 0 .. NSTAGE-1 fill the whole ring.
 #pragma unroll
@@ -298,14 +299,15 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
   }
   wait_stages<C, NSTAGE - 1>(wave);
   block_barrier();
-  Frags<C> f0, f1;
-  read_frags<C>(f0, smem, 0, wm, wn, lane);
+  Frags<C> f[2];
+  read_frags<C>(f[0], smem, 0, wm, wn, lane);
 
-  // Stage s: F1 <- (s, k-step 1); MFMAs (s, 0) on F0; wait until stage s+1 has
-  // landed and this wave's reads of stage s are done; barrier; refill stage s's
-  // buffer with stage s+NSTAGE; F0 <- (s+1, 0); MFMAs (s, 1) on F1.  The
-  // barrier sits between two groups of MFMAs, and the next stage's first
-  // fragments are in flight while the second group executes.
+  // Stage s, k-steps 0 .. KST-1: while the MFMAs of k-step ks run on one
+  // fragment set, the next k-step's fragments are read into the other.  Before
+  // the last k-step: wait until stage s+1 has landed and this wave's reads of
+  // stage s are done, barrier, refill stage s's buffer with stage s+NSTAGE and
+  // read the first fragments of stage s+1.  The barrier sits between two groups
+  // of MFMAs.
   int buf = 0;
   for (int cs = g.t_begin; cs < g.t_end; cs += g.ts) {
     const int ce = min(cs + g.ts, g.t_end);
@@ -313,25 +315,27 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
       for (int t = cs; t < ce; ++t) {
         const uint32_t cur_off = buf * C::STAGE_BYTES;
         buf = buf + 1 == NSTAGE ? 0 : buf + 1;
-        read_frags<C>(f1, smem + cur_off, 1, wm, wn, lane);
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < C::BMW; ++i)
+        for (int ks = 0; ks < C::KST; ++ks) {
+          Frags<C>& cur = f[ks & 1];
+          Frags<C>& nx = f[(ks + 1) & 1];
+          if (ks + 1 < C::KST) {
+            read_frags<C>(nx, smem + cur_off, ks + 1, wm, wn, lane);
+          } else {
+            wait_stages<C, NSTAGE - 2>(wave);
+            wait_lgkm0();
+            block_barrier();
+            load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
+            cursor_next(nxt, g);
+            read_frags<C>(nx, smem + buf * C::STAGE_BYTES, 0, wm, wn, lane);
+          }
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], f0.a[i], f0.b[j]);
-        __builtin_amdgcn_sched_barrier(0);
-        wait_stages<C, NSTAGE - 2>(wave);
-        wait_lgkm0();
-        block_barrier();
-        load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
-        cursor_next(nxt, g);
-        read_frags<C>(f0, smem + buf * C::STAGE_BYTES, 0, wm, wn, lane);
-        __builtin_amdgcn_sched_barrier(0);
+          for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
-        for (int i = 0; i < C::BMW; ++i)
-#pragma unroll
-          for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], f1.a[i], f1.b[j]);
-        __builtin_amdgcn_sched_barrier(0);
+            for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], cur.a[i], cur.b[j]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
       if ((g.fold_mask >> p) & 1u) {
         const int32_t l = g.fold_ell[p];
@@ -386,10 +390,13 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
       }
 }
 
-// The tile configurations the launcher chooses from.
-using Cfg4w128x64 = Cfg<2, 2, 4, 2>;  // 256 x 128, 4 waves (1 per SIMD)
-using Cfg8w64x64 = Cfg<4, 2, 2, 2>;   // 256 x 128, 8 waves (2 per SIMD)
-using Cfg8w64x96 = Cfg<4, 2, 2, 3>;   // 256 x 192, 8 waves (2 per SIMD)
+// The tile configurations the launcher chooses from: waves (M x N), 32x32
+// blocks per wave (M x N), k-steps per stage, LDS ring depth.
+using Cfg4w128x64 = Cfg<2, 2, 4, 2, 2, 4>;   // 256 x 128, 4 waves (1 per SIMD)
+using Cfg8w64x64 = Cfg<4, 2, 2, 2, 2, 4>;    // 256 x 128, 8 waves (2 per SIMD)
+using Cfg8w64x96 = Cfg<4, 2, 2, 3, 2, 4>;    // 256 x 192, 8 waves (2 per SIMD)
+using Cfg4w128x64k4 = Cfg<2, 2, 4, 2, 4, 3>; // 256 x 128, 4 waves, 4 k-steps per stage
+using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps per stage
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;
@@ -401,13 +408,14 @@ __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, in
 }
 
 // Tile configuration for a problem.  AWE_GEMM_CFG (0: 256x128 with 4 waves,
-// 1: 256x128 with 8 waves, 2: 256x192 with 8 waves) overrides the choice;
+// 1: 256x128 with 8 waves, 2: 256x192 with 8 waves, 3 and 4: as 0 and 1 with
+// 4 k-steps per stage) overrides the choice;
 // otherwise the wider tile is taken unless its coarser tiles leave more of the
 // last round of workgroups idle.
 int choose_cfg(int64_t M, int64_t N) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
-  if (forced >= 0 && forced <= 2) return forced;
+  if (forced >= 0 && forced <= 4) return forced;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) {
     int v = 0;
@@ -423,6 +431,9 @@ int choose_cfg(int64_t M, int64_t N) {
 template <class C>
 awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
   const int64_t tiles_m = (L.M + C::BM - 1) / C::BM, tiles_n = (L.N + C::BN - 1) / C::BN;
+  g.t_begin = (int32_t)(L.k_begin / C::KT);
+  g.t_end = (int32_t)(L.k_end / C::KT);
+  g.ts = (int32_t)(L.k_seg / C::KT);
   g.tiles_m = (int32_t)tiles_m;
   g.tiles_n = (int32_t)tiles_n;
   const int64_t blocks = tiles_m * tiles_n;
@@ -497,9 +508,6 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.rbb = (int32_t)((L.N + kBrickRows - 1) / kBrickRows);
   const int64_t kp = (L.K + kKPad - 1) / kKPad * kKPad;
   g.KS = (int32_t)(kp / kBrickK);
-  g.t_begin = (int32_t)(L.k_begin / kKPad);
-  g.t_end = (int32_t)(L.k_end / kKPad);
-  g.ts = (int32_t)(L.k_seg / kKPad);
   g.r = L.r;
   g.pidx_a = g.pidx_b = 0;
   for (int k = 0; k < L.r; ++k) {
@@ -519,6 +527,8 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   switch (choose_cfg(L.M, L.N)) {
     case 0: return launch_tile<Cfg4w128x64>(g, L, stream);
     case 2: return launch_tile<Cfg8w64x96>(g, L, stream);
+    case 3: return launch_tile<Cfg4w128x64k4>(g, L, stream);
+    case 4: return launch_tile<Cfg8w64x64k4>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }

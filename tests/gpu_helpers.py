@@ -1,7 +1,8 @@
 """Helpers for the GPU tests: device upload and decoding of the stored plane layout.
 
 The decoder follows the plane layout that include/awe.h documents (1 KiB
-bricks of 32 rows x 64 reduction indices, lane L = 32 h + t owning row t and
+bricks of 32 rows x 64 reduction indices, stored k-step major, K padded to
+256, lane L = 32 h + t owning row t and
 indices 32 h .. 32 h + 31, two E2M1 codes per byte, low nibble first).
 """
 import numpy as np
@@ -24,7 +25,7 @@ def to_dev(x):
 def decode_planes(buf, nplanes, rows, K):
     """Stored planes (uint8 numpy) -> int64 array [nplanes, rows, K] of doubled values; padding checked."""
     R32 = -(-rows // 32)
-    Kp = -(-K // 128) * 128
+    Kp = -(-K // 256) * 256
     KS = Kp // 64
     stride = R32 * KS * 1024
     # k-step major: brick (rb, ks) at (ks * R32 + rb) * 1024

@@ -46,7 +46,7 @@ def test_encoding_info_matches_oracle(name):
     assert (info["c_a"], info["c_b"]) == (c_a, c_b)
     assert info["n_g"] == s.n_g
     assert info["k_star"] == sc.k_star(s.n_g, c_a, c_b)
-    assert info["k_seg"] % 128 == 0 and 0 < info["k_seg"] <= info["k_star"]
+    assert info["k_seg"] % 256 == 0 and 0 < info["k_seg"] <= info["k_star"]
     assert info["k_seg"] * s.n_g * c_a * c_b < 2 ** 23
     assert info["range_a"] == s.range_a and info["range_b"] == s.range_b
 
@@ -99,8 +99,9 @@ def test_selected_moduli_have_schemes(paper):
 def test_plane_bytes():
     for enc, npl in ((awe.ENC_AWE6, 6), (awe.ENC_B13, 3), (awe.ENC_AWE4, 4)):
         assert awe.plane_bytes(enc, 0, awe.SIDE_A, 8192, 8192) == npl * 8192 * 8192 // 2
-        # ragged: rows up to a multiple of 32, K up to a multiple of 128
+        # ragged: rows up to a multiple of 32, K up to a multiple of 256
         assert awe.plane_bytes(enc, 0, awe.SIDE_A, 33, 129) == npl * 64 * 256 // 2
+        assert awe.plane_bytes(enc, 0, awe.SIDE_A, 33, 257) == npl * 64 * 512 // 2
         assert awe.plane_bytes(enc, 0, awe.SIDE_A, 0, 100) == 0
     ws = awe.workspace_bytes(awe.ENC_AWE4, 0, 100, 50, 300)
     a = awe.plane_bytes(awe.ENC_AWE4, 0, awe.SIDE_A, 100, 300)
@@ -135,10 +136,10 @@ def test_error_paths_host_only():
                             fake, 1 << 40, None, None) == awe.ERR_INVALID_VALUE
     assert L.awe_gemm_exact(awe.ENC_AWE6, 64, 64, 64, fake, 64, fake, 64, fake, 64, 7,
                             fake, 1 << 40, None, None) == awe.ERR_INVALID_VALUE
-    # fold segment must be a multiple of 128 within the encoding's bound
+    # fold segment must be a multiple of 256 within the encoding's bound
     assert L.awe_gemm_planes(awe.ENC_AWE6, 0, 64, 64, 1024, fake, fake, fake, 64, awe.I32, 100,
                              None) == awe.ERR_INVALID_VALUE
-    big = awe.get_encoding_info(awe.ENC_AWE6)["k_seg"] + 128
+    big = awe.get_encoding_info(awe.ENC_AWE6)["k_seg"] + 256
     assert L.awe_gemm_planes(awe.ENC_AWE6, 0, 64, 64, 1024, fake, fake, fake, 64, awe.I32, big,
                              None) == awe.ERR_INVALID_VALUE
     # residues are written as int32 only

@@ -87,7 +87,7 @@ def _planes(enc, m, A, B):
 
 
 @pytest.mark.parametrize("enc", EXACT)
-@pytest.mark.parametrize("kseg", [128, 384, 1024])
+@pytest.mark.parametrize("kseg", [256, 512, 1024])
 def test_forced_fold_segments(enc, kseg):
     M, N, K = 130, 260, 2000
     A, B = _operands(enc, M, N, K, seed=11)
@@ -111,7 +111,7 @@ def test_ldc_larger_than_n():
 
 
 def test_multi_launch_reduction():
-    # K beyond what one launch's int32 accumulator may hold (130944 for int8 x int8): the
+    # K beyond what one launch's int32 accumulator may hold (130816 for int8 x int8): the
     # host splits the reduction and the launches add into the int64 output
     M, N, K = 40, 72, 300_000
     A, B = inputs.int8_pair(M, N, K, seed=9)
@@ -120,8 +120,9 @@ def test_multi_launch_reduction():
 
 
 def test_fp32_partial_near_bound():
-    # AWE4: c_A c_B = 24, fold segment 349440, so one FP32 partial reaches 24 * 349440 = 8386560,
-    # just below 2^23; constant operands put every product at its largest magnitude
+    # AWE4: c_A c_B = 24, fold segment 349440 (a multiple of 256), so one FP32 partial reaches
+    # 24 * 349440 = 8386560, just below 2^23; constant operands put every product at its largest
+    # magnitude
     info = awe.get_encoding_info(awe.ENC_AWE4)
     K = info["k_seg"]
     loa, TA = awe.get_plane_table(awe.ENC_AWE4, 0, awe.SIDE_A)
@@ -159,11 +160,12 @@ def test_mod_forced_segments():
     assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
 
 
-@pytest.mark.parametrize("cfg", ["0", "1", "2"])
+@pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4"])
 @pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13])
 def test_every_tile_configuration(monkeypatch, cfg, enc):
     # AWE_GEMM_CFG forces one of the GEMM's tile configurations (256x128 on 4 or 8
-    # waves, 256x192 on 8 waves); every one must give the exact product
+    # waves with 2 or 4 k-steps per stage, 256x192 on 8 waves); every one must give
+    # the exact product
     monkeypatch.setenv("AWE_GEMM_CFG", cfg)
     M, N, K = 300, 420, 1100
     A, B = _operands(enc, M, N, K, seed=int(cfg) + 40)

@@ -8,9 +8,10 @@ encode A, encode B, the r FP4 products with their fused reconstruction
 The workload is M = N = K = 8192 with int8 entries uniform in [-128, 127]
 (seed 0) and int32 C.  Printed: one JSON line with the end-to-end exact TOPS
 as ``value``, the roofline of the dominant kernel (the GEMM) from HIP events
-on its stream, the 9-product base-13 baseline and the native INT8 MFMA GEMM
-(hipBLASLt through torch._int_mm) timed in the same run as context, and the
-oracle timed on the host's cores on a bounded sample.
+on its stream, the 9-product base-13 baseline, the native INT8 MFMA GEMM
+(hipBLASLt through torch._int_mm) and the sustained rate of the FP4 MFMA alone
+timed in the same run as context, and the oracle timed on the host's cores on
+a bounded sample.
 """
 import argparse
 import json
@@ -42,8 +43,8 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(the sharding design is described in DESIGN.md); use --gpus 1", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path; use --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -147,6 +148,11 @@ def main():
             line["int8_mfma_context"]["equal_to_exact_C"] = bool(torch.equal(Ci, C))
         except Exception as ex:  # noqa: BLE001 - context only
             line["int8_mfma_context"] = {"error": str(ex)[:200]}
+    if not args.no_context:
+        probe = mfma_sustained()
+        if probe:
+            probe["gemm_frac_of_8_wave_rate"] = round(gemm_tflops / probe["8_waves_per_cu_TFLOPs"], 4)
+        line["mfma_sustained"] = probe
     if args.calibrate_copy:
         src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -157,6 +163,29 @@ def main():
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(A_h, B_h)
     print(json.dumps(line), flush=True)
+
+
+def mfma_sustained(iters=20000):
+    """Dense FP4 rate of the GEMM's MFMA issued back to back from registers with 8 and
+    with 4 waves per compute unit (libawe_probe.so): the practical ceiling, at the clock
+    the chip holds under full MFMA load, next to the data-sheet peak."""
+    import ctypes
+
+    from paper_2609_24519_amd import build as hip_build
+
+    if not os.path.exists(hip_build.PROBE_LIB):
+        return None
+    lib = ctypes.CDLL(hip_build.PROBE_LIB)
+    lib.awe_mfma_peak.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    out = {}
+    for waves in (8, 4):
+        tf = ctypes.c_double(0.0)
+        rc = lib.awe_mfma_peak(waves, iters, ctypes.byref(tf))
+        if rc != 0:
+            return {"error": "HIP error %d" % rc}
+        out["%d_waves_per_cu_TFLOPs" % waves] = round(tf.value, 1)
+        out["%d_waves_frac_of_peak" % waves] = round(tf.value / FP4_PEAK_TFLOPS, 4)
+    return out
 
 
 def gemm_traffic():

@@ -30,7 +30,7 @@
  * Stored plane layout (the output of awe_encode, the input of
  * awe_gemm_planes).  One side holds P planes back to back; plane p starts at
  * byte p * stride, stride = ceil(rows/32) * (Kp/64) * 1024 with
- * Kp = K rounded up to a multiple of 256.  A plane is a grid of 1024-byte
+ * Kp = K rounded up to a multiple of AWE_K_PAD (256).  A plane is a grid of 1024-byte
  * bricks, brick (rb, ks) at byte (ks * ceil(rows/32) + rb) * 1024 (k-step
  * major: the bricks of one k-step for consecutive row blocks are adjacent),
  * covering rows (A: rows of A; B: columns of B) rb*32 .. rb*32+31 and
@@ -83,6 +83,7 @@ typedef enum awe_dtype { AWE_I32 = 0, AWE_I64 = 1 } awe_dtype;
 #define AWE_MAX_LIMBS 4
 #define AWE_MAX_PLANES 8
 #define AWE_MAX_PRODUCTS 16
+#define AWE_K_PAD 256 /* stored planes pad the reduction length to a multiple of this */
 
 /* A configuration record (Alg. 1 input): weights, planes, reconstruction and bounds. */
 typedef struct awe_encoding_info {
@@ -105,7 +106,7 @@ typedef struct awe_encoding_info {
   int64_t ell[AWE_MAX_PRODUCTS];  /* reconstruction numerators ell_k (mod m: balanced residues) */
   int32_t group[AWE_MAX_PRODUCTS];/* accumulator shared by product k (equal ell_k) */
   int64_t k_star;                 /* floor(2^24 / (n_g c_a c_b)), Sec. 3.4 */
-  int64_t k_seg;                  /* default fold segment of the GEMM (<= k_star), multiple of 256 */
+  int64_t k_seg;                  /* default fold segment of the GEMM (<= k_star), multiple of AWE_K_PAD */
 } awe_encoding_info;
 
 /* Host.  The configuration record of an encoding (for AWE_ENC_MOD, of modulus m; the
@@ -136,7 +137,7 @@ awe_status awe_encode(awe_encoding enc, int32_t modulus, awe_side side,
    C = (sum_k ell_k P_k) / D exactly, or (sum_k lambda_k P_k) mod m in [0, m) for
    AWE_ENC_MOD (then c_type must be AWE_I32).  planes_a / planes_b come from awe_encode
    with the same M, N, K.  k_seg: fold segment length (0 = the encoding's default;
-   otherwise a positive multiple of 256 no larger than the default): every FP32 partial
+   otherwise a positive multiple of AWE_K_PAD no larger than the default): every FP32 partial
    covers at most k_seg reduction indices and is then added to an integer accumulator. */
 awe_status awe_gemm_planes(awe_encoding enc, int32_t modulus, int64_t M, int64_t N, int64_t K,
                            const void* planes_a, const void* planes_b,

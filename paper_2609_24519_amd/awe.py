@@ -26,6 +26,7 @@ SIDE_A, SIDE_B = 0, 1
 I32, I64 = 0, 1
 
 MAX_LIMBS, MAX_PLANES, MAX_PRODUCTS = 4, 8, 16
+K_PAD = 256  # AWE_K_PAD: stored planes pad the reduction length to a multiple of this
 
 
 class EncodingInfo(ctypes.Structure):

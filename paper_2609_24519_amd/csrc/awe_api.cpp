@@ -36,7 +36,7 @@ size_t side_bytes(const Scheme& s, bool sideA, int64_t rows, int64_t K) {
   return (size_t)(sideA ? s.na : s.nb) * (size_t)plane_stride_bytes(rows, K);
 }
 
-// Largest reduction length (multiple of 256) one GEMM launch may cover so that
+// Largest reduction length (multiple of kKPad) one GEMM launch may cover so that
 // the int32 accumulator's true value fits: |D C| <= D max|A| max|B| K for an
 // exact scheme, |sum lambda_k P_k| <= sum|lambda_k| c_A c_B K for a congruence.
 int64_t launch_k_limit(const Scheme& s) {
@@ -70,7 +70,8 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
   if (k_seg == 0) k_seg = s.k_seg;
   if (k_seg < 0 || k_seg % kKPad != 0 || k_seg > s.k_seg)
     return fail(AWE_ERR_INVALID_VALUE,
-                "k_seg must be a positive multiple of 256 no larger than " + std::to_string(s.k_seg));
+                "k_seg must be a positive multiple of " + std::to_string(kKPad) +
+                    " no larger than " + std::to_string(s.k_seg));
 
   GemmLaunch L{};
   L.planes_a = reinterpret_cast<const uint8_t*>(pa);

@@ -15,7 +15,7 @@ constexpr int kMaxProducts = AWE_MAX_PRODUCTS;
 constexpr int kBrickRows = 32;     // rows (A) or columns (B) per brick
 constexpr int kBrickK = 64;        // reduction indices per brick
 constexpr int kBrickBytes = 1024;  // 32 x 64 E2M1 codes, 2 per byte
-constexpr int kKPad = 256;         // the reduction length is padded to this multiple
+constexpr int kKPad = AWE_K_PAD;   // the reduction length is padded to this multiple
 
 // LUT entry flag: the input byte is outside the encoding's range.
 constexpr uint32_t kLutInvalid = 0x80000000u;

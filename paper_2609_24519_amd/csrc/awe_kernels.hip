@@ -409,9 +409,10 @@ __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, in
 
 // Tile configuration for a problem.  AWE_GEMM_CFG (0: 256x128 with 4 waves,
 // 1: 256x128 with 8 waves, 2: 256x192 with 8 waves, 3 and 4: as 0 and 1 with
-// 4 k-steps per stage) overrides the choice;
-// otherwise the wider tile is taken unless its coarser tiles leave more of the
-// last round of workgroups idle.
+// 4 k-steps per stage) overrides the choice.  Otherwise: 256x128 on 8 waves
+// with 4 k-steps per stage, or 256x192 when its rounds of workgroups (each
+// about 1.37 times as long as a 256x128 round, measured at 8192^3) finish
+// sooner, which happens when the 128-wide tiling leaves a ragged last round.
 int choose_cfg(int64_t M, int64_t N) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
@@ -423,9 +424,9 @@ int choose_cfg(int64_t M, int64_t N) {
       cus = v;
   }
   const int64_t tm = (M + 255) / 256;
-  const double t128 = (double)((tm * ((N + 127) / 128) + cus - 1) / cus) * 2.0;
-  const double t192 = (double)((tm * ((N + 191) / 192) + cus - 1) / cus) * 3.0 / 1.2;
-  return t192 < t128 ? 2 : 1;
+  const double t128 = (double)((tm * ((N + 127) / 128) + cus - 1) / cus);
+  const double t192 = (double)((tm * ((N + 191) / 192) + cus - 1) / cus) * 1.37;
+  return t192 < t128 ? 2 : 4;
 }
 
 template <class C>

@@ -1,0 +1,67 @@
+// Sustained rate of the GEMM's instruction, the scaled 32x32x64 MFMA with E2M1
+// operands and FP32 accumulation, when every wave issues independent MFMAs
+// from registers and touches no memory in the loop.  It gives the practical
+// ceiling the GEMM kernel is compared with next to the data-sheet peak (which
+// assumes the peak engine clock under full MFMA load).  Benchmark helper only:
+// not part of the product path.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int kMfmaPerIter = 16;
+constexpr double kFlopPerMfma = 2.0 * 32 * 32 * 64;
+
+__global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float* sink) {
+  v16f c[4] = {};
+  const v8i a = {(int)threadIdx.x, 0x11111111, 0x22222222, 0x33333333, 0, 0, 0, 0};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int m = 0; m < kMfmaPerIter; ++m)
+      c[m & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, a, c[m & 3], 4, 4, 0, 0x80808080,
+                                                                0, 0x80808080);
+  }
+  const float s = c[0][0] + c[1][0] + c[2][0] + c[3][0];
+  if (s == 0.125f) sink[blockIdx.x] = s;  // never true in practice; keeps the MFMAs live
+}
+
+}  // namespace
+
+// Runs one workgroup of `waves_per_cu` waves (1..8) per compute unit for
+// `iters` iterations of 16 MFMAs per wave after one warm-up launch, and
+// writes the achieved dense FP4 rate in TFLOP/s.  Returns 0, or a HIP error code.
+extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
+  if (waves_per_cu < 1 || waves_per_cu > 8 || iters < 1 || tflops == nullptr) return (int)hipErrorInvalidValue;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return (int)e;
+  float* sink = nullptr;
+  if ((e = hipMalloc(&sink, sizeof(float) * cus)) != hipSuccess) return (int)e;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  float ms = 0.f;
+  const dim3 grid(cus), block(64 * waves_per_cu);
+  if ((e = hipEventCreate(&e0)) == hipSuccess && (e = hipEventCreate(&e1)) == hipSuccess) {
+    hipLaunchKernelGGL(mfma_peak_kernel, grid, block, 0, nullptr, iters, sink);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipEventRecord(e0, nullptr);
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(mfma_peak_kernel, grid, block, 0, nullptr, iters, sink);
+      e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = hipEventRecord(e1, nullptr);
+    if (e == hipSuccess) e = hipEventSynchronize(e1);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  }
+  if (e0) hipEventDestroy(e0);
+  if (e1) hipEventDestroy(e1);
+  hipFree(sink);
+  if (e != hipSuccess) return (int)e;
+  const double flop = (double)cus * waves_per_cu * iters * kMfmaPerIter * kFlopPerMfma;
+  *tflops = flop / ((double)ms * 1e-3) / 1e12;
+  return 0;
+}

@@ -3,6 +3,8 @@
     python -m paper_2609_24519_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>"
     python -m paper_2609_24519_amd.profiling traffic <fetch_counter_collection.csv> \\
         <write_counter_collection.csv> <out.json> <out.md> "<fetch command>" "<write command>"
+    python -m paper_2609_24519_amd.profiling counters <out.md> <fp4_flop_per_gemm> \\
+        "<command>" <counter_collection.csv> [<counter_collection.csv> ...]
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a short
 Markdown table.  ``traffic`` takes two ``--pmc`` runs (FETCH_SIZE, then
@@ -11,6 +13,10 @@ device copy of a known size (``bench.py --calibrate-copy``), scales every
 kernel's counters by what the counters read for that copy, and records the
 per-dispatch HBM bytes of the GEMM together with a hash of the kernel source
 they were taken on, so that a later change to the kernel makes them stale.
+``counters`` summarises one or more ``--pmc`` passes over the same command:
+per kernel the FP4 MFMA operation count (checked against the algorithmic
+r 2MNK), MFMA busy cycles, LDS bank conflicts and activity, L2 hit rate and
+request latency.
 """
 import csv
 import hashlib
@@ -90,10 +96,82 @@ def traffic(fetch_csv, write_csv, out_json, out_md, fetch_cmd, write_cmd):
         f.write("\n".join(lines) + "\n")
 
 
+def _dispatch_counters(paths):
+    """{kernel: {"n": dispatches, counter: mean per dispatch, "_res": resources}} over CSV files."""
+    per = {}
+    for path in paths:
+        seen = {}
+        for r in csv.DictReader(open(path)):
+            key = (path, r["Dispatch_Id"])
+            d = seen.setdefault(key, {"kernel": r["Kernel_Name"], "vals": {}, "res": {
+                "arch_vgpr": r.get("Arch_VGPR_Count", r.get("VGPR_Count", "")),
+                "accum_vgpr": r.get("Accum_VGPR_Count", ""), "sgpr": r.get("SGPR_Count", ""),
+                "lds_bytes": r.get("LDS_Block_Size", ""), "scratch": r.get("Scratch_Size", ""),
+                "ns": float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+                if r.get("End_Timestamp") else 0.0}})
+            d["vals"][r["Counter_Name"]] = d["vals"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        for d in seen.values():
+            k = per.setdefault(_short(d["kernel"]), {"sums": {}, "cnt": {}, "res": d["res"], "ns": []})
+            k["ns"].append(d["res"]["ns"])
+            for c, v in d["vals"].items():
+                k["sums"][c] = k["sums"].get(c, 0.0) + v
+                k["cnt"][c] = k["cnt"].get(c, 0) + 1
+    out = {}
+    for name, k in per.items():
+        mean = {c: k["sums"][c] / k["cnt"][c] for c in k["sums"]}
+        mean["_ns"] = sum(k["ns"]) / len(k["ns"])
+        mean["_res"] = k["res"]
+        out[name] = mean
+    return out
+
+
+def counters(out_md, fp4_flop, command, paths):
+    fp4_flop = float(fp4_flop)
+    data = _dispatch_counters(paths)
+    lines = ["# GEMM counters (rocprofv3 --pmc, one pass per counter group)", "",
+             "Command (each pass): `%s`" % command, "",
+             "Per-dispatch means.  MOPS counts units of 512 FLOP; a 32x32x64 FP4 MFMA is",
+             "256 MOPS and keeps its SIMD busy 32 cycles.  Expected FP4 work per GEMM",
+             "dispatch: r 2MNK = %.4g FLOP." % fp4_flop, ""]
+    for name, m in data.items():
+        if "gemm_kernel" not in name:
+            continue
+        lines += ["## %s" % name, "", "| quantity | value |", "|---|---|"]
+        lines.append("| duration (us) | %.1f |" % (m["_ns"] / 1e3))
+        mops = m.get("SQ_INSTS_VALU_MFMA_MOPS_F6F4")
+        if mops is not None:
+            lines.append("| FP4 MFMA FLOP (MOPS x 512) | %.6g (expected %.6g, ratio %.6f) |" % (
+                mops * 512, fp4_flop, mops * 512 / fp4_flop))
+            busy = m.get("SQ_VALU_MFMA_BUSY_CYCLES")
+            if busy is not None:
+                lines.append("| MFMA busy SIMD-cycles | %.6g (= %.3f x 32 per MFMA) |" % (
+                    busy, busy / (mops / 256.0) / 32.0 if mops else 0.0))
+        for c, label in (("SQ_LDS_BANK_CONFLICT", "LDS bank-conflict cycles"),
+                         ("SQ_LDS_IDX_ACTIVE", "LDS active cycles"),
+                         ("SQ_WAIT_INST_LDS", "wave-cycles waiting on LDS instructions"),
+                         ("SQ_BUSY_CYCLES", "SQ busy cycles"), ("GRBM_GUI_ACTIVE", "GRBM GUI active")):
+            if c in m:
+                lines.append("| %s (%s) | %.6g |" % (label, c, m[c]))
+        if "TCC_HIT" in m and "TCC_MISS" in m:
+            lines.append("| L2 hit rate (TCC_HIT / (HIT + MISS)) | %.3f |" % (
+                m["TCC_HIT"] / max(m["TCC_HIT"] + m["TCC_MISS"], 1.0)))
+        if "TCP_TCC_READ_REQ" in m:
+            lines.append("| L1 -> L2 read requests (x 128 B) | %.4g (%.2f GB) |" % (
+                m["TCP_TCC_READ_REQ"], m["TCP_TCC_READ_REQ"] * 128 / 1e9))
+            if "TCP_TCC_READ_REQ_LATENCY" in m:
+                lines.append("| mean L2 read latency (cycles) | %.0f |" % (
+                    m["TCP_TCC_READ_REQ_LATENCY"] / max(m["TCP_TCC_READ_REQ"], 1.0)))
+        lines.append("")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], sys.argv[4])
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:8])
+    elif sys.argv[1] == "counters":
+        counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:])
     else:
         raise SystemExit(__doc__)

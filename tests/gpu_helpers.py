@@ -2,7 +2,7 @@
 
 The decoder follows the plane layout that include/awe.h documents (1 KiB
 bricks of 32 rows x 64 reduction indices, stored k-step major, K padded to
-256, lane L = 32 h + t owning row t and
+a multiple of awe.K_PAD, lane L = 32 h + t owning row t and
 indices 32 h .. 32 h + 31, two E2M1 codes per byte, low nibble first).
 """
 import numpy as np
@@ -25,7 +25,8 @@ def to_dev(x):
 def decode_planes(buf, nplanes, rows, K):
     """Stored planes (uint8 numpy) -> int64 array [nplanes, rows, K] of doubled values; padding checked."""
     R32 = -(-rows // 32)
-    Kp = -(-K // 256) * 256
+    from paper_2609_24519_amd import awe
+    Kp = -(-K // awe.K_PAD) * awe.K_PAD
     KS = Kp // 64
     stride = R32 * KS * 1024
     # k-step major: brick (rb, ks) at (ks * R32 + rb) * 1024

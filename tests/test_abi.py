@@ -23,6 +23,12 @@ def oracle_mod(m):
     return modm.find_scheme(m)
 
 
+def test_k_pad_matches_header():
+    import re
+    with open(awe.HEADER) as f:
+        assert int(re.search(r"#define AWE_K_PAD (\d+)", f.read()).group(1)) == awe.K_PAD
+
+
 def test_exports_every_declared_symbol():
     L = awe.lib()
     names = awe.header_symbols()
@@ -46,7 +52,7 @@ def test_encoding_info_matches_oracle(name):
     assert (info["c_a"], info["c_b"]) == (c_a, c_b)
     assert info["n_g"] == s.n_g
     assert info["k_star"] == sc.k_star(s.n_g, c_a, c_b)
-    assert info["k_seg"] % 256 == 0 and 0 < info["k_seg"] <= info["k_star"]
+    assert info["k_seg"] % awe.K_PAD == 0 and 0 < info["k_seg"] <= info["k_star"]
     assert info["k_seg"] * s.n_g * c_a * c_b < 2 ** 23
     assert info["range_a"] == s.range_a and info["range_b"] == s.range_b
 
@@ -99,9 +105,9 @@ def test_selected_moduli_have_schemes(paper):
 def test_plane_bytes():
     for enc, npl in ((awe.ENC_AWE6, 6), (awe.ENC_B13, 3), (awe.ENC_AWE4, 4)):
         assert awe.plane_bytes(enc, 0, awe.SIDE_A, 8192, 8192) == npl * 8192 * 8192 // 2
-        # ragged: rows up to a multiple of 32, K up to a multiple of 256
-        assert awe.plane_bytes(enc, 0, awe.SIDE_A, 33, 129) == npl * 64 * 256 // 2
-        assert awe.plane_bytes(enc, 0, awe.SIDE_A, 33, 257) == npl * 64 * 512 // 2
+        # ragged: rows up to a multiple of 32, K up to a multiple of K_PAD
+        assert awe.plane_bytes(enc, 0, awe.SIDE_A, 33, 129) == npl * 64 * awe.K_PAD // 2
+        assert awe.plane_bytes(enc, 0, awe.SIDE_A, 33, awe.K_PAD + 1) == npl * 64 * 2 * awe.K_PAD // 2
         assert awe.plane_bytes(enc, 0, awe.SIDE_A, 0, 100) == 0
     ws = awe.workspace_bytes(awe.ENC_AWE4, 0, 100, 50, 300)
     a = awe.plane_bytes(awe.ENC_AWE4, 0, awe.SIDE_A, 100, 300)
@@ -136,10 +142,12 @@ def test_error_paths_host_only():
                             fake, 1 << 40, None, None) == awe.ERR_INVALID_VALUE
     assert L.awe_gemm_exact(awe.ENC_AWE6, 64, 64, 64, fake, 64, fake, 64, fake, 64, 7,
                             fake, 1 << 40, None, None) == awe.ERR_INVALID_VALUE
-    # fold segment must be a multiple of 256 within the encoding's bound
+    # fold segment must be a multiple of K_PAD within the encoding's bound
     assert L.awe_gemm_planes(awe.ENC_AWE6, 0, 64, 64, 1024, fake, fake, fake, 64, awe.I32, 100,
                              None) == awe.ERR_INVALID_VALUE
-    big = awe.get_encoding_info(awe.ENC_AWE6)["k_seg"] + 256
+    assert L.awe_gemm_planes(awe.ENC_AWE6, 0, 64, 64, 1024, fake, fake, fake, 64, awe.I32,
+                             awe.K_PAD // 2, None) == awe.ERR_INVALID_VALUE
+    big = awe.get_encoding_info(awe.ENC_AWE6)["k_seg"] + awe.K_PAD
     assert L.awe_gemm_planes(awe.ENC_AWE6, 0, 64, 64, 1024, fake, fake, fake, 64, awe.I32, big,
                              None) == awe.ERR_INVALID_VALUE
     # residues are written as int32 only

@@ -87,7 +87,7 @@ def _planes(enc, m, A, B):
 
 
 @pytest.mark.parametrize("enc", EXACT)
-@pytest.mark.parametrize("kseg", [256, 512, 1024])
+@pytest.mark.parametrize("kseg", [awe.K_PAD, 2 * awe.K_PAD, 4 * awe.K_PAD])
 def test_forced_fold_segments(enc, kseg):
     M, N, K = 130, 260, 2000
     A, B = _operands(enc, M, N, K, seed=11)
@@ -120,11 +120,12 @@ def test_multi_launch_reduction():
 
 
 def test_fp32_partial_near_bound():
-    # AWE4: c_A c_B = 24, fold segment 349440 (a multiple of 256), so one FP32 partial reaches
-    # 24 * 349440 = 8386560, just below 2^23; constant operands put every product at its largest
-    # magnitude
+    # AWE4: c_A c_B = 24, default fold segment = the largest multiple of K_PAD not above
+    # (2^23 - 1) / 24 (349440), so one FP32 partial reaches 24 * 349440 = 8386560, just below
+    # 2^23; constant operands put every product at its largest magnitude
     info = awe.get_encoding_info(awe.ENC_AWE4)
     K = info["k_seg"]
+    assert K % awe.K_PAD == 0 and 24 * K < 2 ** 23 <= 24 * (K + awe.K_PAD)
     loa, TA = awe.get_plane_table(awe.ENC_AWE4, 0, awe.SIDE_A)
     lob, TB = awe.get_plane_table(awe.ENC_AWE4, 0, awe.SIDE_B)
     xs = [x for x in range(loa, loa + TA.shape[0]) if np.abs(TA[x - loa]).max() == 3]
@@ -155,7 +156,7 @@ def test_mod_forced_segments():
     A, B = inputs.residue_pair(64, 200, 3000, m)
     pa, pb = _planes(awe.ENC_MOD, m, A, B)
     C = torch.empty((64, 200), dtype=torch.int32, device="cuda")
-    awe.gemm_planes(awe.ENC_MOD, m, 64, 200, 3000, pa, pb, C, 200, awe.I32, 256)
+    awe.gemm_planes(awe.ENC_MOD, m, 64, 200, 3000, pa, pb, C, 200, awe.I32, awe.K_PAD)
     torch.cuda.synchronize()
     assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
 

@@ -99,12 +99,17 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
 // ---------------------------------------------------------------------------
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
-template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_>
+template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
   static constexpr int KST = KST_;        // k-steps (64 reduction indices each) per stage
   static constexpr int KT = 64 * KST;     // reduction indices per stage
   static constexpr int NSTAGE = NSTAGE_;  // LDS ring depth
+  // Fragments are read PD k-steps before their MFMAs, into NSETS register sets
+  // (k-step ks of every stage uses set ks % NSETS, so NSETS divides KST).
+  static constexpr int PD = PD_;
+  static constexpr int NSETS = PD == 1 ? 2 : KST;
+  static_assert(PD >= 1 && PD < NSETS && KST % NSETS == 0, "fragment prefetch distance");
   static constexpr int NW = WM * WN;
   static constexpr int THREADS = 64 * NW;
   static constexpr int BM = WM * BMW * 32, BN = WN * BNW * 32;
@@ -267,6 +272,30 @@ __device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& t
   tn = in / gm;
 }
 
+// One output of the epilogue: the int32 accumulator holds D*C (exact schemes,
+// modulo 2^32, the true value fits) or sum lambda_k P_k (residues).
+__device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col, int32_t val) {
+  if (row >= g.M || col >= g.N) return;
+  const int64_t off = (int64_t)row * g.ldc + col;
+  if (g.modulus) {
+    const int32_t m = g.modulus;
+    int32_t rr = val % m;
+    if (rr < 0) rr += m;
+    int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
+    if (g.accumulate) rr = (Cp[off] + rr) % m;
+    Cp[off] = rr;
+  } else {
+    val >>= g.log2D;
+    if (g.c64) {
+      int64_t* Cp = reinterpret_cast<int64_t*>(g.C);
+      Cp[off] = g.accumulate ? Cp[off] + (int64_t)val : (int64_t)val;
+    } else {
+      int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
+      Cp[off] = g.accumulate ? (int32_t)((uint32_t)Cp[off] + (uint32_t)val) : val;
+    }
+  }
+}
+
 template <class C>
 __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
@@ -299,43 +328,47 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
   }
   wait_stages<C, NSTAGE - 1>(wave);
   block_barrier();
-  Frags<C> f[2];
-  read_frags<C>(f[0], smem, 0, wm, wn, lane);
+  constexpr int PD = C::PD, NSETS = C::NSETS;
+  Frags<C> f[NSETS];
+#pragma unroll
+  for (int ks = 0; ks < PD; ++ks) read_frags<C>(f[ks], smem, ks, wm, wn, lane);
 
-  // Stage s, k-steps 0 .. KST-1: while the MFMAs of k-step ks run on one
-  // fragment set, the next k-step's fragments are read into the other.  Before
-  // the last k-step: wait until stage s+1 has landed and this wave's reads of
-  // stage s are done, barrier, refill stage s's buffer with stage s+NSTAGE and
-  // read the first fragments of stage s+1.  The barrier sits between two groups
-  // of MFMAs.
+  // Stage s, k-steps 0 .. KST-1: the MFMAs of k-step ks run on fragment set
+  // ks % NSETS while the reads of k-step ks + PD go into another set.  At k-step
+  // KST - PD, before the first read that crosses into stage s+1: wait until
+  // stage s+1 has landed and this wave's reads of stage s are done (all of them
+  // were issued by then), barrier, refill stage s's buffer with stage s+NSTAGE.
+  // The barrier sits between two groups of MFMAs.
   int buf = 0;
   for (int cs = g.t_begin; cs < g.t_end; cs += g.ts) {
     const int ce = min(cs + g.ts, g.t_end);
     for (int p = 0; p < g.r; ++p) {
       for (int t = cs; t < ce; ++t) {
         const uint32_t cur_off = buf * C::STAGE_BYTES;
-        buf = buf + 1 == NSTAGE ? 0 : buf + 1;
+        const int nbuf = buf + 1 == NSTAGE ? 0 : buf + 1;
 #pragma unroll
         for (int ks = 0; ks < C::KST; ++ks) {
-          Frags<C>& cur = f[ks & 1];
-          Frags<C>& nx = f[(ks + 1) & 1];
-          if (ks + 1 < C::KST) {
-            read_frags<C>(nx, smem + cur_off, ks + 1, wm, wn, lane);
-          } else {
+          if (ks == C::KST - PD) {
             wait_stages<C, NSTAGE - 2>(wave);
             wait_lgkm0();
             block_barrier();
             load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
             cursor_next(nxt, g);
-            read_frags<C>(nx, smem + buf * C::STAGE_BYTES, 0, wm, wn, lane);
           }
+          const int kr = ks + PD;  // k-step whose fragments are read now
+          if (kr < C::KST)
+            read_frags<C>(f[kr % NSETS], smem + cur_off, kr, wm, wn, lane);
+          else
+            read_frags<C>(f[kr % NSETS], smem + nbuf * C::STAGE_BYTES, kr - C::KST, wm, wn, lane);
           __builtin_amdgcn_sched_barrier(0);
+          const Frags<C>& cur = f[ks % NSETS];
 #pragma unroll
           for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
             for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], cur.a[i], cur.b[j]);
           __builtin_amdgcn_sched_barrier(0);
         }
+        buf = nbuf;
       }
       if ((g.fold_mask >> p) & 1u) {
         const int32_t l = g.fold_ell[p];
@@ -364,30 +397,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < C::BNW; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
-        const int col = col0 + j * 32;
-        if (row >= g.M || col >= g.N) continue;
-        const int64_t off = (int64_t)row * g.ldc + col;
-        int32_t val = iacc[i][j][v];
-        if (g.modulus) {
-          const int32_t m = g.modulus;
-          int32_t rr = val % m;
-          if (rr < 0) rr += m;
-          int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
-          if (g.accumulate) rr = (Cp[off] + rr) % m;
-          Cp[off] = rr;
-        } else {
-          val >>= g.log2D;
-          if (g.c64) {
-            int64_t* Cp = reinterpret_cast<int64_t*>(g.C);
-            Cp[off] = g.accumulate ? Cp[off] + (int64_t)val : (int64_t)val;
-          } else {
-            int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
-            Cp[off] = g.accumulate ? (int32_t)((uint32_t)Cp[off] + (uint32_t)val) : val;
-          }
-        }
-      }
+      for (int v = 0; v < 16; ++v)
+        store_output(g, row0 + i * 32 + 8 * (v >> 2) + (v & 3), col0 + j * 32, iacc[i][j][v]);
 }
 
 // The tile configurations the launcher chooses from: waves (M x N), 32x32
@@ -397,6 +408,7 @@ using Cfg8w64x64 = Cfg<4, 2, 2, 2, 2, 4>;    // 256 x 128, 8 waves (2 per SIMD)
 using Cfg8w64x96 = Cfg<4, 2, 2, 3, 2, 4>;    // 256 x 192, 8 waves (2 per SIMD)
 using Cfg4w128x64k4 = Cfg<2, 2, 4, 2, 4, 3>; // 256 x 128, 4 waves, 4 k-steps per stage
 using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps per stage
+using Cfg8w64x64k4p2 = Cfg<4, 2, 2, 2, 4, 3, 2>;  // as above, fragments read 2 k-steps ahead
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;
@@ -409,14 +421,16 @@ __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, in
 
 // Tile configuration for a problem.  AWE_GEMM_CFG (0: 256x128 with 4 waves,
 // 1: 256x128 with 8 waves, 2: 256x192 with 8 waves, 3 and 4: as 0 and 1 with
-// 4 k-steps per stage) overrides the choice.  Otherwise: 256x128 on 8 waves
-// with 4 k-steps per stage, or 256x192 when its rounds of workgroups (each
-// about 1.37 times as long as a 256x128 round, measured at 8192^3) finish
-// sooner, which happens when the 128-wide tiling leaves a ragged last round.
+// 4 k-steps per stage, 5: as 4 with fragments read two k-steps ahead)
+// overrides the choice.  Otherwise: 256x128 on 8 waves with 4 k-steps per
+// stage and fragments read two k-steps ahead, or 256x192 when its rounds of
+// workgroups (each about 1.37 times as long as a 256x128 round, measured at
+// 8192^3) finish sooner, which happens when the 128-wide tiling leaves a
+// ragged last round.
 int choose_cfg(int64_t M, int64_t N) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
-  if (forced >= 0 && forced <= 4) return forced;
+  if (forced >= 0 && forced <= 5) return forced;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) {
     int v = 0;
@@ -426,7 +440,7 @@ int choose_cfg(int64_t M, int64_t N) {
   const int64_t tm = (M + 255) / 256;
   const double t128 = (double)((tm * ((N + 127) / 128) + cus - 1) / cus);
   const double t192 = (double)((tm * ((N + 191) / 192) + cus - 1) / cus) * 1.37;
-  return t192 < t128 ? 2 : 4;
+  return t192 < t128 ? 2 : 5;
 }
 
 template <class C>
@@ -530,6 +544,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 2: return launch_tile<Cfg8w64x96>(g, L, stream);
     case 3: return launch_tile<Cfg4w128x64k4>(g, L, stream);
     case 4: return launch_tile<Cfg8w64x64k4>(g, L, stream);
+    case 5: return launch_tile<Cfg8w64x64k4p2>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }

@@ -7,9 +7,12 @@ and neither imports the other.  Only ``tests/``, ``__graft_entry__.smoke()``
 and the CPU-baseline leg of ``bench.py`` may import or execute it.
 
 * ``gemm``    -- the plain definition C = A B (and C mod m), a C triple loop
-                 with a 64-bit accumulator, loaded through ctypes.
+                 with a 64-bit accumulator (128-bit for int64 operands),
+                 loaded through ctypes.
 * ``schemes`` -- the paper's encodings (storable set, limb tables, planes,
                  reconstruction coefficients, coverage, K*), the scheme
                  identity and the run-time procedure in plain numpy int64.
 * ``modm``    -- the congruence (mod m) schemes and their tables.
+* ``crt``     -- residues and the Chinese-remainder reconstruction of a
+                 residue number system, in Python integers.
 """

@@ -89,6 +89,46 @@ void oracle_gemm_u8_mod_sampled(int64_t m, int64_t nr, const int64_t* rows,
     }
 }
 
+/* C = A B exactly for int64 entries, accumulated in 128 bits: the integer
+   product a residue number system reconstructs (Sec. 5.3, with B the input
+   bound, |C| <= K B_A B_B).  The caller keeps sum_k |A[i,k] B[k,j]| below
+   2^127 (e.g. |entries| <= 2^53 - 1 with K <= 2^20).  Each entry of C is
+   returned as two words, C = hi * 2^64 + lo with lo unsigned. */
+void oracle_gemm_i64_i128(int64_t M, int64_t N, int64_t K,
+                          const int64_t* A, int64_t lda,
+                          const int64_t* B, int64_t ldb,
+                          uint64_t* lo, int64_t* hi, int64_t ldc)
+{
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < M; ++i) {
+        for (int64_t j = 0; j < N; ++j) {
+            __int128 acc = 0;
+            for (int64_t k = 0; k < K; ++k) acc += (__int128)A[i * lda + k] * (__int128)B[k * ldb + j];
+            lo[i * ldc + j] = (uint64_t)acc;
+            hi[i * ldc + j] = (int64_t)(acc >> 64);
+        }
+    }
+}
+
+/* Sampled variant of the 128-bit product: rows x cols of C, row-major nr x nc. */
+void oracle_gemm_i64_i128_sampled(int64_t nr, const int64_t* rows,
+                                  int64_t nc, const int64_t* cols, int64_t K,
+                                  const int64_t* A, int64_t lda,
+                                  const int64_t* B, int64_t ldb,
+                                  uint64_t* lo, int64_t* hi)
+{
+    #pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < nr; ++r) {
+        const int64_t* a = A + rows[r] * lda;
+        for (int64_t c = 0; c < nc; ++c) {
+            __int128 acc = 0;
+            for (int64_t k = 0; k < K; ++k) acc += (__int128)a[k] * (__int128)B[k * ldb + cols[c]];
+            lo[r * nc + c] = (uint64_t)acc;
+            hi[r * nc + c] = (int64_t)(acc >> 64);
+        }
+    }
+}
+
 /* Number of OpenMP threads the loops above will use (reported with timings). */
 int oracle_num_threads(void)
 {

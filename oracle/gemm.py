@@ -1,8 +1,9 @@
 """Oracle (test infrastructure only): ctypes wrapper of ``gemm.c``.
 
 ``gemm.c`` is the plain definition of the exact integer product C = A B
-(Sec. 1 and the postcondition of Alg. 1) and of its residue C mod m
-(Sec. 5.3).  ``build()`` compiles it with gcc; nothing here touches a GPU.
+(Sec. 1 and the postcondition of Alg. 1), of its residue C mod m (Sec. 5.3),
+and of the wide product of int64 matrices a residue number system
+reconstructs (Sec. 5.3), accumulated in 128 bits.  ``build()`` compiles it with gcc; nothing here touches a GPU.
 """
 import ctypes
 import os
@@ -39,6 +40,9 @@ def _load():
         lib.oracle_gemm_i8_i64_sampled.argtypes = [_I64, _P, _I64, _P, _I64, _P, _I64, _P, _I64, _P]
         lib.oracle_gemm_u8_mod.argtypes = [_I64, _I64, _I64, _I64, _P, _I64, _P, _I64, _P, _I64]
         lib.oracle_gemm_u8_mod_sampled.argtypes = [_I64, _I64, _P, _I64, _P, _I64, _P, _I64, _P, _I64, _P]
+        lib.oracle_gemm_i64_i128.argtypes = [_I64, _I64, _I64, _P, _I64, _P, _I64, _P, _P, _I64]
+        lib.oracle_gemm_i64_i128_sampled.argtypes = [_I64, _P, _I64, _P, _I64, _P, _I64, _P, _I64,
+                                                     _P, _P]
         lib.oracle_num_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -113,3 +117,48 @@ def gemm_mod_sampled(m, A, B, rows, cols):
         _load().oracle_gemm_u8_mod_sampled(m, rows.size, _ptr(rows), cols.size, _ptr(cols), K,
                                            _ptr(A), K, _ptr(B), N, _ptr(C))
     return C
+
+
+def _join128(lo, hi):
+    """Two int64 words per entry -> numpy object array of Python ints hi * 2^64 + lo."""
+    out = np.empty(lo.shape, dtype=object)
+    flat_lo, flat_hi, flat = lo.ravel(), hi.ravel(), out.ravel()
+    for i in range(flat.size):
+        flat[i] = (int(flat_hi[i]) << 64) + int(flat_lo[i])
+    return out
+
+
+def gemm_i128(A, B, words=False):
+    """Exact C = A B for int64 A (M x K) and B (K x N), with sum_k |a b| < 2^127.
+
+    Returns a numpy object array of Python ints, or with ``words=True`` the pair
+    (lo uint64, hi int64) with C = hi * 2^64 + lo."""
+    A = np.ascontiguousarray(A, dtype=np.int64)
+    B = np.ascontiguousarray(B, dtype=np.int64)
+    M, K = A.shape
+    K2, N = B.shape
+    assert K == K2
+    lo = np.zeros((M, N), dtype=np.uint64)
+    hi = np.zeros((M, N), dtype=np.int64)
+    if M and N:
+        _load().oracle_gemm_i64_i128(M, N, K, _ptr(A), K, _ptr(B), N, _ptr(lo), _ptr(hi), N)
+    return (lo, hi) if words else _join128(lo, hi)
+
+
+def gemm_i128_sampled(A, B, rows, cols, words=False):
+    """Exact (A B)[rows][:, cols] for int64 operands without forming the full product."""
+    A = np.ascontiguousarray(A, dtype=np.int64)
+    B = np.ascontiguousarray(B, dtype=np.int64)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    M, K = A.shape
+    K2, N = B.shape
+    assert K == K2
+    assert rows.size == 0 or (rows.min() >= 0 and rows.max() < M)
+    assert cols.size == 0 or (cols.min() >= 0 and cols.max() < N)
+    lo = np.zeros((rows.size, cols.size), dtype=np.uint64)
+    hi = np.zeros((rows.size, cols.size), dtype=np.int64)
+    if rows.size and cols.size:
+        _load().oracle_gemm_i64_i128_sampled(rows.size, _ptr(rows), cols.size, _ptr(cols), K,
+                                             _ptr(A), K, _ptr(B), N, _ptr(lo), _ptr(hi))
+    return (lo, hi) if words else _join128(lo, hi)

@@ -9,8 +9,9 @@ The workload is M = N = K = 8192 with int8 entries uniform in [-128, 127]
 (seed 0) and int32 C.  Printed: one JSON line with the end-to-end exact TOPS
 as ``value``, the roofline of the dominant kernel (the GEMM) from HIP events
 on its stream, the 9-product base-13 baseline, the native INT8 MFMA GEMM
-(hipBLASLt through torch._int_mm) and the sustained rate of the FP4 MFMA alone
-timed in the same run as context, and the oracle timed on the host's cores on
+(hipBLASLt through torch._int_mm), the residue-number-system route for 53-bit
+integers (the integer layer of Ozaki scheme II) and the sustained rate of the
+FP4 MFMA alone timed in the same run as context, and the oracle timed on the host's cores on
 a bounded sample.
 """
 import argparse
@@ -149,6 +150,7 @@ def main():
         except Exception as ex:  # noqa: BLE001 - context only
             line["int8_mfma_context"] = {"error": str(ex)[:200]}
     if not args.no_context:
+        line["ozaki2_int53"] = ozaki2_context(dev)
         probe = mfma_sustained()
         if probe:
             probe["gemm_frac_of_8_wave_rate"] = round(gemm_tflops / probe["8_waves_per_cu_TFLOPs"], 4)
@@ -163,6 +165,52 @@ def main():
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(A_h, B_h)
     print(json.dumps(line), flush=True)
+
+
+def ozaki2_context(dev, M=4096, N=4096, K=16384):
+    """The residue route of Sec. 5.3 as the integer layer of Ozaki scheme II: exact product of
+    53-bit integer matrices through the 23-modulus FP64-significand set (60 FP4 products),
+    awe_gemm_crt end to end (residues, mod-m GEMMs, reconstruction to 128-bit words and the
+    nearest double).  Timed with HIP events on the current stream."""
+    import torch
+
+    from paper_2609_24519_amd import awe
+
+    with open(os.path.join(ROOT, "tests", "golden", "moduli_fp64_k16384.txt")) as f:
+        rows = [l for l in f if l.strip() and not l.startswith("#")]
+    moduli = [int(x) for x in rows[0].split()]
+    b53 = (1 << 53) - 1
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    A = torch.randint(-b53, b53, (M, K), dtype=torch.int64, device=dev, generator=g)
+    B = torch.randint(-b53, b53, (K, N), dtype=torch.int64, device=dev, generator=g)
+    c128 = torch.empty((M, N, 2), dtype=torch.int64, device=dev)
+    c64 = torch.empty((M, N), dtype=torch.float64, device=dev)
+    wsn = awe.crt_workspace_bytes(moduli, M, N, K)
+    ws = torch.empty(wsn, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def run():
+        awe.gemm_crt(M, N, K, A, K, B, N, b53, b53, moduli, c128, c64, N, ws, wsn, None, stream)
+
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 3
+    e0.record(stream)
+    for _ in range(reps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    products = sum(awe.get_encoding_info(awe.ENC_MOD, m)["r"] for m in moduli)
+    out = {"workload": "M=N=%d, K=%d, int64 entries uniform in [-(2^53-1), 2^53-1], %d moduli, "
+                       "%d FP4 products" % (M, K, len(moduli), products),
+           "ms": round(ms, 3), "fp64_equiv_TFLOPs": round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 1),
+           "fp4_products_TFLOPs": round(products * 2.0 * M * N * K / (ms * 1e-3) / 1e12, 1)}
+    del A, B, c128, c64, ws
+    torch.cuda.empty_cache()
+    return out
 
 
 def mfma_sustained(iters=20000):

@@ -164,6 +164,51 @@ awe_status awe_gemm_mod(int32_t m, int64_t M, int64_t N, int64_t K,
                         void* workspace, size_t ws_bytes, int32_t* d_range_flag,
                         hipStream_t stream);
 
+/* ---- Residue number system (Sec. 5.3) ---------------------------------------------------
+   A residue number system computes an integer product as its residues modulo pairwise
+   coprime moduli m_1..m_n, one mod-m product per modulus, and recovers it by the Chinese
+   remainder theorem; the result is unique when M = m_1 ... m_n > 2 K B_A B_B, B the bound
+   on the entries (Sec. 5.3).  With 53-bit entries this is the integer layer of Ozaki
+   scheme II (Sec. 2) for the FP64 significand.  Moduli lie in [2, 256] and n <= AWE_MAX_MODULI. */
+#define AWE_MAX_MODULI 32
+
+/* Device.  Residues of int64 entries: out + j*out_stride receives x mod moduli[j] in [0, m)
+   as uint8, rows x cols row-major and dense (leading dimension cols); x is rows x cols
+   row-major with leading dimension ld >= cols.  moduli is a host array.  Entries with
+   |x| > bound set *d_range_flag (device, nullable) to a nonzero value; their residues are
+   still exact.  The moduli need not be coprime here.  AWE_ERR_INVALID_VALUE for a modulus
+   outside [2, 256], a bad n or size. */
+awe_status awe_residues(const int64_t* x, int64_t rows, int64_t cols, int64_t ld, int64_t bound,
+                        const int32_t* moduli, int32_t n, uint8_t* out, int64_t out_stride,
+                        int32_t* d_range_flag, hipStream_t stream);
+
+/* Device.  Chinese-remainder reconstruction.  residues + j*res_stride holds a rows x cols
+   int32 matrix (leading dimension ld_res) of residues in [0, moduli[j]), as awe_gemm_mod
+   writes them.  Writes the unique X in (-M/2, M/2] with X = residue (mod m_j) for all j:
+   into c128 (nullable) as two int64 words per entry, c128[2*(i*ldc+j)] = low 64 bits
+   (two's complement) and c128[2*(i*ldc+j)+1] = high 64 bits, so X = hi 2^64 + (unsigned) lo;
+   and into c64 (nullable) rounded to the nearest double (ties to even).  The moduli must be
+   pairwise coprime with M < 2^127 (AWE_ERR_INVALID_VALUE otherwise); residues outside
+   [0, m_j) give an unspecified X. */
+awe_status awe_crt(const int32_t* residues, int64_t res_stride, int64_t rows, int64_t cols,
+                   int64_t ld_res, const int32_t* moduli, int32_t n,
+                   int64_t* c128, double* c64, int64_t ldc, hipStream_t stream);
+
+/* Host.  Workspace bytes awe_gemm_crt needs for these moduli and sizes. */
+awe_status awe_crt_workspace_bytes(const int32_t* moduli, int32_t n, int64_t M, int64_t N,
+                                   int64_t K, size_t* bytes);
+
+/* Exact C = A B for int64 A (M x K, lda) and B (K x N, ldb) with |entries| <= bound_a and
+   bound_b, through residues: awe_residues on both operands, awe_gemm_mod for every modulus,
+   awe_crt into c128 and/or c64 (as for awe_crt, leading dimension ldc).  Requires
+   M_prod > 2 K bound_a bound_b (AWE_ERR_OVERFLOW otherwise) and every modulus to have a
+   scheme (AWE_ERR_UNSUPPORTED).  Entries beyond their bound set *d_range_flag. */
+awe_status awe_gemm_crt(int64_t M, int64_t N, int64_t K, const int64_t* A, int64_t lda,
+                        const int64_t* B, int64_t ldb, int64_t bound_a, int64_t bound_b,
+                        const int32_t* moduli, int32_t n, int64_t* c128, double* c64, int64_t ldc,
+                        void* workspace, size_t ws_bytes, int32_t* d_range_flag,
+                        hipStream_t stream);
+
 /* Host.  Static description of a status code. */
 const char* awe_status_string(awe_status s);
 

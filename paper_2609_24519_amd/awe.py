@@ -79,12 +79,18 @@ def lib():
                                      _P, _SZ, _P, _P]
         L.awe_gemm_mod.argtypes = [_I32, _I64, _I64, _I64, _P, _I64, _P, _I64, _P, _I64,
                                    _P, _SZ, _P, _P]
+        L.awe_residues.argtypes = [_P, _I64, _I64, _I64, _I64, _P, _I32, _P, _I64, _P, _P]
+        L.awe_crt.argtypes = [_P, _I64, _I64, _I64, _I64, _P, _I32, _P, _P, _I64, _P]
+        L.awe_crt_workspace_bytes.argtypes = [_P, _I32, _I64, _I64, _I64, ctypes.POINTER(_SZ)]
+        L.awe_gemm_crt.argtypes = [_I64, _I64, _I64, _P, _I64, _P, _I64, _I64, _I64, _P, _I32,
+                                   _P, _P, _I64, _P, _SZ, _P, _P]
         L.awe_status_string.argtypes = [_I32]
         L.awe_status_string.restype = ctypes.c_char_p
         L.awe_last_error.argtypes = []
         L.awe_last_error.restype = ctypes.c_char_p
         for name in ("awe_get_encoding_info", "awe_get_plane_table", "awe_plane_bytes", "awe_encode",
-                     "awe_gemm_planes", "awe_workspace_bytes", "awe_gemm_exact", "awe_gemm_mod"):
+                     "awe_gemm_planes", "awe_workspace_bytes", "awe_gemm_exact", "awe_gemm_mod",
+                     "awe_residues", "awe_crt", "awe_crt_workspace_bytes", "awe_gemm_crt"):
             getattr(L, name).restype = _I32
         _lib = L
     return _lib
@@ -192,6 +198,39 @@ def gemm_mod(m, M, N, K, A, lda, B, ldb, C, ldc, workspace, ws_bytes, d_range_fl
                               ws_bytes, _ptr(d_range_flag), _stream(stream)), "awe_gemm_mod")
 
 
+# ---- residue number system (moduli: a sequence of ints, passed as a host int32 array) ----
+def _moduli(moduli):
+    arr = (ctypes.c_int32 * len(moduli))(*[int(m) for m in moduli])
+    return arr, len(moduli)
+
+
+def residues(x, rows, cols, ld, bound, moduli, out, out_stride, d_range_flag=None, stream=None):
+    arr, n = _moduli(moduli)
+    _check(lib().awe_residues(_ptr(x), rows, cols, ld, bound, arr, n, _ptr(out), out_stride,
+                              _ptr(d_range_flag), _stream(stream)), "awe_residues")
+
+
+def crt(res, res_stride, rows, cols, ld_res, moduli, c128=None, c64=None, ldc=None, stream=None):
+    arr, n = _moduli(moduli)
+    _check(lib().awe_crt(_ptr(res), res_stride, rows, cols, ld_res, arr, n, _ptr(c128), _ptr(c64),
+                         cols if ldc is None else ldc, _stream(stream)), "awe_crt")
+
+
+def crt_workspace_bytes(moduli, M, N, K):
+    arr, n = _moduli(moduli)
+    out = _SZ(0)
+    _check(lib().awe_crt_workspace_bytes(arr, n, M, N, K, ctypes.byref(out)), "awe_crt_workspace_bytes")
+    return out.value
+
+
+def gemm_crt(M, N, K, A, lda, B, ldb, bound_a, bound_b, moduli, c128, c64, ldc, workspace, ws_bytes,
+             d_range_flag=None, stream=None):
+    arr, n = _moduli(moduli)
+    _check(lib().awe_gemm_crt(M, N, K, _ptr(A), lda, _ptr(B), ldb, bound_a, bound_b, arr, n,
+                              _ptr(c128), _ptr(c64), ldc, _ptr(workspace), ws_bytes,
+                              _ptr(d_range_flag), _stream(stream)), "awe_gemm_crt")
+
+
 # ---- torch conveniences (allocation with torch, then the calls above) -------------
 def matmul_exact(A, B, enc=ENC_AWE6, out_dtype=None, d_range_flag=None):
     """C = A B exactly for int8 CUDA tensors A (M x K) and B (K x N)."""
@@ -220,3 +259,18 @@ def matmul_mod(m, A, B, d_range_flag=None):
     ws = torch.empty(max(ws_n, 1), dtype=torch.uint8, device=A.device)
     gemm_mod(m, M, N, K, A, A.stride(0), B, B.stride(0), C, C.stride(0), ws, ws_n, d_range_flag)
     return C
+
+
+def matmul_crt(A, B, moduli, bound_a, bound_b, d_range_flag=None):
+    """Exact A B for int64 CUDA tensors through residues; returns (c128, c64): the integer as
+    an int64 tensor of shape (M, N, 2) holding (low, high) words, and its nearest double."""
+    import torch
+    M, K = A.shape
+    _, N = B.shape
+    c128 = torch.empty((M, N, 2), dtype=torch.int64, device=A.device)
+    c64 = torch.empty((M, N), dtype=torch.float64, device=A.device)
+    ws_n = crt_workspace_bytes(moduli, M, N, K)
+    ws = torch.empty(max(ws_n, 1), dtype=torch.uint8, device=A.device)
+    gemm_crt(M, N, K, A, A.stride(0), B, B.stride(0), bound_a, bound_b, moduli, c128, c64, N, ws, ws_n,
+             d_range_flag)
+    return c128, c64

@@ -19,7 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libawe.so")
-SOURCES = ["awe_kernels.hip", "awe_tables.cpp", "awe_api.cpp"]
+SOURCES = ["awe_kernels.hip", "awe_rns.hip", "awe_tables.cpp", "awe_api.cpp"]
 PROBE_LIB = os.path.join(HERE, "libawe_probe.so")
 PROBE_SOURCES = ["mfma_peak.hip"]
 ARCH = "gfx950"
@@ -68,7 +68,7 @@ def resources(out_md):
     import yaml
 
     rows = []
-    for src in ["awe_kernels.hip"]:
+    for src in ["awe_kernels.hip", "awe_rns.hip"]:
         with tempfile.TemporaryDirectory() as td:
             asm = os.path.join(td, "k.s")
             cmd = [hipcc(), "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",

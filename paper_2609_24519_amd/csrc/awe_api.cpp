@@ -166,6 +166,97 @@ awe_status exact_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, const vo
   return gemm_planes_impl(s, M, N, K, pa, pb, C, ldc, c_type, 0, stream);
 }
 
+// ---- residue number system ----
+
+uint32_t inverse_mod(uint32_t a, uint32_t m) {  // a^-1 mod m by the extended Euclidean algorithm
+  int64_t t = 0, nt = 1, r = m, nr = a % m;
+  while (nr != 0) {
+    const int64_t q = r / nr;
+    std::swap(t, nt);
+    nt -= q * t;
+    std::swap(r, nr);
+    nr -= q * r;
+  }
+  return r == 1 ? (uint32_t)((t % m + m) % m) : 0;
+}
+
+// Checks a moduli set (1..AWE_MAX_MODULI moduli in 2..256; for a
+// reconstruction also pairwise coprime with product below 2^127) and derives
+// the constants of the residue and reconstruction kernels.
+awe_status rns_setup(const int32_t* moduli, int32_t n, ResidueParams* rp, CrtParams* cp,
+                     unsigned __int128* prod, bool reconstruct = true) {
+  if (moduli == nullptr || n < 1 || n > kMaxModuli)
+    return fail(AWE_ERR_INVALID_VALUE, "need 1 to " + std::to_string(kMaxModuli) + " moduli");
+  const unsigned __int128 limit = ((unsigned __int128)1 << 127) - 1;
+  unsigned __int128 M = 1;
+  for (int j = 0; j < n; ++j) {
+    const int32_t m = moduli[j];
+    if (m < 2 || m > 256) return fail(AWE_ERR_INVALID_VALUE, "moduli must lie in [2, 256]");
+    if (!reconstruct) continue;
+    for (int i = 0; i < j; ++i)
+      if (std::__gcd(moduli[i], m) != 1) return fail(AWE_ERR_INVALID_VALUE, "moduli are not pairwise coprime");
+    if (M > limit / (unsigned)m) return fail(AWE_ERR_INVALID_VALUE, "product of the moduli must stay below 2^127");
+    M *= (unsigned)m;
+  }
+  if (rp) {
+    std::memset(rp, 0, sizeof(*rp));
+    rp->n = n;
+    for (int j = 0; j < n; ++j) {
+      const uint32_t m = (uint32_t)moduli[j];
+      rp->m[j] = m;
+      rp->minv[j] = 0xffffffffu / m;
+      rp->p32[j] = (uint32_t)((uint64_t(1) << 32) % m);
+      rp->p64[j] = (uint32_t)(((unsigned __int128)1 << 64) % m);
+    }
+  }
+  if (cp) {
+    std::memset(cp, 0, sizeof(*cp));
+    cp->n = n;
+    for (int j = 0; j < n; ++j) {
+      const uint32_t m = (uint32_t)moduli[j];
+      cp->m[j] = m;
+      cp->minv[j] = 0xffffffffu / m;
+      uint64_t pj = 1;  // m_0 ... m_{j-1} mod m
+      for (int i = 0; i < j; ++i) {
+        cp->c[i][j] = (uint8_t)pj;
+        pj = pj * (uint32_t)moduli[i] % m;
+      }
+      cp->d[j] = inverse_mod((uint32_t)pj, m);
+      const uint32_t most = (uint32_t)(kMaxModuli - 1) * 255u * 255u;  // largest subtracted sum
+      cp->off[j] = (most / m + 1) * m;
+    }
+    cp->M_lo = (uint64_t)M;
+    cp->M_hi = (uint64_t)(M >> 64);
+    const unsigned __int128 h = M / 2;
+    cp->half_lo = (uint64_t)h;
+    cp->half_hi = (uint64_t)(h >> 64);
+  }
+  if (prod) *prod = M;
+  return AWE_OK;
+}
+
+struct CrtLayout {  // workspace of awe_gemm_crt
+  size_t res_a, res_b, res_c, planes, total;
+};
+
+CrtLayout crt_layout(const int32_t* moduli, int32_t n, int64_t M, int64_t N, int64_t K, awe_status* st) {
+  CrtLayout L{};
+  *st = AWE_OK;
+  L.res_a = (size_t)round_up((int64_t)n * M * K, 256);
+  L.res_b = (size_t)round_up((int64_t)n * K * N, 256);
+  L.res_c = (size_t)round_up((int64_t)n * M * N * 4, 256);
+  size_t planes = 0;
+  for (int j = 0; j < n; ++j) {
+    const Scheme* s = scheme_or_fail(AWE_ENC_MOD, moduli[j], st);
+    if (!s) return L;
+    planes = std::max(planes, (size_t)round_up((int64_t)side_bytes(*s, true, M, K), 256) +
+                                  side_bytes(*s, false, N, K));
+  }
+  L.planes = planes;
+  L.total = L.res_a + L.res_b + L.res_c + L.planes;
+  return L;
+}
+
 }  // namespace
 
 void set_error(const std::string& msg) { g_last_error = msg; }
@@ -299,6 +390,97 @@ awe_status awe_gemm_mod(int32_t m, int64_t M, int64_t N, int64_t K, const uint8_
   if (!s) return st;
   return exact_impl(*s, M, N, K, A, lda, B, ldb, C, ldc, AWE_I32, workspace, ws_bytes, d_range_flag,
                     stream);
+}
+
+awe_status awe_residues(const int64_t* x, int64_t rows, int64_t cols, int64_t ld, int64_t bound,
+                        const int32_t* moduli, int32_t n, uint8_t* out, int64_t out_stride,
+                        int32_t* d_range_flag, hipStream_t stream) {
+  ResidueParams P;
+  awe_status st = rns_setup(moduli, n, &P, nullptr, nullptr, false);
+  if (st != AWE_OK) return st;
+  if (rows < 0 || cols < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  if (rows == 0 || cols == 0) return AWE_OK;
+  if (x == nullptr || out == nullptr) return fail(AWE_ERR_INVALID_VALUE, "NULL pointer");
+  if (ld < cols) return fail(AWE_ERR_INVALID_VALUE, "leading dimension too small");
+  if (n > 1 && out_stride < rows * cols) return fail(AWE_ERR_INVALID_VALUE, "out_stride too small");
+  if (bound < 0) return fail(AWE_ERR_INVALID_VALUE, "negative bound");
+  return launch_residues(x, rows, cols, ld, bound, P, out, out_stride, d_range_flag, stream);
+}
+
+awe_status awe_crt(const int32_t* residues, int64_t res_stride, int64_t rows, int64_t cols,
+                   int64_t ld_res, const int32_t* moduli, int32_t n, int64_t* c128, double* c64,
+                   int64_t ldc, hipStream_t stream) {
+  CrtParams P;
+  awe_status st = rns_setup(moduli, n, nullptr, &P, nullptr);
+  if (st != AWE_OK) return st;
+  if (rows < 0 || cols < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  if (rows == 0 || cols == 0) return AWE_OK;
+  if (residues == nullptr) return fail(AWE_ERR_INVALID_VALUE, "residues are NULL");
+  if (ld_res < cols || ldc < cols) return fail(AWE_ERR_INVALID_VALUE, "leading dimension too small");
+  if (n > 1 && res_stride < (rows - 1) * ld_res + cols)
+    return fail(AWE_ERR_INVALID_VALUE, "res_stride too small");
+  if (c128 == nullptr && c64 == nullptr) return AWE_OK;
+  return launch_crt(residues, res_stride, rows, cols, ld_res, P, c128, c64, ldc, stream);
+}
+
+awe_status awe_crt_workspace_bytes(const int32_t* moduli, int32_t n, int64_t M, int64_t N, int64_t K,
+                                   size_t* bytes) {
+  if (bytes == nullptr) return fail(AWE_ERR_INVALID_VALUE, "bytes is NULL");
+  if (M < 0 || N < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  awe_status st = rns_setup(moduli, n, nullptr, nullptr, nullptr);
+  if (st != AWE_OK) return st;
+  const CrtLayout L = crt_layout(moduli, n, M, N, K, &st);
+  if (st != AWE_OK) return st;
+  *bytes = L.total;
+  return AWE_OK;
+}
+
+awe_status awe_gemm_crt(int64_t M, int64_t N, int64_t K, const int64_t* A, int64_t lda,
+                        const int64_t* B, int64_t ldb, int64_t bound_a, int64_t bound_b,
+                        const int32_t* moduli, int32_t n, int64_t* c128, double* c64, int64_t ldc,
+                        void* workspace, size_t ws_bytes, int32_t* d_range_flag,
+                        hipStream_t stream) {
+  ResidueParams rp;
+  CrtParams cp;
+  unsigned __int128 Mprod;
+  awe_status st = rns_setup(moduli, n, &rp, &cp, &Mprod);
+  if (st != AWE_OK) return st;
+  if (M < 0 || N < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  if (bound_a < 0 || bound_b < 0) return fail(AWE_ERR_INVALID_VALUE, "negative bound");
+  if (M == 0 || N == 0) return AWE_OK;
+  if (K > 0 && (A == nullptr || B == nullptr)) return fail(AWE_ERR_INVALID_VALUE, "A or B is NULL");
+  if (K > 0 && (lda < K || ldb < N)) return fail(AWE_ERR_INVALID_VALUE, "leading dimension too small");
+  if (ldc < N) return fail(AWE_ERR_INVALID_VALUE, "ldc < N");
+  // uniqueness: prod m > 2 K bound_a bound_b  <=>  bound_a bound_b <= (prod m - 1) / (2K)
+  if (K > 0) {
+    const unsigned __int128 ab = (unsigned __int128)(uint64_t)bound_a * (uint64_t)bound_b;
+    if (ab > (Mprod - 1) / (2 * (unsigned __int128)(uint64_t)K))
+      return fail(AWE_ERR_OVERFLOW, "product of the moduli must exceed 2 K bound_a bound_b");
+  }
+  const CrtLayout L = crt_layout(moduli, n, M, N, K, &st);
+  if (st != AWE_OK) return st;
+  if (L.total > 0 && (workspace == nullptr || ws_bytes < L.total))
+    return fail(AWE_ERR_WORKSPACE, "workspace smaller than awe_crt_workspace_bytes");
+  uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+  uint8_t* ra = ws;
+  uint8_t* rb = ra + L.res_a;
+  int32_t* rc = reinterpret_cast<int32_t*>(rb + L.res_b);
+  uint8_t* planes = rb + L.res_b + L.res_c;
+  if (K > 0) {
+    st = launch_residues(A, M, K, lda, bound_a, rp, ra, M * K, d_range_flag, stream);
+    if (st != AWE_OK) return st;
+    st = launch_residues(B, K, N, ldb, bound_b, rp, rb, K * N, d_range_flag, stream);
+    if (st != AWE_OK) return st;
+  }
+  for (int j = 0; j < n; ++j) {
+    const Scheme* s = scheme_or_fail(AWE_ENC_MOD, moduli[j], &st);
+    if (!s) return st;
+    st = exact_impl(*s, M, N, K, ra + (size_t)j * M * K, K, rb + (size_t)j * K * N, N, rc + (size_t)j * M * N,
+                    N, AWE_I32, planes, L.planes, nullptr, stream);
+    if (st != AWE_OK) return st;
+  }
+  if (c128 == nullptr && c64 == nullptr) return AWE_OK;
+  return launch_crt(rc, M * N, M, N, N, cp, c128, c64, ldc, stream);
 }
 
 const char* awe_status_string(awe_status s) {

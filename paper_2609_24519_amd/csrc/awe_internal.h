@@ -92,6 +92,34 @@ struct GemmLaunch {
 };
 awe_status launch_gemm(const GemmLaunch& g, hipStream_t stream);
 
+// ---- residue number system (awe_rns.hip) ----
+constexpr int kMaxModuli = AWE_MAX_MODULI;
+
+struct ResidueParams {
+  int32_t n;
+  uint32_t m[kMaxModuli];
+  uint32_t minv[kMaxModuli];  // floor((2^32 - 1) / m)
+  uint32_t p32[kMaxModuli];   // 2^32 mod m
+  uint32_t p64[kMaxModuli];   // 2^64 mod m
+};
+awe_status launch_residues(const int64_t* x, int64_t rows, int64_t cols, int64_t ld, int64_t bound,
+                           const ResidueParams& P, uint8_t* out, int64_t out_stride, int32_t* flag,
+                           hipStream_t stream);
+
+struct CrtParams {
+  int32_t n;
+  uint32_t m[kMaxModuli];
+  uint32_t minv[kMaxModuli];
+  uint32_t d[kMaxModuli];       // (m_0 ... m_{j-1})^-1 mod m_j
+  uint32_t off[kMaxModuli];     // multiple of m_j above any subtracted digit sum
+  uint8_t c[kMaxModuli][kMaxModuli];  // c[i][j] = (m_0 ... m_{i-1}) mod m_j, i < j
+  uint64_t M_lo, M_hi;          // M = m_0 ... m_{n-1} < 2^127
+  uint64_t half_lo, half_hi;    // floor(M / 2)
+};
+awe_status launch_crt(const int32_t* res, int64_t res_stride, int64_t rows, int64_t cols,
+                      int64_t ld_res, const CrtParams& P, int64_t* c128, double* c64, int64_t ldc,
+                      hipStream_t stream);
+
 void set_error(const std::string& msg);
 
 }  // namespace awe

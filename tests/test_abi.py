@@ -115,6 +115,34 @@ def test_plane_bytes():
     assert ws == (a + 255) // 256 * 256 + b
 
 
+def test_residue_number_system_host_checks():
+    fp64 = [5, 7, 8, 9, 11, 13, 31, 37, 41, 43, 47, 53, 59, 61, 67, 71, 73, 79, 83, 89, 149, 151, 157]
+    assert awe.crt_workspace_bytes(fp64, 4096, 4096, 16384) > 23 * 4096 * 4096 * 6
+    for bad in ([4, 6], [1, 3], [300], [], list(range(2, 40))):
+        with pytest.raises(awe.AweError) as e:
+            awe.crt_workspace_bytes(bad, 4, 4, 4)
+        assert e.value.status == awe.ERR_INVALID_VALUE
+    # product above 2^127
+    big = [251, 241, 239, 233, 229, 227, 223, 211, 199, 197, 193, 191, 181, 179, 173, 167, 163]
+    with pytest.raises(awe.AweError):
+        awe.crt_workspace_bytes(big, 4, 4, 4)
+    L = awe.lib()
+    fake = ctypes.c_void_p(4096)
+    arr = (ctypes.c_int32 * 3)(3, 5, 7)
+    # uniqueness: 105 <= 2 K bound_a bound_b, rejected before anything is enqueued
+    assert L.awe_gemm_crt(8, 8, 16384, fake, 16384, fake, 8, 1, 1, arr, 3, fake, None, 8, fake,
+                          1 << 40, None, None) == awe.ERR_OVERFLOW
+    # a modulus without a scheme in the supported families
+    arr2 = (ctypes.c_int32 * 2)(251, 3)
+    assert L.awe_gemm_crt(8, 8, 1, fake, 1, fake, 8, 1, 1, arr2, 2, fake, None, 8, fake, 1 << 40,
+                          None, None) == awe.ERR_UNSUPPORTED
+    # residues accept moduli that are not coprime; reconstruction does not
+    arr3 = (ctypes.c_int32 * 2)(4, 6)
+    assert L.awe_residues(fake, 0, 4, 4, 1, arr3, 2, fake, 16, None, None) == awe.OK
+    assert L.awe_crt(fake, 16, 4, 4, 4, arr3, 2, fake, None, 4, None) == awe.ERR_INVALID_VALUE
+    assert L.awe_residues(fake, 4, 4, 4, 1, arr, 3, fake, 15, None, None) == awe.ERR_INVALID_VALUE
+
+
 def test_error_paths_host_only():
     L = awe.lib()
     i = awe.EncodingInfo()

@@ -1,0 +1,163 @@
+"""GPU parity of the residue-number-system route (Sec. 5.3) against the oracle:
+residues of int64 matrices, the Chinese-remainder reconstruction (128-bit words and
+nearest double), and the exact product of 53-bit integer matrices through the FP64
+residue set (23 moduli) at K = 16,384."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import crt as ocrt
+from oracle import gemm as og
+from paper_2609_24519_amd import awe, inputs
+from tests.gpu_helpers import to_dev
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+B53 = (1 << 53) - 1
+
+
+def _moduli():
+    with open(os.path.join(GOLDEN, "moduli_fp64_k16384.txt")) as f:
+        lines = [l for l in f if l.strip() and not l.startswith("#")]
+    return [int(x) for x in lines[0].split()]
+
+
+def _words_to_ints(c128):
+    w = c128.cpu().numpy().reshape(-1, 2)
+    return np.array([(int(h) << 64) + (int(l) & ((1 << 64) - 1)) for l, h in w],
+                    dtype=object).reshape(c128.shape[:-1])
+
+
+@pytest.mark.parametrize("shape", [(1, 1), (37, 129), (300, 65), (64, 1000)])
+def test_residues(shape):
+    rows, cols = shape
+    # every modulus of the FP64 set, plus the extremes of the allowed range (residues
+    # need no coprimality)
+    ms = _moduli() + [2, 3, 255, 256]
+    rng = np.random.default_rng(rows * 7 + cols)
+    x = rng.integers(-(1 << 63), (1 << 63) - 1, size=(rows, cols), dtype=np.int64, endpoint=True)
+    x.ravel()[: min(6, x.size)] = [-(1 << 63), (1 << 63) - 1, -1, 0, B53, -B53][: min(6, x.size)]
+    ld = cols + 3
+    xp = np.zeros((rows, ld), dtype=np.int64)
+    xp[:, :cols] = x
+    xd = to_dev(xp)
+    for chunk in (ms[:12], ms[12:]):
+        if not chunk:
+            continue
+        out = torch.empty(len(chunk) * rows * cols, dtype=torch.uint8, device="cuda")
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        awe.residues(xd, rows, cols, ld, (1 << 63) - 1, chunk, out, rows * cols, flag)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().reshape(len(chunk), rows, cols)
+        for j, m in enumerate(chunk):
+            assert np.array_equal(got[j], ocrt.residues(x, m).astype(np.uint8)), m
+        # the bound 2^63 - 1 excludes only -2^63, which the first entry holds
+        assert int(flag.item()) == int(bool((x == np.iinfo(np.int64).min).any()))
+
+
+def test_residues_range_flag():
+    x = np.array([[B53, -B53, 0, B53 + 1]], dtype=np.int64)
+    out = torch.empty(4, dtype=torch.uint8, device="cuda")
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    awe.residues(to_dev(x), 1, 4, 4, B53, [13], out, 4, flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) != 0
+    assert np.array_equal(out.cpu().numpy(), ocrt.residues(x[0], 13))
+
+
+@pytest.mark.parametrize("moduli", ["fp64", [3, 5, 7], [256, 255, 253, 251]])
+def test_crt_reconstruction(moduli):
+    ms = _moduli() if moduli == "fp64" else moduli
+    M = ocrt.modulus_product(ms)
+    rng = np.random.default_rng(len(ms))
+    rows, cols = 33, 70
+    vals = [int.from_bytes(rng.bytes(16), "little") % M - M // 2 for _ in range(rows * cols)]
+    edge = [0, 1, -1, M // 2, -(M // 2) + 1, M // 2 - 1]
+    vals[: len(edge)] = edge
+    X = np.array(vals, dtype=object).reshape(rows, cols)
+    ld = cols + 5
+    stride = rows * ld + 7
+    res = np.zeros((len(ms), stride), dtype=np.int32)
+    for j, m in enumerate(ms):
+        r = np.vectorize(lambda v: v % m, otypes=[np.int64])(X)
+        res[j, : rows * ld].reshape(rows, ld)[:, :cols] = r
+    c128 = torch.empty((rows, cols, 2), dtype=torch.int64, device="cuda")
+    c64 = torch.empty((rows, cols), dtype=torch.float64, device="cuda")
+    awe.crt(to_dev(res), stride, rows, cols, ld, ms, c128, c64, cols)
+    torch.cuda.synchronize()
+    assert (_words_to_ints(c128) == X).all()
+    assert np.array_equal(c64.cpu().numpy(), ocrt.to_double(X))
+
+
+def test_crt_double_rounding_edges():
+    # integers just around ties at several magnitudes: the double must be the
+    # correctly rounded one (ties to even), including values with a nonzero high word
+    ms = _moduli()
+    vals = []
+    for e in (53, 60, 64, 65, 80, 100, 118):
+        base = 1 << e
+        ulp = 1 << (e - 52)
+        for d in (0, 1, ulp // 2 - 1, ulp // 2, ulp // 2 + 1, ulp - 1, ulp + ulp // 2):
+            vals += [base + d, -(base + d)]
+    X = np.array(vals, dtype=object).reshape(1, -1)
+    n = X.shape[1]
+    res = np.stack([np.vectorize(lambda v: v % m, otypes=[np.int64])(X).astype(np.int32).ravel()
+                    for m in ms])
+    c64 = torch.empty((1, n), dtype=torch.float64, device="cuda")
+    awe.crt(to_dev(res), n, 1, n, n, ms, None, c64, n)
+    torch.cuda.synchronize()
+    assert np.array_equal(c64.cpu().numpy(), ocrt.to_double(X))
+
+
+def _int53_pair(M, N, K, seed):
+    rng = np.random.default_rng(seed)
+    A = rng.integers(-B53, B53, size=(M, K), dtype=np.int64, endpoint=True)
+    B = rng.integers(-B53, B53, size=(K, N), dtype=np.int64, endpoint=True)
+    return A, B
+
+
+@pytest.mark.parametrize("shape", [(40, 24, 16384), (33, 65, 1000), (5, 7, 1)])
+def test_gemm_crt_full(shape):
+    M, N, K = shape
+    ms = _moduli()
+    A, B = _int53_pair(M, N, K, seed=M + N + K)
+    c128, c64 = awe.matmul_crt(to_dev(A), to_dev(B), ms, B53, B53)
+    torch.cuda.synchronize()
+    ref = og.gemm_i128(A, B)
+    assert (_words_to_ints(c128) == ref).all()
+    assert np.array_equal(c64.cpu().numpy(), ocrt.to_double(ref))
+
+
+def test_gemm_crt_extremes():
+    # every product at the bound: C = -K B^2 needs 120 bits and the top of the range
+    ms = _moduli()
+    K = 16384
+    A = np.full((32, K), B53, dtype=np.int64)
+    B = np.full((K, 16), -B53, dtype=np.int64)
+    B[:, 1::2] = B53
+    c128, c64 = awe.matmul_crt(to_dev(A), to_dev(B), ms, B53, B53)
+    torch.cuda.synchronize()
+    got = _words_to_ints(c128)
+    assert (got[:, 0::2] == -K * B53 * B53).all() and (got[:, 1::2] == K * B53 * B53).all()
+    assert (c64.cpu().numpy()[:, 1] == float(K * B53 * B53)).all()
+
+
+def test_gemm_crt_4096_sampled():
+    # the FP64-significand workload: 4096 x 4096 x 16384, |entries| <= 2^53 - 1, 23 moduli
+    ms = _moduli()
+    M = N = 4096
+    K = 16384
+    A, B = _int53_pair(M, N, K, seed=0)
+    c128, c64 = awe.matmul_crt(to_dev(A), to_dev(B), ms, B53, B53)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(1)
+    rows = np.concatenate([[0, M - 1], rng.choice(M, 30, replace=False)])
+    cols = np.concatenate([[0, N - 1], rng.choice(N, 30, replace=False)])
+    ref = og.gemm_i128_sampled(A, B, rows, cols)
+    sub = c128[torch.as_tensor(rows, device="cuda")][:, torch.as_tensor(cols, device="cuda")]
+    assert (_words_to_ints(sub) == ref).all()
+    sub64 = c64[torch.as_tensor(rows, device="cuda")][:, torch.as_tensor(cols, device="cuda")]
+    assert np.array_equal(sub64.cpu().numpy(), ocrt.to_double(ref))

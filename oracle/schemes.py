@@ -71,6 +71,8 @@ class Scheme:
         self.range_a = range_a  # inclusive input range the A table must cover
         self.range_b = range_b
         self.n_g = n_g
+        # sides whose limbs are base-13 positional digits instead of the choice rule
+        self.positional = ()
         # distinct stored planes per side, in order of first use
         self.planes_a = []
         self.planes_b = []
@@ -162,10 +164,21 @@ def b13():
             j = s - i
             if 0 <= j < 3:
                 prods.append((_e(i, 3), _e(j, 3), 13 ** s))
-    return Scheme("b13", (1, 13, 169), (1, 13, 169), prods, 1, 8, 8, INT8_RANGE, INT8_RANGE, n_g=3)
+    s = Scheme("b13", (1, 13, 169), (1, 13, 169), prods, 1, 8, 8, INT8_RANGE, INT8_RANGE, n_g=3)
+    s.positional = ("a", "b")
+    return s
 
 
-PAPER_SCHEMES = {"b13": b13, "awe6": awe6, "awe6_alt": awe6_alt, "awe4": awe4}
+def ternary():
+    """{0, +-1} x INT8 in 3 products (Sec. 6.2): a ternary weight is one limb (w = (1,)),
+    the INT8 side takes base-13 positional limbs, and C = sum_j 13^j (a)(b_j)."""
+    prods = [((1,), _e(j, 3), 13 ** j) for j in range(3)]
+    s = Scheme("ternary", (1,), (1, 13, 169), prods, 1, 1, 8, (-1, 1), INT8_RANGE)
+    s.positional = ("b",)
+    return s
+
+
+PAPER_SCHEMES = {"b13": b13, "awe6": awe6, "awe6_alt": awe6_alt, "awe4": awe4, "ternary": ternary}
 
 
 # ---------------------------------------------------------------------------
@@ -309,7 +322,7 @@ def k_star(n_g, c_a, c_b, F=24):
 def limb_table(s, side):
     """x -> limb tuple for every x in the side's input range."""
     lo, hi = s.range_a if side == "a" else s.range_b
-    if s.name == "b13":
+    if side in s.positional:
         return {x: b13_digits(x) for x in range(lo, hi + 1)}
     w = s.w if side == "a" else s.v
     planes = s.planes_a if side == "a" else s.planes_b

@@ -86,7 +86,7 @@ def test_kstar_formula(paper):
     assert sc.k_star(1, 14, 14) == paper["kstar.fp8fp4"][0]
 
 
-@pytest.mark.parametrize("name", ["b13", "awe6", "awe6_alt", "awe4"])
+@pytest.mark.parametrize("name", ["b13", "awe6", "awe6_alt", "awe4", "ternary"])
 def test_round_trip_and_storability(name):
     s = sc.PAPER_SCHEMES[name]()
     for side in ("a", "b"):
@@ -103,12 +103,12 @@ def test_round_trip_and_storability(name):
                 assert sc.dot(c, a) in sc.S_SET and abs(sc.dot(c, a)) <= cap
 
 
-@pytest.mark.parametrize("name", ["b13", "awe6", "awe6_alt", "awe4"])
+@pytest.mark.parametrize("name", ["b13", "awe6", "awe6_alt", "awe4", "ternary"])
 def test_brute_force_all_pairs(name):
     assert sc.brute_force_pairs(sc.PAPER_SCHEMES[name]())
 
 
-@pytest.mark.parametrize("name", ["awe6", "awe6_alt", "awe4"])
+@pytest.mark.parametrize("name", ["awe6", "awe6_alt", "awe4", "ternary"])
 def test_identity_all_admissible(name):
     assert sc.identity_all_admissible(sc.PAPER_SCHEMES[name]())
 
@@ -121,6 +121,21 @@ def test_scheme_gemm_equals_plain_product():
     for name in ("b13", "awe6", "awe6_alt"):
         assert np.array_equal(sc.scheme_gemm(sc.PAPER_SCHEMES[name](), A, B), A @ B)
     assert np.array_equal(sc.scheme_gemm(sc.awe4(), A4, B), A4 @ B)
+
+
+def test_ternary_scheme(paper):
+    # Sec. 6.2: {0, +-1} x INT8 takes 3 products; the INT8 side keeps its base-13 digits
+    # (largest |digit| 8), the ternary side one limb, so K* = 2^24 / (1 * 8)
+    s = sc.ternary()
+    assert s.r == 3 and len(s.planes_a) == 1 and len(s.planes_b) == 3
+    assert sc.stored_cap(s, "a") == 1 and sc.stored_cap(s, "b") == 8
+    assert sc.k_star(1, sc.stored_cap(s, "a"), sc.stored_cap(s, "b")) == paper["kstar.ternary_int8"][0]
+    assert sc.coefficient_identity_holds(s)
+    rng = np.random.default_rng(4)
+    A = rng.integers(-1, 1, (11, 50), endpoint=True)
+    B = rng.integers(-128, 127, (50, 7), endpoint=True)
+    assert np.array_equal(sc.scheme_gemm(s, A, B), A @ B)
+    assert sc.limb_table(s, "b") == {x: sc.b13_digits(x) for x in range(-128, 128)}
 
 
 def test_endpoints_are_covered():

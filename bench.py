@@ -8,7 +8,8 @@ encode A, encode B, the r FP4 products with their fused reconstruction
 The workload is M = N = K = 8192 with int8 entries uniform in [-128, 127]
 (seed 0) and int32 C.  Printed: one JSON line with the end-to-end exact TOPS
 as ``value``, the roofline of the dominant kernel (the GEMM) from HIP events
-on its stream, the 9-product base-13 baseline, the native INT8 MFMA GEMM
+on its stream, the 9-product base-13 baseline, the 3-product {0,+-1} x INT8
+GEMM, the native INT8 MFMA GEMM
 (hipBLASLt through torch._int_mm), the residue-number-system route for 53-bit
 integers (the integer layer of Ozaki scheme II) and the sustained rate of the
 FP4 MFMA alone timed in the same run as context, and the oracle timed on the host's cores on
@@ -150,6 +151,24 @@ def main():
         except Exception as ex:  # noqa: BLE001 - context only
             line["int8_mfma_context"] = {"error": str(ex)[:200]}
     if not args.no_context:
+        # {0, +-1} x INT8 (Sec. 6.2) on the same B: 3 products
+        At = torch.from_numpy(inputs.int8_pair(M, 8, K, seed=5, a_range=(-1, 1))[0]).to(dev)
+        tinfo, pta, ptb = setup(awe.ENC_TERNARY)
+        awe.encode(awe.ENC_TERNARY, 0, awe.SIDE_A, At, M, K, K, pta, None, stream)
+        awe.encode(awe.ENC_TERNARY, 0, awe.SIDE_B, B, N, K, N, ptb, None, stream)
+        awe.gemm_planes(awe.ENC_TERNARY, 0, M, N, K, pta, ptb, C, N, awe.I32, 0, stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(5):
+            awe.gemm_planes(awe.ENC_TERNARY, 0, M, N, K, pta, ptb, C, N, awe.I32, 0, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tms = e0.elapsed_time(e1) / 5
+        line["ternary_3_products"] = {
+            "gemm_ms": round(tms, 4), "gemm_exact_TOPS": round(ops / (tms * 1e-3) / 1e12, 2),
+            "fp4_peak_frac": round(tinfo["r"] * ops / (tms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
+        del At, pta, ptb
         line["ozaki2_int53"] = ozaki2_context(dev)
         probe = mfma_sustained()
         if probe:

@@ -74,7 +74,9 @@ typedef enum awe_encoding {
   AWE_ENC_AWE6ALT = 3, /* INT8 x INT8 in 6 products, w = v = (1, 11, 39) (Sec. 4.3; App. A) */
   AWE_ENC_AWE4 = 4,    /* INT4 x INT8 in 4 products, A = 3a0 + 5a1, B = 5b0 + 3b1 + 42b2, D = 2
                           (App. A).  The int4 operand is stored one value per int8 byte. */
-  AWE_ENC_MOD = 5      /* residues modulo m (Sec. 5.3); needs the modulus argument */
+  AWE_ENC_MOD = 5,     /* residues modulo m (Sec. 5.3); needs the modulus argument */
+  AWE_ENC_TERNARY = 6  /* {0, +-1} x INT8 in 3 products: the ternary A entry is one limb, B takes
+                          the base-13 limbs, C = sum_j 13^j P_j (Sec. 6.2).  A is int8 in [-1, 1]. */
 } awe_encoding;
 
 typedef enum awe_side { AWE_SIDE_A = 0, AWE_SIDE_B = 1 } awe_side;
@@ -125,7 +127,8 @@ awe_status awe_plane_bytes(awe_encoding enc, int32_t modulus, awe_side side,
 
 /* Encode one operand into its stored planes (Alg. 1, first two loops).
    side A: x is rows x K, x[i*ld + k];  side B: x is K x rows, x[k*ld + j] (rows = N).
-   x holds int8 (exact encodings; int4 values for the A side of AWE_ENC_AWE4) or uint8
+   x holds int8 (exact encodings; int4 values for the A side of AWE_ENC_AWE4, values in
+   [-1, 1] for the A side of AWE_ENC_TERNARY) or uint8
    residues (AWE_ENC_MOD).  planes receives awe_plane_bytes bytes.  A value outside the
    encoding's range is stored as 0 and, when d_range_flag is not NULL, sets *d_range_flag
    to a nonzero value (the flag is never cleared by the library). */

@@ -37,7 +37,7 @@ struct Scheme {
   int log2D = 0;
   int cap_a = 12, cap_b = 12;        // bound on |stored value| the tables may use
   int32_t xmin_a = 0, xmax_a = 0, xmin_b = 0, xmax_b = 0;
-  bool positional13 = false;          // base-13 digits with carries instead of the choice rule
+  bool positional13_a = false, positional13_b = false;  // base-13 digits with carries instead of the choice rule
   bool a_unsigned = false, b_unsigned = false;  // residues arrive as uint8
 
   // derived by build_tables()

@@ -114,10 +114,34 @@ void define_b13(Scheme& s) {
       s.ell[s.r] = pw;
       ++s.r;
     }
-  s.positional13 = true;
+  s.positional13_a = s.positional13_b = true;
   s.cap_a = s.cap_b = 12;
   s.xmin_a = s.xmin_b = -128;
   s.xmax_a = s.xmax_b = 127;
+}
+
+// {0, +-1} x INT8 in 3 products (Sec. 6.2): a ternary value is one limb of
+// weight 1 on A; B takes the three base-13 positional limbs; C = sum_j 13^j P_j.
+void define_ternary(Scheme& s) {
+  s.p = 1;
+  s.q = 3;
+  s.w[0] = 1;
+  s.v[0] = 1; s.v[1] = 13; s.v[2] = 169;
+  s.na = 1;
+  s.nb = 3;
+  s.alpha[0][0] = 1;
+  for (int k = 0; k < 3; ++k) s.beta[k][k] = 1;
+  s.r = 3;
+  for (int k = 0; k < 3; ++k) {
+    s.pa[k] = 0;
+    s.pb[k] = k;
+    s.ell[k] = k == 0 ? 1 : (k == 1 ? 13 : 169);
+  }
+  s.positional13_b = true;
+  s.cap_a = 1;
+  s.cap_b = 12;
+  s.xmin_a = -1; s.xmax_a = 1;
+  s.xmin_b = -128; s.xmax_b = 127;
 }
 
 // ---- limb tuples ----------------------------------------------------------
@@ -217,7 +241,7 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
     while (X < 2047 && hit[X + 1 + 2047] && hit[-(X + 1) + 2047]) ++X;
     (sideA ? s.coverage_a : s.coverage_b) = X;
   }
-  if (s.positional13) {
+  if (sideA ? s.positional13_a : s.positional13_b) {
     for (int x = xmin; x <= xmax; ++x) {
       int d[3];
       base13_digits(x, d);
@@ -462,7 +486,7 @@ int64_t plane_stride_bytes(int64_t rows, int64_t K) {
 }
 
 const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std::string* msg) {
-  if (enc < AWE_ENC_B13 || enc > AWE_ENC_MOD) {
+  if (enc < AWE_ENC_B13 || enc > AWE_ENC_TERNARY) {
     *st = AWE_ERR_INVALID_VALUE;
     *msg = "unknown encoding";
     return nullptr;
@@ -493,6 +517,7 @@ const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std:
     case AWE_ENC_AWE6: define_awe6(*s, false); break;
     case AWE_ENC_AWE6ALT: define_awe6(*s, true); break;
     case AWE_ENC_AWE4: define_awe4(*s); break;
+    case AWE_ENC_TERNARY: define_ternary(*s); break;
     case AWE_ENC_MOD:
       ok = define_mod(*s, modulus, &m);
       if (!ok) fail = AWE_ERR_UNSUPPORTED;

@@ -15,7 +15,8 @@ import pytest
 from oracle import modm, schemes as sc
 from paper_2609_24519_amd import awe
 
-EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4}
+EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
+         "ternary": awe.ENC_TERNARY}
 
 
 @lru_cache(maxsize=None)

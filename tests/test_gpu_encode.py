@@ -10,7 +10,8 @@ from tests.gpu_helpers import decode_planes, to_dev
 
 pytestmark = pytest.mark.gpu
 
-EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4}
+EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
+         "ternary": awe.ENC_TERNARY}
 
 
 def _encode(enc, m, side, X, rows, K, flag=None):

@@ -15,7 +15,7 @@ from tests.gpu_helpers import to_dev
 
 pytestmark = pytest.mark.gpu
 
-EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4]
+EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4, awe.ENC_TERNARY]
 
 
 def _run_exact(enc, A, B, out=torch.int32):
@@ -26,7 +26,7 @@ def _run_exact(enc, A, B, out=torch.int32):
 
 
 def _operands(enc, M, N, K, seed):
-    a_range = (-8, 7) if enc == awe.ENC_AWE4 else (-128, 127)
+    a_range = {awe.ENC_AWE4: (-8, 7), awe.ENC_TERNARY: (-1, 1)}.get(enc, (-128, 127))
     return inputs.int8_pair(M, N, K, seed, a_range=a_range)
 
 
@@ -162,7 +162,7 @@ def test_mod_forced_segments():
 
 
 @pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4", "5"])
-@pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13])
+@pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13, awe.ENC_TERNARY])
 def test_every_tile_configuration(monkeypatch, cfg, enc):
     # AWE_GEMM_CFG forces one of the GEMM's tile configurations (256x128 on 4 or 8
     # waves with 2 or 4 k-steps per stage, 256x192 on 8 waves, fragments read one or
@@ -178,3 +178,16 @@ def test_every_tile_configuration(monkeypatch, cfg, enc):
     torch.cuda.synchronize()
     assert np.array_equal(Cm.cpu().numpy(), og.gemm_mod(m, Ar, Br))
 
+
+
+def test_ternary_4096_sampled():
+    # {0, +-1} x INT8 (Sec. 6.2) at 4096 x 4096 x 8192, int32 C, sampled tiles
+    M = N = 4096
+    K = 8192
+    A, B = inputs.int8_pair(M, N, K, seed=3, a_range=(-1, 1))
+    C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_TERNARY, torch.int32)
+    torch.cuda.synchronize()
+    Ch = C.cpu().numpy()
+    for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=2):
+        ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
+        assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)

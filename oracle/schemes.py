@@ -178,7 +178,30 @@ def ternary():
     return s
 
 
-PAPER_SCHEMES = {"b13": b13, "awe6": awe6, "awe6_alt": awe6_alt, "awe4": awe4, "ternary": ternary}
+def fp16_12():
+    """FP16 x FP16 significands in 12 products, App. A: weights (1, 9, 71, 639) on both sides.
+
+    With P_ij = a_i b_j and Q_kl = (a_{2k} + 2 a_{2k+1})(b_{2l} + 2 b_{2l+1}), k, l in {0, 1}:
+    2AB = sum_{k,l} 71^(k+l) (-7 P_{2k,2l} + 126 P_{2k+1,2l+1} + 9 Q_kl), D = 2; stored values
+    within 12.  Products are listed grouped by (k, l), in that order inside each group.
+    The input range is the 12-bit two's-complement range (coverage 2160 reaches past it).
+    """
+    def q(k):
+        return tuple(1 if t == 2 * k else (2 if t == 2 * k + 1 else 0) for t in range(4))
+
+    prods = []
+    for k in (0, 1):
+        for l in (0, 1):
+            o = 71 ** (k + l)
+            prods.append((_e(2 * k, 4), _e(2 * l, 4), -7 * o))
+            prods.append((_e(2 * k + 1, 4), _e(2 * l + 1, 4), 126 * o))
+            prods.append((q(k), q(l), 9 * o))
+    w = (1, 9, 71, 639)
+    return Scheme("fp16_12", w, w, prods, 2, 12, 12, (-2048, 2047), (-2048, 2047))
+
+
+PAPER_SCHEMES = {"b13": b13, "awe6": awe6, "awe6_alt": awe6_alt, "awe4": awe4, "ternary": ternary,
+                 "fp16_12": fp16_12}
 
 
 # ---------------------------------------------------------------------------

@@ -8,6 +8,7 @@ brute force over every input pair.  The mutation tests plant a mistake in a
 copy of a scheme and require the pins to catch it.
 """
 import copy
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -191,3 +192,31 @@ def test_mutation_wrong_weight_caught():
     except ValueError:  # the weights may no longer cover the int8 range
         ok = False
     assert not ok
+
+
+def test_fp16_12_scheme(paper):
+    # App. A: FP16 x FP16 significands in 12 products
+    s = sc.fp16_12()
+    assert s.w == tuple(paper["fp16_12.w"]) and s.r == paper["fp16_12.products"][0]
+    assert s.D == paper["fp16_12.D"][0]
+    inner = paper["fp16_12.inner_ell"]
+    o = paper["fp16_12.outer"][0]
+    assert [l for _, _, l in s.products] == [x * o ** (k + l) for k in (0, 1) for l in (0, 1)
+                                              for x in inner]
+    assert len(s.planes_a) == 6 and len(s.planes_b) == 6
+    assert sc.coefficient_identity_holds(s)
+    # re-solving the coefficients from planes and weights alone gives the same ell / D
+    assert sc.solve_ell(s) == [Fraction(l, s.D) for _, _, l in s.products]
+    # coverage of the weights over the admissible tuples at cap 12, and the K* bound
+    assert sc.coverage(s.w, sc.admissible(s.planes_a, 4, 12)) == paper["fp16_12.coverage"][0]
+    ca, cb = sc.stored_cap(s, "a"), sc.stored_cap(s, "b")
+    assert (ca, cb) == tuple(paper["fp16_12.cap"])
+    assert sc.k_star(1, ca, cb) == paper["fp16_12.kstar"][0]
+
+
+def test_fp16_12_all_input_pairs():
+    # every pair of 12-bit inputs through the tables: sum_k ell_k planeA planeB = 2 x y
+    s = sc.fp16_12()
+    assert sc.brute_force_pairs(s)
+    limbs = sc.limb_table(s, "a")
+    assert all(sc.dot(s.w, limbs[x]) == x for x in range(-2048, 2048))

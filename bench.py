@@ -9,7 +9,7 @@ The workload is M = N = K = 8192 with int8 entries uniform in [-128, 127]
 (seed 0) and int32 C.  Printed: one JSON line with the end-to-end exact TOPS
 as ``value``, the roofline of the dominant kernel (the GEMM) from HIP events
 on its stream, the 9-product base-13 baseline, the 3-product {0,+-1} x INT8
-GEMM, the native INT8 MFMA GEMM
+GEMM, the 12-product FP16-significand GEMM, the native INT8 MFMA GEMM
 (hipBLASLt through torch._int_mm), the residue-number-system route for 53-bit
 integers (the integer layer of Ozaki scheme II) and the sustained rate of the
 FP4 MFMA alone timed in the same run as context, and the oracle timed on the host's cores on
@@ -169,6 +169,7 @@ def main():
             "gemm_ms": round(tms, 4), "gemm_exact_TOPS": round(ops / (tms * 1e-3) / 1e12, 2),
             "fp4_peak_frac": round(tinfo["r"] * ops / (tms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
         del At, pta, ptb
+        line["fp16_12_products"] = fp16_context(dev, M)
         line["ozaki2_int53"] = ozaki2_context(dev)
         probe = mfma_sustained()
         if probe:
@@ -184,6 +185,43 @@ def main():
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(A_h, B_h)
     print(json.dumps(line), flush=True)
+
+
+def fp16_context(dev, n):
+    """App. A's FP16-significand scheme: 12-bit integers (int16 in [-2048, 2047]) in 12 FP4
+    products (four launch groups), n^3, int64 C, awe_gemm_planes on resident planes."""
+    import numpy as np
+    import torch
+
+    from paper_2609_24519_amd import awe, inputs
+
+    rng = np.random.default_rng(7)
+    A = torch.from_numpy(inputs.uniform(rng, (n, n), -2048, 2047, np.int16)).to(dev)
+    B = torch.from_numpy(inputs.uniform(rng, (n, n), -2048, 2047, np.int16)).to(dev)
+    enc = awe.ENC_FP16
+    info = awe.get_encoding_info(enc)
+    pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, n, n), dtype=torch.uint8, device=dev)
+    pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, n, n), dtype=torch.uint8, device=dev)
+    C = torch.empty((n, n), dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+    awe.encode(enc, 0, awe.SIDE_A, A, n, n, n, pa, None, stream)
+    awe.encode(enc, 0, awe.SIDE_B, B, n, n, n, pb, None, stream)
+    awe.gemm_planes(enc, 0, n, n, n, pa, pb, C, n, awe.I64, 0, stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(3):
+        awe.gemm_planes(enc, 0, n, n, n, pa, pb, C, n, awe.I64, 0, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 3
+    ops = 2.0 * n * n * n
+    out = {"workload": "M=N=K=%d, int16 entries uniform in [-2048, 2047], int64 C" % n,
+           "gemm_ms": round(ms, 3), "gemm_exact_TOPS": round(ops / (ms * 1e-3) / 1e12, 1),
+           "fp4_peak_frac": round(info["r"] * ops / (ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
+    del A, B, pa, pb, C
+    torch.cuda.empty_cache()
+    return out
 
 
 def ozaki2_context(dev, M=4096, N=4096, K=16384):

@@ -75,8 +75,12 @@ typedef enum awe_encoding {
   AWE_ENC_AWE4 = 4,    /* INT4 x INT8 in 4 products, A = 3a0 + 5a1, B = 5b0 + 3b1 + 42b2, D = 2
                           (App. A).  The int4 operand is stored one value per int8 byte. */
   AWE_ENC_MOD = 5,     /* residues modulo m (Sec. 5.3); needs the modulus argument */
-  AWE_ENC_TERNARY = 6  /* {0, +-1} x INT8 in 3 products: the ternary A entry is one limb, B takes
+  AWE_ENC_TERNARY = 6, /* {0, +-1} x INT8 in 3 products: the ternary A entry is one limb, B takes
                           the base-13 limbs, C = sum_j 13^j P_j (Sec. 6.2).  A is int8 in [-1, 1]. */
+  AWE_ENC_FP16 = 7     /* FP16-significand integers x FP16-significand integers in 12 products,
+                          w = v = (1, 9, 71, 639), D = 2 (App. A).  Both operands are int16 in
+                          [-2048, 2047]; the products run as four launches, one per outer weight
+                          71^(k+l), each adding its share into C. */
 } awe_encoding;
 
 typedef enum awe_side { AWE_SIDE_A = 0, AWE_SIDE_B = 1 } awe_side;
@@ -128,7 +132,7 @@ awe_status awe_plane_bytes(awe_encoding enc, int32_t modulus, awe_side side,
 /* Encode one operand into its stored planes (Alg. 1, first two loops).
    side A: x is rows x K, x[i*ld + k];  side B: x is K x rows, x[k*ld + j] (rows = N).
    x holds int8 (exact encodings; int4 values for the A side of AWE_ENC_AWE4, values in
-   [-1, 1] for the A side of AWE_ENC_TERNARY) or uint8
+   [-1, 1] for the A side of AWE_ENC_TERNARY), int16 (AWE_ENC_FP16) or uint8
    residues (AWE_ENC_MOD).  planes receives awe_plane_bytes bytes.  A value outside the
    encoding's range is stored as 0 and, when d_range_flag is not NULL, sets *d_range_flag
    to a nonzero value (the flag is never cleared by the library). */
@@ -152,10 +156,11 @@ awe_status awe_workspace_bytes(awe_encoding enc, int32_t modulus, int64_t M, int
                                int64_t K, size_t* bytes);
 
 /* C = A B exactly (Alg. 1 end to end): encode A, encode B, products, reconstruction.
-   enc is one of the exact encodings.  int8 A (int4 values for AWE_ENC_AWE4) and int8 B.
+   enc is one of the exact encodings.  A and B hold int8 (int4 values for the A side of
+   AWE_ENC_AWE4, [-1, 1] for the A side of AWE_ENC_TERNARY) or int16 (AWE_ENC_FP16).
    c_type AWE_I32 requires max|A| max|B| K <= 2^31 - 1 (else AWE_ERR_OVERFLOW). */
 awe_status awe_gemm_exact(awe_encoding enc, int64_t M, int64_t N, int64_t K,
-                          const int8_t* A, int64_t lda, const int8_t* B, int64_t ldb,
+                          const void* A, int64_t lda, const void* B, int64_t ldb,
                           void* C, int64_t ldc, awe_dtype c_type,
                           void* workspace, size_t ws_bytes, int32_t* d_range_flag,
                           hipStream_t stream);

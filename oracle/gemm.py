@@ -162,3 +162,12 @@ def gemm_i128_sampled(A, B, rows, cols, words=False):
         _load().oracle_gemm_i64_i128_sampled(rows.size, _ptr(rows), cols.size, _ptr(cols), K,
                                              _ptr(A), K, _ptr(B), N, _ptr(lo), _ptr(hi))
     return (lo, hi) if words else _join128(lo, hi)
+
+
+def gemm_i64_wide(A, B):
+    """Exact C = A B for integer operands of any width up to int64 whose product fits int64
+    (e.g. int16 significands): the 128-bit loop, checked to fit, as int64."""
+    lo, hi = gemm_i128(np.asarray(A, dtype=np.int64), np.asarray(B, dtype=np.int64), words=True)
+    C = lo.view(np.int64)
+    assert np.array_equal(hi, np.where(C < 0, -1, 0)), "product exceeds int64"
+    return C

@@ -19,9 +19,9 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "awe.h")
 # awe_status
 OK, ERR_INVALID_VALUE, ERR_UNSUPPORTED, ERR_OVERFLOW, ERR_WORKSPACE, ERR_HIP, ERR_TABLE = range(7)
 # awe_encoding
-ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY = 1, 2, 3, 4, 5, 6
+ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY, ENC_FP16 = 1, 2, 3, 4, 5, 6, 7
 ENCODINGS = {"b13": ENC_B13, "awe6": ENC_AWE6, "awe6_alt": ENC_AWE6ALT, "awe4": ENC_AWE4, "mod": ENC_MOD,
-             "ternary": ENC_TERNARY}
+             "ternary": ENC_TERNARY, "fp16_12": ENC_FP16}
 # awe_side, awe_dtype
 SIDE_A, SIDE_B = 0, 1
 I32, I64 = 0, 1

@@ -38,11 +38,20 @@ size_t side_bytes(const Scheme& s, bool sideA, int64_t rows, int64_t K) {
 
 // Largest reduction length (multiple of kKPad) one GEMM launch may cover so that
 // the int32 accumulator's true value fits: |D C| <= D max|A| max|B| K for an
-// exact scheme, |sum lambda_k P_k| <= sum|lambda_k| c_A c_B K for a congruence.
+// exact scheme, |sum lambda_k P_k| <= sum|lambda_k| c_A c_B K for a congruence,
+// and for launch groups |sum_{k in g} (ell_k / outer_g) P_k| over the worst group.
 int64_t launch_k_limit(const Scheme& s) {
   const int64_t lim = 0x7fffffffLL;
   int64_t per_k;
-  if (s.modulus) {
+  if (s.n_lgroups > 1) {
+    per_k = 1;
+    for (int g = 0; g < s.n_lgroups; ++g) {
+      int64_t sum = 0;
+      for (int k = 0; k < s.r; ++k)
+        if (s.lgroup[k] == g) sum += std::abs(s.ell[k] / s.louter[g]);
+      per_k = std::max(per_k, sum * s.c_a * s.c_b);
+    }
+  } else if (s.modulus) {
     int64_t sum = 0;
     for (int k = 0; k < s.r; ++k) sum += std::abs(s.ell[k]);
     per_k = sum * s.c_a * s.c_b;
@@ -81,14 +90,6 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
   L.M = M;
   L.N = N;
   L.K = K;
-  L.r = s.r;
-  L.fold_mask = 0;
-  for (int k = 0; k < s.r; ++k) {
-    L.pa[k] = s.pa[k];
-    L.pb[k] = s.pb[k];
-    L.fold_ell[k] = (int32_t)s.ell[k];
-    if (k == s.r - 1 || s.group[k + 1] != s.group[k]) L.fold_mask |= 1u << k;
-  }
   L.k_seg = k_seg;
   L.C = C;
   L.ldc = ldc;
@@ -102,12 +103,27 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
     L.accumulate = false;
     return launch_gemm(L, stream);
   }
+  // one launch per (reduction range, launch group); every launch after the first adds into C
   for (int64_t k0 = 0; k0 < kp; k0 += step) {
-    L.k_begin = k0;
-    L.k_end = std::min(kp, k0 + step);
-    L.accumulate = k0 > 0;
-    awe_status st = launch_gemm(L, stream);
-    if (st != AWE_OK) return st;
+    for (int g = 0; g < s.n_lgroups; ++g) {
+      L.r = 0;
+      L.fold_mask = 0;
+      for (int k = 0; k < s.r; ++k) {
+        if (s.lgroup[k] != g) continue;
+        L.pa[L.r] = s.pa[k];
+        L.pb[L.r] = s.pb[k];
+        L.fold_ell[L.r] = (int32_t)(s.ell[k] / s.louter[g]);
+        const bool last = k == s.r - 1 || s.group[k + 1] != s.group[k] || s.lgroup[k + 1] != g;
+        if (last) L.fold_mask |= 1u << L.r;
+        ++L.r;
+      }
+      L.outer = s.louter[g];
+      L.k_begin = k0;
+      L.k_end = std::min(kp, k0 + step);
+      L.accumulate = k0 > 0 || g > 0;
+      awe_status st = launch_gemm(L, stream);
+      if (st != AWE_OK) return st;
+    }
   }
   return AWE_OK;
 }
@@ -134,7 +150,12 @@ awe_status encode_impl(const Scheme& s, awe_side side, const void* x, int64_t ro
   e.planes = reinterpret_cast<uint8_t*>(planes);
   e.plane_stride = plane_stride_bytes(rows, K);
   e.flag = flag;
-  e.lut = sideA ? s.lut_a : s.lut_b;
+  e.lut = sideA ? s.lut_a.data() : s.lut_b.data();
+  e.wide = s.wide;
+  e.xmin = sideA ? s.xmin_a : s.xmin_b;
+  e.nvalues = s.table_size(sideA);
+  e.side = sideA ? 0 : 1;
+  e.table_key = &s;
   return launch_encode(e, stream);
 }
 
@@ -320,11 +341,10 @@ awe_status awe_get_plane_table(awe_encoding enc, int32_t modulus, awe_side side,
   const bool a = side == AWE_SIDE_A;
   const int lo = a ? s->xmin_a : s->xmin_b, hi = a ? s->xmax_a : s->xmax_b;
   const int np = a ? s->na : s->nb;
-  const bool uns = a ? s->a_unsigned : s->b_unsigned;
   if (values == nullptr || n_values < (int64_t)(hi - lo + 1) * np)
     return fail(AWE_ERR_INVALID_VALUE, "values too small");
   for (int x = lo; x <= hi; ++x) {
-    const int b = uns ? x : (int)(uint8_t)(int8_t)x;
+    const int b = s->table_index(a, x);
     for (int k = 0; k < np; ++k) values[(int64_t)(x - lo) * np + k] = (a ? s->val_a : s->val_b)[b][k];
   }
   return AWE_OK;
@@ -370,8 +390,8 @@ awe_status awe_workspace_bytes(awe_encoding enc, int32_t modulus, int64_t M, int
   return AWE_OK;
 }
 
-awe_status awe_gemm_exact(awe_encoding enc, int64_t M, int64_t N, int64_t K, const int8_t* A,
-                          int64_t lda, const int8_t* B, int64_t ldb, void* C, int64_t ldc,
+awe_status awe_gemm_exact(awe_encoding enc, int64_t M, int64_t N, int64_t K, const void* A,
+                          int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                           awe_dtype c_type, void* workspace, size_t ws_bytes, int32_t* d_range_flag,
                           hipStream_t stream) {
   if (enc == AWE_ENC_MOD) return fail(AWE_ERR_INVALID_VALUE, "use awe_gemm_mod for residues");

@@ -1,7 +1,9 @@
 // Internal declarations shared by the host table code, the kernels and the C ABI.
 #pragma once
+#include <array>
 #include <cstdint>
 #include <string>
+#include <vector>
 
 #include "../../include/awe.h"
 
@@ -20,6 +22,9 @@ constexpr int kKPad = AWE_K_PAD;   // the reduction length is padded to this mul
 // LUT entry flag: the input byte is outside the encoding's range.
 constexpr uint32_t kLutInvalid = 0x80000000u;
 
+// Inputs of a wide encoding are int16 in [xmin, xmax], at most this many values.
+constexpr int kWideValues = 4096;
+
 // One scheme (Definition 4.1 of the paper, or its mod-m congruence form)
 // together with the encoding tables derived from it.
 struct Scheme {
@@ -34,19 +39,40 @@ struct Scheme {
   int32_t pa[kMaxProducts] = {}, pb[kMaxProducts] = {};
   int64_t ell[kMaxProducts] = {};
   int32_t group[kMaxProducts] = {};  // products with equal ell that share an accumulator
+  // Launch groups: the products of group g run as one GEMM launch that folds them with
+  // inner coefficients ell_k / outer_g and adds outer_g (sum) / D into C.  One group with
+  // outer 1 unless the coefficients outgrow the int32 fold (the FP16 scheme).
+  int n_lgroups = 1;
+  int32_t lgroup[kMaxProducts] = {};
+  int64_t louter[kMaxProducts] = {1};
   int log2D = 0;
   int cap_a = 12, cap_b = 12;        // bound on |stored value| the tables may use
   int32_t xmin_a = 0, xmax_a = 0, xmin_b = 0, xmax_b = 0;
   bool positional13_a = false, positional13_b = false;  // base-13 digits with carries instead of the choice rule
   bool a_unsigned = false, b_unsigned = false;  // residues arrive as uint8
+  bool wide = false;  // int16 inputs; tables indexed by x - xmin instead of the input byte
 
   // derived by build_tables()
   int c_a = 0, c_b = 0, n_g = 1;
   int32_t coverage_a = 0, coverage_b = 0;
   int64_t k_star = 0, k_seg = 0;
-  int32_t val_a[256][kMaxPlanes] = {};  // plane values per input byte (index: byte value)
-  int32_t val_b[256][kMaxPlanes] = {};
-  uint32_t lut_a[256] = {}, lut_b[256] = {};  // packed E2M1 codes per input byte
+  // Per table index (the input byte, or x - xmin for a wide encoding): the plane values
+  // and the packed E2M1 codes (kLutInvalid for an input outside the range).
+  std::vector<std::array<int32_t, kMaxPlanes>> val_a, val_b;
+  std::vector<uint32_t> lut_a, lut_b;
+  int table_size(bool sideA) const {
+    return wide ? (sideA ? xmax_a - xmin_a : xmax_b - xmin_b) + 1 : 256;
+  }
+  // Input value of table index i.
+  int table_value(bool sideA, int i) const {
+    if (wide) return i + (sideA ? xmin_a : xmin_b);
+    return (sideA ? a_unsigned : b_unsigned) ? i : (int)(int8_t)(uint8_t)i;
+  }
+  // Table index of input value x (which must lie in the range).
+  int table_index(bool sideA, int x) const {
+    if (wide) return x - (sideA ? xmin_a : xmin_b);
+    return (sideA ? a_unsigned : b_unsigned) ? x : (int)(uint8_t)(int8_t)x;
+  }
 };
 
 // Builds (once, thread-safe) and returns the scheme; nullptr with a message on failure.
@@ -68,7 +94,11 @@ struct EncodeLaunch {
   uint8_t* planes;
   int64_t plane_stride;
   int32_t* flag;
-  const uint32_t* lut;  // 256 entries (host memory; passed by value to the kernel)
+  const uint32_t* lut;  // host memory: 256 entries (passed by value), or the wide table
+  bool wide;            // int16 inputs, table over [xmin, xmin + nvalues)
+  int32_t xmin, nvalues;
+  int side;             // which of the two device-resident wide tables to use
+  const void* table_key;  // identity of the wide table (its Scheme)
 };
 awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream);
 
@@ -80,6 +110,7 @@ struct GemmLaunch {
   int r;
   int32_t pa[kMaxProducts], pb[kMaxProducts];
   int32_t fold_ell[kMaxProducts];  // coefficient applied when the accumulator is folded after product k
+  int64_t outer;                   // the launch adds outer * (sum / D) into C
   uint32_t fold_mask;              // bit k: fold after product k
   int64_t k_seg;                   // fold segment length (multiple of kKPad)
   int64_t k_begin, k_end;          // reduction range of this launch (multiples of kKPad)

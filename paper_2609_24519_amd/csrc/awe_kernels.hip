@@ -4,11 +4,18 @@
 
 #include <algorithm>
 #include <cstdlib>
+#include <map>
+#include <mutex>
 #include <string>
 
 #include "awe_internal.h"
 
 namespace awe {
+
+// Code tables of a wide encoding (int16 inputs), one per side: too large for
+// kernel arguments, so they live in device memory of the module.
+__device__ uint32_t g_wide_lut[2][kWideValues];
+
 namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
@@ -72,6 +79,67 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
     for (int j = 0; j < 32; ++j) d[j >> 3] |= ((e[j] >> (4 * p)) & 0xfu) << (4 * (j & 7));
     *reinterpret_cast<uint4*>(dst + p * plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Encoder for a wide encoding (int16 inputs in [xmin, xmin + nvalues)): the
+// same brick production from a table of up to 4096 packed codes.  The table
+// is too large for kernel arguments; it lives in a device array (one per side,
+// uploaded once per device) and each workgroup stages it into LDS, then walks
+// several bricks per wave to spread that load.
+// ---------------------------------------------------------------------------
+template <bool kTransposed>
+__global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict__ x, int64_t rows,
+                                                       int64_t K, int64_t ld, int64_t KS, int64_t R32,
+                                                       int64_t nbricks, int nplanes,
+                                                       uint8_t* __restrict__ planes, int64_t plane_stride,
+                                                       int32_t* flag, int side, int32_t xmin,
+                                                       int32_t nvalues) {
+  __shared__ uint32_t slut[kWideValues];
+  for (int i = threadIdx.x; i < nvalues; i += blockDim.x) slut[i] = g_wide_lut[side][i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  auto look = [&](int v) -> uint32_t {
+    const uint32_t i = (uint32_t)(v - xmin);
+    return i < (uint32_t)nvalues ? slut[i] : kLutInvalid;
+  };
+  uint32_t bad = 0;
+  for (int64_t brick = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); brick < nbricks;
+       brick += (int64_t)gridDim.x * 4) {
+    const int64_t rb = brick / KS, ks = brick - rb * KS;
+    const int64_t row = rb * kBrickRows + (lane & 31);
+    const int64_t k0 = ks * kBrickK + (lane >> 5) * 32;
+    const bool row_ok = row < rows;
+    uint32_t e[32];
+    if (!kTransposed) {
+      const int16_t* src = x + row * ld + k0;
+      if (row_ok && k0 + 32 <= K && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint4 w = *reinterpret_cast<const uint4*>(src + 8 * q);
+          const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) e[8 * q + j] = look((int16_t)(ws[j >> 1] >> (16 * (j & 1))));
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? look(src[j]) : 0u;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? look(x[(k0 + j) * ld + row]) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < 32; ++j) bad |= e[j];
+    uint8_t* dst = planes + (ks * R32 + rb) * kBrickBytes + lane * 16;
+    for (int p = 0; p < nplanes; ++p) {
+      uint32_t d[4] = {0, 0, 0, 0};
+#pragma unroll
+      for (int j = 0; j < 32; ++j) d[j >> 3] |= ((e[j] >> (4 * p)) & 0xfu) << (4 * (j & 7));
+      *reinterpret_cast<uint4*>(dst + p * plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
+    }
+  }
+  if ((bad & kLutInvalid) && flag != nullptr) atomicOr(flag, 1);
 }
 
 // ---------------------------------------------------------------------------
@@ -142,6 +210,7 @@ struct GemmArgs {
   int32_t M, N;
   int32_t c64, accumulate, log2D, modulus;
   int32_t tiles_m, tiles_n;
+  int64_t outer;  // C (+)= outer * (sum / D)
 };
 
 // Position in the reduction stream: product p, k-tile t, current fold segment [cs, ce).
@@ -273,7 +342,8 @@ __device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& t
 }
 
 // One output of the epilogue: the int32 accumulator holds D*C (exact schemes,
-// modulo 2^32, the true value fits) or sum lambda_k P_k (residues).
+// modulo 2^32, the true value fits) or sum lambda_k P_k (residues); a launch
+// group of a wider scheme contributes outer * (its sum / D).
 __device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col, int32_t val) {
   if (row >= g.M || col >= g.N) return;
   const int64_t off = (int64_t)row * g.ldc + col;
@@ -285,13 +355,13 @@ __device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col
     if (g.accumulate) rr = (Cp[off] + rr) % m;
     Cp[off] = rr;
   } else {
-    val >>= g.log2D;
+    const int64_t t = (int64_t)(val >> g.log2D) * g.outer;
     if (g.c64) {
       int64_t* Cp = reinterpret_cast<int64_t*>(g.C);
-      Cp[off] = g.accumulate ? Cp[off] + (int64_t)val : (int64_t)val;
+      Cp[off] = g.accumulate ? Cp[off] + t : t;
     } else {
       int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
-      Cp[off] = g.accumulate ? (int32_t)((uint32_t)Cp[off] + (uint32_t)val) : val;
+      Cp[off] = g.accumulate ? (int32_t)((uint32_t)Cp[off] + (uint32_t)t) : (int32_t)t;
     }
   }
 }
@@ -474,12 +544,65 @@ awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
 
 }  // namespace
 
+// Uploads a wide encoding's code table into g_wide_lut on the current device,
+// once per device and side (the table never changes afterwards: one wide
+// encoding per side is supported).
+awe_status ensure_wide_table(const EncodeLaunch& e) {
+  static std::mutex mu;
+  static std::map<std::pair<int, int>, const void*> loaded;
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) {
+    set_error(std::string("wide table: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = loaded.find({dev, e.side});
+  if (it != loaded.end()) {
+    if (it->second == e.table_key) return AWE_OK;
+    set_error("only one wide encoding table per side is supported");
+    return AWE_ERR_UNSUPPORTED;
+  }
+  if (e.nvalues > kWideValues) {
+    set_error("wide encoding table too large");
+    return AWE_ERR_UNSUPPORTED;
+  }
+  err = hipMemcpyToSymbol(HIP_SYMBOL(g_wide_lut), e.lut, sizeof(uint32_t) * e.nvalues,
+                          sizeof(uint32_t) * kWideValues * e.side, hipMemcpyHostToDevice);
+  if (err != hipSuccess) {
+    set_error(std::string("wide table upload: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  loaded[{dev, e.side}] = e.table_key;
+  return AWE_OK;
+}
+
 awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
   const int64_t rb = (e.rows + kBrickRows - 1) / kBrickRows;
   const int64_t kp = (e.K + kKPad - 1) / kKPad * kKPad;
   const int64_t KS = kp / kBrickK;
   const int64_t nbricks = rb * KS;
   if (nbricks == 0) return AWE_OK;
+  if (e.wide) {
+    awe_status st = ensure_wide_table(e);
+    if (st != AWE_OK) return st;
+    const int64_t blocks = std::min<int64_t>((nbricks + 15) / 16, 4096);
+    const int16_t* x = reinterpret_cast<const int16_t*>(e.x);
+    if (e.transposed)
+      hipLaunchKernelGGL(encode16_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, x, e.rows,
+                         e.K, e.ld, KS, rb, nbricks, e.nplanes, e.planes, e.plane_stride, e.flag, e.side,
+                         e.xmin, e.nvalues);
+    else
+      hipLaunchKernelGGL(encode16_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, x, e.rows,
+                         e.K, e.ld, KS, rb, nbricks, e.nplanes, e.planes, e.plane_stride, e.flag, e.side,
+                         e.xmin, e.nvalues);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) {
+      set_error(std::string("encode launch: ") + hipGetErrorString(err));
+      return AWE_ERR_HIP;
+    }
+    return AWE_OK;
+  }
   LutArg lut;
   for (int i = 0; i < 256; ++i) lut.v[i] = e.lut[i];
   const int64_t blocks = (nbricks + 3) / 4;
@@ -539,6 +662,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.accumulate = L.accumulate;
   g.log2D = L.log2D;
   g.modulus = L.modulus;
+  g.outer = L.outer;
   switch (choose_cfg(L.M, L.N)) {
     case 0: return launch_tile<Cfg4w128x64>(g, L, stream);
     case 2: return launch_tile<Cfg8w64x96>(g, L, stream);

@@ -144,6 +144,49 @@ void define_ternary(Scheme& s) {
   s.xmin_b = -128; s.xmax_b = 127;
 }
 
+// FP16 x FP16 significands in 12 products (App. A): w = v = (1, 9, 71, 639),
+// planes a_0..a_3, a_0 + 2 a_1, a_2 + 2 a_3; for the outer pair (k, l) the
+// products P_{2k,2l}, P_{2k+1,2l+1}, Q_kl with coefficients 71^(k+l) (-7, 126, 9),
+// D = 2.  Each (k, l) is a launch group (outer weight 71^(k+l)): its inner sum
+// is 2 (a_{2k} + 9 a_{2k+1})(b_{2l} + 9 b_{2l+1}), which fits the int32 fold.
+void define_fp16(Scheme& s) {
+  s.p = s.q = 4;
+  const int32_t w[4] = {1, 9, 71, 639};
+  for (int i = 0; i < 4; ++i) s.w[i] = s.v[i] = w[i];
+  // stored planes in order of first use: a_0, a_1, a_0 + 2 a_1, a_2, a_3, a_2 + 2 a_3
+  s.na = s.nb = 6;
+  for (auto* pl : {&s.alpha, &s.beta}) {
+    set_plane(*pl, 0, {1, 0, 0, 0});
+    set_plane(*pl, 1, {0, 1, 0, 0});
+    set_plane(*pl, 2, {1, 2, 0, 0});
+    set_plane(*pl, 3, {0, 0, 1, 0});
+    set_plane(*pl, 4, {0, 0, 0, 1});
+    set_plane(*pl, 5, {0, 0, 1, 2});
+  }
+  const int64_t inner[3] = {-7, 126, 9};
+  s.r = 0;
+  s.n_lgroups = 4;
+  for (int k = 0; k < 2; ++k)
+    for (int l = 0; l < 2; ++l) {
+      const int g = 2 * k + l;
+      const int64_t outer = (k + l == 0) ? 1 : (k + l == 1 ? 71 : 71 * 71);
+      s.louter[g] = outer;
+      const int pa[3] = {3 * k, 3 * k + 1, 3 * k + 2}, pb[3] = {3 * l, 3 * l + 1, 3 * l + 2};
+      for (int t = 0; t < 3; ++t) {
+        s.pa[s.r] = pa[t];
+        s.pb[s.r] = pb[t];
+        s.ell[s.r] = inner[t] * outer;
+        s.lgroup[s.r] = g;
+        ++s.r;
+      }
+    }
+  s.log2D = 1;
+  s.cap_a = s.cap_b = 12;
+  s.xmin_a = s.xmin_b = -2048;
+  s.xmax_a = s.xmax_b = 2047;
+  s.wide = true;
+}
+
 // ---- limb tuples ----------------------------------------------------------
 struct Tuple {
   int a[kMaxLimbs];
@@ -212,7 +255,8 @@ void base13_digits(int x, int* out) {
   if (x != 0) out[0] = INT_MAX;  // not representable in 3 limbs (never for int8)
 }
 
-// Builds the limb table of one side: for every input byte, the chosen limbs.
+// Builds the limb table of one side: for every table index (input byte, or
+// x - xmin for a wide encoding), the chosen limbs, plane values and codes.
 // Returns false with a message if an input of the range has no tuple.
 bool build_side(Scheme& s, bool sideA, std::string* msg) {
   const int p = sideA ? s.p : s.q;
@@ -222,24 +266,28 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
   const int cap = sideA ? s.cap_a : s.cap_b;
   const int xmin = sideA ? s.xmin_a : s.xmin_b;
   const int xmax = sideA ? s.xmax_a : s.xmax_b;
-  const bool uns = sideA ? s.a_unsigned : s.b_unsigned;
-  int32_t(*val)[kMaxPlanes] = sideA ? s.val_a : s.val_b;
-  uint32_t* lut = sideA ? s.lut_a : s.lut_b;
+  auto& val = sideA ? s.val_a : s.val_b;
+  auto& lut = sideA ? s.lut_a : s.lut_b;
   const int nx = xmax - xmin + 1;
+  const int nt = s.table_size(sideA);
+  val.assign(nt, std::array<int32_t, kMaxPlanes>{});
+  lut.assign(nt, kLutInvalid);
 
   std::vector<Tuple> best(nx);
   std::vector<char> have(nx, 0);
-  std::vector<char> hit(4096, 0);  // values of w.a seen (exact schemes; for the coverage)
   if (s.modulus == 0) {
     // values of w.a over the admissible tuples, for the coverage (Sec. 4.2)
+    int64_t span = 0;
+    for (int i = 0; i < p; ++i) span += 12 * (int64_t)std::abs(wts[i]);
+    std::vector<char> hit(2 * span + 1, 0);
     for_admissible(p, planes, np, cap, [&](const int* a) {
       int64_t x = 0;
       for (int i = 0; i < p; ++i) x += (int64_t)wts[i] * a[i];
-      if (x >= -2047 && x <= 2048) hit[x + 2047] = 1;
+      hit[x + span] = 1;
     });
-    int X = 0;
-    while (X < 2047 && hit[X + 1 + 2047] && hit[-(X + 1) + 2047]) ++X;
-    (sideA ? s.coverage_a : s.coverage_b) = X;
+    int64_t X = 0;
+    while (X < span && hit[X + 1 + span] && hit[-(X + 1) + span]) ++X;
+    (sideA ? s.coverage_a : s.coverage_b) = (int32_t)X;
   }
   if (sideA ? s.positional13_a : s.positional13_b) {
     for (int x = xmin; x <= xmax; ++x) {
@@ -271,13 +319,9 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
     }
 
   int cmax = 0;
-  for (int b = 0; b < 256; ++b) {
-    int x = uns ? b : (int)(int8_t)(uint8_t)b;
-    for (int k = 0; k < kMaxPlanes; ++k) val[b][k] = 0;
-    if (x < xmin || x > xmax) {
-      lut[b] = kLutInvalid;
-      continue;
-    }
+  for (int b = 0; b < nt; ++b) {
+    const int x = s.table_value(sideA, b);
+    if (x < xmin || x > xmax) continue;  // stays kLutInvalid
     const int* a = best[x - xmin].a;
     uint32_t packed = 0;
     for (int k = 0; k < np; ++k) {
@@ -312,12 +356,13 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
 
 // Definition 4.1 identity (or its congruence) on every pair of table inputs.
 bool check_identity(const Scheme& s, std::string* msg) {
-  for (int ba = 0; ba < 256; ++ba) {
+  const int na = s.table_size(true), nb = s.table_size(false);
+  for (int ba = 0; ba < na; ++ba) {
     if (s.lut_a[ba] & kLutInvalid) continue;
-    int x = s.a_unsigned ? ba : (int)(int8_t)(uint8_t)ba;
-    for (int bb = 0; bb < 256; ++bb) {
+    const int x = s.table_value(true, ba);
+    for (int bb = 0; bb < nb; ++bb) {
       if (s.lut_b[bb] & kLutInvalid) continue;
-      int y = s.b_unsigned ? bb : (int)(int8_t)(uint8_t)bb;
+      const int y = s.table_value(false, bb);
       int64_t acc = 0;
       for (int k = 0; k < s.r; ++k) acc += s.ell[k] * s.val_a[ba][s.pa[k]] * s.val_b[bb][s.pb[k]];
       bool ok = s.modulus ? pmod(acc - (int64_t)x * y, s.modulus) == 0
@@ -351,9 +396,41 @@ void derive_bounds(Scheme& s) {
   s.k_seg = seg / kKPad * kKPad;
 }
 
+// Every launch group must reconstruct D times an integer on its own (its
+// coefficient matrix sum_k (ell_k / outer) alpha_k beta_k^T divisible by D), so
+// that the shift by log2 D can be applied per launch; its inner coefficients
+// must fit the kernel's signed 24-bit fold multiply.
+bool check_launch_groups(const Scheme& s, std::string* msg) {
+  for (int g = 0; g < s.n_lgroups; ++g) {
+    int64_t cm[kMaxLimbs][kMaxLimbs] = {};
+    for (int k = 0; k < s.r; ++k) {
+      if (s.lgroup[k] != g) continue;
+      if (s.louter[g] == 0 || s.ell[k] % s.louter[g] != 0) {
+        *msg = "coefficient not a multiple of its launch group's outer weight";
+        return false;
+      }
+      const int64_t inner = s.ell[k] / s.louter[g];
+      if (inner < -(1 << 23) || inner >= (1 << 23)) {
+        *msg = "inner coefficient outside the 24-bit fold multiply";
+        return false;
+      }
+      for (int i = 0; i < s.p; ++i)
+        for (int j = 0; j < s.q; ++j) cm[i][j] += inner * s.alpha[s.pa[k]][i] * s.beta[s.pb[k]][j];
+    }
+    for (int i = 0; i < s.p; ++i)
+      for (int j = 0; j < s.q; ++j)
+        if (cm[i][j] % (int64_t(1) << s.log2D) != 0) {
+          *msg = "launch group does not reconstruct a multiple of D";
+          return false;
+        }
+  }
+  return true;
+}
+
 bool finish(Scheme& s, std::string* msg) {
   if (!build_side(s, true, msg) || !build_side(s, false, msg)) return false;
   if (!check_identity(s, msg)) return false;
+  if (!check_launch_groups(s, msg)) return false;
   derive_bounds(s);
   if (s.k_seg < kKPad) {
     *msg = "fold segment below one k-tile";
@@ -486,7 +563,7 @@ int64_t plane_stride_bytes(int64_t rows, int64_t K) {
 }
 
 const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std::string* msg) {
-  if (enc < AWE_ENC_B13 || enc > AWE_ENC_TERNARY) {
+  if (enc < AWE_ENC_B13 || enc > AWE_ENC_FP16) {
     *st = AWE_ERR_INVALID_VALUE;
     *msg = "unknown encoding";
     return nullptr;
@@ -518,6 +595,7 @@ const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std:
     case AWE_ENC_AWE6ALT: define_awe6(*s, true); break;
     case AWE_ENC_AWE4: define_awe4(*s); break;
     case AWE_ENC_TERNARY: define_ternary(*s); break;
+    case AWE_ENC_FP16: define_fp16(*s); break;
     case AWE_ENC_MOD:
       ok = define_mod(*s, modulus, &m);
       if (!ok) fail = AWE_ERR_UNSUPPORTED;

@@ -16,7 +16,7 @@ from oracle import modm, schemes as sc
 from paper_2609_24519_amd import awe
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
-         "ternary": awe.ENC_TERNARY}
+         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16}
 
 
 @lru_cache(maxsize=None)

@@ -11,7 +11,11 @@ from tests.gpu_helpers import decode_planes, to_dev
 pytestmark = pytest.mark.gpu
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
-         "ternary": awe.ENC_TERNARY}
+         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16}
+
+
+def _dtype(lo, hi):
+    return np.int8 if -128 <= lo and hi <= 127 else np.int16
 
 
 def _encode(enc, m, side, X, rows, K, flag=None):
@@ -31,10 +35,10 @@ def _encode(enc, m, side, X, rows, K, flag=None):
 def test_encode_matches_oracle(name, rows, K):
     s = sc.PAPER_SCHEMES[name]()
     rng = np.random.default_rng(rows * 1000 + K)
-    A = inputs.uniform(rng, (rows, K), *s.range_a)
+    A = inputs.uniform(rng, (rows, K), *s.range_a, dtype=_dtype(*s.range_a))
     got = _encode(EXACT[name], 0, awe.SIDE_A, A, rows, K)
     assert np.array_equal(got, sc.encode_planes(s, "a", A))
-    B = inputs.uniform(rng, (K, rows), *s.range_b)  # K x N, N = rows
+    B = inputs.uniform(rng, (K, rows), *s.range_b, dtype=_dtype(*s.range_b))  # K x N, N = rows
     got = _encode(EXACT[name], 0, awe.SIDE_B, B, rows, K)
     assert np.array_equal(got, np.swapaxes(sc.encode_planes(s, "b", B), 1, 2))
 
@@ -65,3 +69,16 @@ def test_range_flag():
     R[0, 0] = 13
     _encode(awe.ENC_MOD, 13, awe.SIDE_B, R, 40, 40, flag)
     assert flag.item() != 0
+
+
+def test_encode_wide_range_flag():
+    # int16 inputs of the FP16 scheme: values outside [-2048, 2047] raise the flag
+    A = np.zeros((32, 64), dtype=np.int16)
+    A[3, 5] = 2047
+    A[7, 9] = -2048
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    _encode(awe.ENC_FP16, 0, awe.SIDE_A, A, 32, 64, flag)
+    assert int(flag.item()) == 0
+    A[8, 8] = 2048
+    _encode(awe.ENC_FP16, 0, awe.SIDE_A, A, 32, 64, flag)
+    assert int(flag.item()) != 0

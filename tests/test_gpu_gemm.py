@@ -191,3 +191,20 @@ def test_ternary_4096_sampled():
     for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=2):
         ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
         assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)
+
+
+
+@pytest.mark.parametrize("shape,out", [((70, 45, 500), torch.int32), ((130, 260, 2000), torch.int64),
+                                       ((33, 40, 16384), torch.int64), ((16, 24, 120_000), torch.int64)])
+def test_fp16_12_products(shape, out):
+    # App. A: 12-bit integers (FP16 significands) in 12 FP4 products, run as four launch
+    # groups with outer weights 71^(k+l); the last shape needs several reduction launches
+    M, N, K = shape
+    rng = np.random.default_rng(M + N + K)
+    A = inputs.uniform(rng, (M, K), -2048, 2047, np.int16)
+    B = inputs.uniform(rng, (K, N), -2048, 2047, np.int16)
+    A[0, :] = -2048
+    B[:, 0] = -2048
+    C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_FP16, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy().astype(np.int64), og.gemm_i64_wide(A, B))

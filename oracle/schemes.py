@@ -73,6 +73,11 @@ class Scheme:
         self.n_g = n_g
         # sides whose limbs are base-13 positional digits instead of the choice rule
         self.positional = ()
+        # side -> (x -> limb tuple) for encodings whose limbs a rule fixes outright
+        self.limb_rule = {}
+        # element format of every stored plane ("e2m1" unless stated)
+        self.formats_a = None
+        self.formats_b = None
         # distinct stored planes per side, in order of first use
         self.planes_a = []
         self.planes_b = []
@@ -200,8 +205,56 @@ def fp16_12():
     return Scheme("fp16_12", w, w, prods, 2, 12, 12, (-2048, 2047), (-2048, 2047))
 
 
+# ---------------------------------------------------------------------------
+# E4M3 (OCP FP8): sign, 4 exponent bits (bias 7), 3 mantissa bits; no infinities,
+# S.1111.111 is NaN.  Small integers (|v| <= 16) are exact.
+# ---------------------------------------------------------------------------
+def e4m3_value(code):
+    sign = -1.0 if code & 0x80 else 1.0
+    e = (code >> 3) & 15
+    m = code & 7
+    if e == 15 and m == 7:
+        return float("nan")
+    if e == 0:
+        return sign * (m / 8.0) * 2.0 ** (1 - 7)
+    return sign * (1.0 + m / 8.0) * 2.0 ** (e - 7)
+
+
+def e4m3_code(v):
+    """Code of an exactly representable value (searched over all codes)."""
+    for c in range(256):
+        if e4m3_value(c) == v and not (v == 0 and c & 0x80):
+            return c
+    raise ValueError("%r is not an E4M3 value" % (v,))
+
+
+FP8FP4_EPS = (0, 1, -1, 2, -2, 3, -3, 4, -4, 6, -6, 8, -8)
+
+
+def fp8fp4_limbs(x):
+    """App. A: x = 13 h + 5 eps with eps in FP8FP4_EPS; eps is fixed by x mod 13, since
+    5 eps = x (mod 13) and the set holds every residue class mod 13 exactly once."""
+    eps = next(e for e in FP8FP4_EPS if (5 * e - x) % 13 == 0)
+    return ((x - 5 * eps) // 13, eps)
+
+
+def fp8fp4():
+    """INT8 x INT8 with 2 FP8 products and 1 FP4 product, App. A.
+
+    A = 13 h + 5 eps, B = 13 h' + 5 eps'; P1 = h h' and P2 = (h + eps)(h' + eps') with the
+    planes h, h + eps stored in FP8 (E4M3), P3 = eps eps' in FP4; AB = 104 P1 + 65 P2 - 40 P3,
+    D = 1.  Plane values stay within 14 (c_A = c_B = 14).
+    """
+    planes = [(1, 0), (1, 1), (0, 1)]
+    prods = [(pl, pl, l) for pl, l in zip(planes, (104, 65, -40))]
+    s = Scheme("fp8fp4", (13, 5), (13, 5), prods, 1, 14, 14, INT8_RANGE, INT8_RANGE)
+    s.limb_rule = {"a": fp8fp4_limbs, "b": fp8fp4_limbs}
+    s.formats_a = s.formats_b = ["e4m3", "e4m3", "e2m1"]
+    return s
+
+
 PAPER_SCHEMES = {"b13": b13, "awe6": awe6, "awe6_alt": awe6_alt, "awe4": awe4, "ternary": ternary,
-                 "fp16_12": fp16_12}
+                 "fp16_12": fp16_12, "fp8fp4": fp8fp4}
 
 
 # ---------------------------------------------------------------------------
@@ -345,6 +398,8 @@ def k_star(n_g, c_a, c_b, F=24):
 def limb_table(s, side):
     """x -> limb tuple for every x in the side's input range."""
     lo, hi = s.range_a if side == "a" else s.range_b
+    if side in s.limb_rule:
+        return {x: s.limb_rule[side](x) for x in range(lo, hi + 1)}
     if side in s.positional:
         return {x: b13_digits(x) for x in range(lo, hi + 1)}
     w = s.w if side == "a" else s.v

@@ -220,3 +220,33 @@ def test_fp16_12_all_input_pairs():
     assert sc.brute_force_pairs(s)
     limbs = sc.limb_table(s, "a")
     assert all(sc.dot(s.w, limbs[x]) == x for x in range(-2048, 2048))
+
+
+def test_e4m3_format_facts(paper):
+    # OCP FP8 E4M3: 1.0, the largest normal 448, the smallest normal 2^-6 and subnormal 2^-9
+    one, big, nmin, smin = paper["e4m3.codes"]
+    assert sc.e4m3_value(one) == 1.0 and sc.e4m3_value(big) == 448.0
+    assert sc.e4m3_value(nmin) == 2.0 ** -6 and sc.e4m3_value(smin) == 2.0 ** -9
+    assert all(sc.e4m3_value(sc.e4m3_code(v)) == v for v in range(-16, 17))
+
+
+def test_fp8fp4_scheme(paper):
+    s = sc.fp8fp4()
+    assert s.w == tuple(paper["fp8fp4.w"]) and [l for _, _, l in s.products] == paper["fp8fp4.ell"]
+    assert sorted(sc.FP8FP4_EPS) == sorted(paper["fp8fp4.eps"])
+    assert sorted(e % 13 for e in sc.FP8FP4_EPS) == list(range(13))  # one per residue class
+    assert all(e in sc.S_SET for e in sc.FP8FP4_EPS)                  # the FP4 limb is storable
+    assert sc.coefficient_identity_holds(s)
+    assert sc.brute_force_pairs(s)                                     # all 65,536 int8 pairs
+    limbs = sc.limb_table(s, "a")
+    assert all(13 * h + 5 * e == x for x, (h, e) in limbs.items())
+    caps = (sc.stored_cap(s, "a"), sc.stored_cap(s, "b"))
+    assert caps == tuple(paper["fp8fp4.cap"])
+    assert sc.k_star(1, *caps) == paper["kstar.fp8fp4"][0]
+    # the FP8 planes hold exact E4M3 integers
+    _, T = sc.plane_table(s, "a")
+    assert all(sc.e4m3_value(sc.e4m3_code(int(v))) == v for v in np.unique(T[:, :2]))
+    rng = np.random.default_rng(9)
+    A = rng.integers(-128, 127, (9, 70), endpoint=True)
+    B = rng.integers(-128, 127, (70, 6), endpoint=True)
+    assert np.array_equal(sc.scheme_gemm(s, A, B), A @ B)

@@ -8,8 +8,9 @@ encode A, encode B, the r FP4 products with their fused reconstruction
 The workload is M = N = K = 8192 with int8 entries uniform in [-128, 127]
 (seed 0) and int32 C.  Printed: one JSON line with the end-to-end exact TOPS
 as ``value``, the roofline of the dominant kernel (the GEMM) from HIP events
-on its stream, the 9-product base-13 baseline, the 3-product {0,+-1} x INT8
-GEMM, the 12-product FP16-significand GEMM, the native INT8 MFMA GEMM
+on its stream, the 9-product base-13 baseline, the 2 FP8 + 1 FP4 scheme, the
+3-product {0,+-1} x INT8 GEMM, the 12-product FP16-significand GEMM, the
+native INT8 MFMA GEMM
 (hipBLASLt through torch._int_mm), the residue-number-system route for 53-bit
 integers (the integer layer of Ozaki scheme II) and the sustained rate of the
 FP4 MFMA alone timed in the same run as context, and the oracle timed on the host's cores on
@@ -151,6 +152,14 @@ def main():
         except Exception as ex:  # noqa: BLE001 - context only
             line["int8_mfma_context"] = {"error": str(ex)[:200]}
     if not args.no_context:
+        # INT8 x INT8 with 2 E4M3 products and 1 E2M1 product (App. A) on the same A and B;
+        # an E4M3 MFMA runs at half the E2M1 rate, so the work is 5 FP4-product equivalents
+        finfo, fwall, fenc_ms, fgemm_ms = run(awe.ENC_FP8FP4, max(3, args.steps // 2), 2)
+        line["fp8fp4_2_fp8_1_fp4"] = {
+            "ms_per_step": round(fwall / max(3, args.steps // 2) * 1e3, 4),
+            "gemm_ms": round(fgemm_ms, 4),
+            "gemm_exact_TOPS": round(ops / (fgemm_ms * 1e-3) / 1e12, 2),
+            "fp4_equiv_peak_frac": round(5 * ops / (fgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
         # {0, +-1} x INT8 (Sec. 6.2) on the same B: 3 products
         At = torch.from_numpy(inputs.int8_pair(M, 8, K, seed=5, a_range=(-1, 1))[0]).to(dev)
         tinfo, pta, ptb = setup(awe.ENC_TERNARY)

@@ -43,6 +43,11 @@
  * the stored value s/2 (s in S): bit 3 the sign, bits 2..0 the magnitude
  * index of |s| in (0, 1, 2, 3, 4, 6, 8, 12).  Padding rows and reduction
  * indices hold code 0 (value 0), so they add nothing to any product.
+ * E4M3 planes (the first two planes of AWE_ENC_FP8FP4) use 2048-byte bricks with
+ * the same geometry: brick (rb, ks) at byte (ks * ceil(rows/32) + rb) * 2048, lane L
+ * owning bytes L*32 .. L*32+31, byte j the OCP E4M3 code of element j (the integer
+ * itself: every stored value has |v| <= 14).  An E4M3 plane takes two strides, and a
+ * side stores its E4M3 planes before its E2M1 planes.
  */
 #ifndef AWE_H
 #define AWE_H
@@ -77,10 +82,13 @@ typedef enum awe_encoding {
   AWE_ENC_MOD = 5,     /* residues modulo m (Sec. 5.3); needs the modulus argument */
   AWE_ENC_TERNARY = 6, /* {0, +-1} x INT8 in 3 products: the ternary A entry is one limb, B takes
                           the base-13 limbs, C = sum_j 13^j P_j (Sec. 6.2).  A is int8 in [-1, 1]. */
-  AWE_ENC_FP16 = 7     /* FP16-significand integers x FP16-significand integers in 12 products,
+  AWE_ENC_FP16 = 7,    /* FP16-significand integers x FP16-significand integers in 12 products,
                           w = v = (1, 9, 71, 639), D = 2 (App. A).  Both operands are int16 in
                           [-2048, 2047]; the products run as four launches, one per outer weight
                           71^(k+l), each adding its share into C. */
+  AWE_ENC_FP8FP4 = 8   /* INT8 x INT8 with 2 FP8 (E4M3) products and 1 FP4 product (App. A):
+                          A = 13 h + 5 eps, planes h, h + eps (E4M3, 2 KiB bricks, see the
+                          layout above) and eps (E2M1); AB = 104 P1 + 65 P2 - 40 P3. */
 } awe_encoding;
 
 typedef enum awe_side { AWE_SIDE_A = 0, AWE_SIDE_B = 1 } awe_side;
@@ -113,6 +121,8 @@ typedef struct awe_encoding_info {
   int32_t group[AWE_MAX_PRODUCTS];/* accumulator shared by product k (equal ell_k) */
   int64_t k_star;                 /* floor(2^24 / (n_g c_a c_b)), Sec. 3.4 */
   int64_t k_seg;                  /* default fold segment of the GEMM (<= k_star), multiple of AWE_K_PAD */
+  int32_t format_a[AWE_MAX_PLANES];  /* element format of stored A plane k: 0 E2M1, 1 E4M3 */
+  int32_t format_b[AWE_MAX_PLANES];
 } awe_encoding_info;
 
 /* Host.  The configuration record of an encoding (for AWE_ENC_MOD, of modulus m; the

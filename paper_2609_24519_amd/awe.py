@@ -19,9 +19,9 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "awe.h")
 # awe_status
 OK, ERR_INVALID_VALUE, ERR_UNSUPPORTED, ERR_OVERFLOW, ERR_WORKSPACE, ERR_HIP, ERR_TABLE = range(7)
 # awe_encoding
-ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY, ENC_FP16 = 1, 2, 3, 4, 5, 6, 7
+ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY, ENC_FP16, ENC_FP8FP4 = 1, 2, 3, 4, 5, 6, 7, 8
 ENCODINGS = {"b13": ENC_B13, "awe6": ENC_AWE6, "awe6_alt": ENC_AWE6ALT, "awe4": ENC_AWE4, "mod": ENC_MOD,
-             "ternary": ENC_TERNARY, "fp16_12": ENC_FP16}
+             "ternary": ENC_TERNARY, "fp16_12": ENC_FP16, "fp8fp4": ENC_FP8FP4}
 # awe_side, awe_dtype
 SIDE_A, SIDE_B = 0, 1
 I32, I64 = 0, 1
@@ -49,6 +49,7 @@ class EncodingInfo(ctypes.Structure):
         ("ell", ctypes.c_int64 * MAX_PRODUCTS),
         ("group", ctypes.c_int32 * MAX_PRODUCTS),
         ("k_star", ctypes.c_int64), ("k_seg", ctypes.c_int64),
+        ("format_a", ctypes.c_int32 * MAX_PLANES), ("format_b", ctypes.c_int32 * MAX_PLANES),
     ]
 
 
@@ -151,6 +152,8 @@ def get_encoding_info(enc, modulus=0):
         "pair_a": list(info.pair_a[:r]), "pair_b": list(info.pair_b[:r]),
         "ell": list(info.ell[:r]), "group": list(info.group[:r]),
         "k_star": info.k_star, "k_seg": info.k_seg,
+        "formats_a": ["e4m3" if f else "e2m1" for f in info.format_a[:info.planes_a]],
+        "formats_b": ["e4m3" if f else "e2m1" for f in info.format_b[:info.planes_b]],
     }
 
 

@@ -33,7 +33,7 @@ const Scheme* scheme_or_fail(awe_encoding enc, int32_t modulus, awe_status* st) 
 }
 
 size_t side_bytes(const Scheme& s, bool sideA, int64_t rows, int64_t K) {
-  return (size_t)(sideA ? s.na : s.nb) * (size_t)plane_stride_bytes(rows, K);
+  return (size_t)s.plane_units(sideA, sideA ? s.na : s.nb) * (size_t)plane_stride_bytes(rows, K);
 }
 
 // Largest reduction length (multiple of kKPad) one GEMM launch may cover so that
@@ -76,17 +76,19 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
   if (!s.modulus && c_type == AWE_I32 &&
       max_abs_input(s, true) * max_abs_input(s, false) * K > 0x7fffffffLL)
     return fail(AWE_ERR_OVERFLOW, "int32 C cannot hold max|A| max|B| K");
-  if (k_seg == 0) k_seg = s.k_seg;
+  const bool own_seg = k_seg == 0;  // each launch group folds at its own bound
+  if (own_seg) k_seg = s.k_seg;
   if (k_seg < 0 || k_seg % kKPad != 0 || k_seg > s.k_seg)
     return fail(AWE_ERR_INVALID_VALUE,
                 "k_seg must be a positive multiple of " + std::to_string(kKPad) +
                     " no larger than " + std::to_string(s.k_seg));
 
   GemmLaunch L{};
+  const int64_t unit_a = plane_stride_bytes(M, K), unit_b = plane_stride_bytes(N, K);
   L.planes_a = reinterpret_cast<const uint8_t*>(pa);
   L.planes_b = reinterpret_cast<const uint8_t*>(pb);
-  L.stride_a = plane_stride_bytes(M, K);
-  L.stride_b = plane_stride_bytes(N, K);
+  L.stride_a = unit_a;
+  L.stride_b = unit_b;
   L.M = M;
   L.N = N;
   L.K = K;
@@ -106,12 +108,20 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
   // one launch per (reduction range, launch group); every launch after the first adds into C
   for (int64_t k0 = 0; k0 < kp; k0 += step) {
     for (int g = 0; g < s.n_lgroups; ++g) {
+      // the group's planes share one format; address them from the first plane of it
+      L.fp8 = s.lfmt[g] == kFmtE4M3;
+      const int first_a = L.fp8 ? 0 : s.planes8(true), first_b = L.fp8 ? 0 : s.planes8(false);
+      L.planes_a = reinterpret_cast<const uint8_t*>(pa) + s.plane_units(true, first_a) * unit_a;
+      L.planes_b = reinterpret_cast<const uint8_t*>(pb) + s.plane_units(false, first_b) * unit_b;
+      L.stride_a = (L.fp8 ? 2 : 1) * unit_a;
+      L.stride_b = (L.fp8 ? 2 : 1) * unit_b;
+      L.k_seg = own_seg ? s.lkseg[g] : k_seg;
       L.r = 0;
       L.fold_mask = 0;
       for (int k = 0; k < s.r; ++k) {
         if (s.lgroup[k] != g) continue;
-        L.pa[L.r] = s.pa[k];
-        L.pb[L.r] = s.pb[k];
+        L.pa[L.r] = s.pa[k] - first_a;
+        L.pb[L.r] = s.pb[k] - first_b;
         L.fold_ell[L.r] = (int32_t)(s.ell[k] / s.louter[g]);
         const bool last = k == s.r - 1 || s.group[k + 1] != s.group[k] || s.lgroup[k + 1] != g;
         if (last) L.fold_mask |= 1u << L.r;
@@ -147,6 +157,7 @@ awe_status encode_impl(const Scheme& s, awe_side side, const void* x, int64_t ro
   e.transposed = !sideA;
   e.is_unsigned = sideA ? s.a_unsigned : s.b_unsigned;
   e.nplanes = sideA ? s.na : s.nb;
+  e.nplanes8 = s.planes8(sideA);
   e.planes = reinterpret_cast<uint8_t*>(planes);
   e.plane_stride = plane_stride_bytes(rows, K);
   e.flag = flag;
@@ -328,6 +339,10 @@ awe_status awe_get_encoding_info(awe_encoding enc, int32_t modulus, awe_encoding
   }
   info.k_star = s->k_star;
   info.k_seg = s->k_seg;
+  for (int k = 0; k < AWE_MAX_PLANES; ++k) {
+    info.format_a[k] = s->fmt_a[k];
+    info.format_b[k] = s->fmt_b[k];
+  }
   *out = info;
   return AWE_OK;
 }

@@ -25,6 +25,10 @@ constexpr uint32_t kLutInvalid = 0x80000000u;
 // Inputs of a wide encoding are int16 in [xmin, xmax], at most this many values.
 constexpr int kWideValues = 4096;
 
+// Plane element formats and limb rules.
+constexpr uint8_t kFmtE2M1 = 0, kFmtE4M3 = 1;
+constexpr int kRuleChoice = 0, kRuleBase13 = 1, kRuleFp8Fp4 = 2;
+
 // One scheme (Definition 4.1 of the paper, or its mod-m congruence form)
 // together with the encoding tables derived from it.
 struct Scheme {
@@ -45,12 +49,28 @@ struct Scheme {
   int n_lgroups = 1;
   int32_t lgroup[kMaxProducts] = {};
   int64_t louter[kMaxProducts] = {1};
+  uint8_t lfmt[kMaxProducts] = {};    // element format of group g's operands (kFmt*)
+  int64_t lkseg[kMaxProducts] = {};   // fold segment of group g (from its own plane bounds)
+  // Element format of every stored plane; planes of one side are stored in this
+  // order, E4M3 planes (twice the bytes) before E2M1 planes.
+  uint8_t fmt_a[kMaxPlanes] = {}, fmt_b[kMaxPlanes] = {};
+  int limb_rule = 0;                  // kRule*: how an input's limbs are chosen
   int log2D = 0;
   int cap_a = 12, cap_b = 12;        // bound on |stored value| the tables may use
   int32_t xmin_a = 0, xmax_a = 0, xmin_b = 0, xmax_b = 0;
   bool positional13_a = false, positional13_b = false;  // base-13 digits with carries instead of the choice rule
   bool a_unsigned = false, b_unsigned = false;  // residues arrive as uint8
   bool wide = false;  // int16 inputs; tables indexed by x - xmin instead of the input byte
+  int planes8(bool sideA) const {  // leading E4M3 planes
+    int n = 0;
+    while (n < (sideA ? na : nb) && (sideA ? fmt_a : fmt_b)[n]) ++n;
+    return n;
+  }
+  // Plane k's offset in units of one E2M1 plane (an E4M3 plane counts 2).
+  int plane_units(bool sideA, int k) const {
+    const int n8 = planes8(sideA);
+    return k <= n8 ? 2 * k : 2 * n8 + (k - n8);
+  }
 
   // derived by build_tables()
   int c_a = 0, c_b = 0, n_g = 1;
@@ -81,6 +101,9 @@ const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std:
 // E2M1 code of a doubled integer in S (sign bit 3, magnitude code 0..7), or -1.
 int e2m1_code(int s);
 
+// E4M3 code of an integer with |v| <= 16, or -1.
+int e4m3_code(int v);
+
 // Bytes of one plane of `rows` x `K`.
 int64_t plane_stride_bytes(int64_t rows, int64_t K);
 
@@ -91,6 +114,7 @@ struct EncodeLaunch {
   bool transposed;  // B side: x[k * ld + row]
   bool is_unsigned;
   int nplanes;
+  int nplanes8;         // the first nplanes8 planes are E4M3 (8-bit codes), the rest E2M1
   uint8_t* planes;
   int64_t plane_stride;
   int32_t* flag;
@@ -111,6 +135,7 @@ struct GemmLaunch {
   int32_t pa[kMaxProducts], pb[kMaxProducts];
   int32_t fold_ell[kMaxProducts];  // coefficient applied when the accumulator is folded after product k
   int64_t outer;                   // the launch adds outer * (sum / D) into C
+  bool fp8;                        // operands are E4M3 planes (else E2M1)
   uint32_t fold_mask;              // bit k: fold after product k
   int64_t k_seg;                   // fold segment length (multiple of kKPad)
   int64_t k_begin, k_end;          // reduction range of this launch (multiples of kKPad)

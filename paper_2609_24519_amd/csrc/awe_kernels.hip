@@ -36,7 +36,7 @@ template <bool kTransposed>
 __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__ x, int64_t rows,
                                                      int64_t K, int64_t ld, int64_t KS,
                                                      int64_t R32, int64_t nbricks, int nplanes,
-                                                     uint8_t* __restrict__ planes,
+                                                     int nplanes8, uint8_t* __restrict__ planes,
                                                      int64_t plane_stride, int32_t* flag,
                                                      LutArg lut) {
   __shared__ uint32_t slut[256];
@@ -72,11 +72,22 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
   for (int j = 0; j < 32; ++j) bad |= e[j];
   if ((bad & kLutInvalid) && flag != nullptr) atomicOr(flag, 1);
 
-  uint8_t* dst = planes + (ks * R32 + rb) * kBrickBytes + lane * 16;
-  for (int p = 0; p < nplanes; ++p) {
+  // E4M3 planes (2 KiB bricks, 32 bytes per lane) first, then the E2M1 planes; an E4M3
+  // plane occupies two plane strides.
+  for (int p = 0; p < nplanes8; ++p) {
+    uint32_t d[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 32; ++j) d[j >> 2] |= ((e[j] >> (8 * p)) & 0xffu) << (8 * (j & 3));
+    uint8_t* dst8 = planes + 2 * p * plane_stride + (ks * R32 + rb) * (2 * kBrickBytes) + lane * 32;
+    *reinterpret_cast<uint4*>(dst8) = make_uint4(d[0], d[1], d[2], d[3]);
+    *reinterpret_cast<uint4*>(dst8 + 16) = make_uint4(d[4], d[5], d[6], d[7]);
+  }
+  uint8_t* dst = planes + 2 * nplanes8 * plane_stride + (ks * R32 + rb) * kBrickBytes + lane * 16;
+  for (int p = 0; p < nplanes - nplanes8; ++p) {
+    const int sh = 8 * nplanes8 + 4 * p;
     uint32_t d[4] = {0, 0, 0, 0};
 #pragma unroll
-    for (int j = 0; j < 32; ++j) d[j >> 3] |= ((e[j] >> (4 * p)) & 0xfu) << (4 * (j & 7));
+    for (int j = 0; j < 32; ++j) d[j >> 3] |= ((e[j] >> sh) & 0xfu) << (4 * (j & 7));
     *reinterpret_cast<uint4*>(dst + p * plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
   }
 }
@@ -167,7 +178,7 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 // ---------------------------------------------------------------------------
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
-template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1>
+template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
   static constexpr int KST = KST_;        // k-steps (64 reduction indices each) per stage
@@ -178,12 +189,17 @@ struct Cfg {
   static constexpr int PD = PD_;
   static constexpr int NSETS = PD == 1 ? 2 : KST;
   static_assert(PD >= 1 && PD < NSETS && KST % NSETS == 0, "fragment prefetch distance");
+  // Operand element format: 0 E2M1 (1 KiB bricks, 16 bytes per lane), 1 E4M3
+  // (2 KiB bricks, 32 bytes per lane; a brick takes two 1 KiB copies).
+  static constexpr int FMT = FMT_;
+  static constexpr int BRICK_BYTES = kBrickBytes << FMT;
+  static constexpr int COPIES = 1 << FMT;  // 1 KiB copies per brick
   static constexpr int NW = WM * WN;
   static constexpr int THREADS = 64 * NW;
   static constexpr int BM = WM * BMW * 32, BN = WN * BNW * 32;
   static constexpr int A_BRICKS = (BM / kBrickRows) * KST;  // per stage: row blocks x k-steps
   static constexpr int B_BRICKS = (BN / kBrickRows) * KST;
-  static constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * kBrickBytes;
+  static constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * BRICK_BYTES;
   static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES;
   // copies per wave and stage: A bricks evenly, B bricks round-robin (the first
   // B_BRICKS % NW waves take one more)
@@ -255,9 +271,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 template <class C, int STAGES>
 __device__ __forceinline__ void wait_stages(int wave) {
   if (C::B_XTRA == 0 || wave < C::B_XTRA)
-    wait_vmcnt<(C::A_PW + C::B_LO + (C::B_XTRA ? 1 : 0)) * STAGES>();
+    wait_vmcnt<(C::A_PW + C::B_LO + (C::B_XTRA ? 1 : 0)) * C::COPIES * STAGES>();
   else
-    wait_vmcnt<(C::A_PW + C::B_LO) * STAGES>();
+    wait_vmcnt<(C::A_PW + C::B_LO) * C::COPIES * STAGES>();
 }
 
 // Workgroup barrier that is also a compiler memory barrier: no LDS access may
@@ -274,22 +290,28 @@ __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, u
                                            int tm, int tn, int wave, int lane) {
   const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u), kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
   // k-step major planes: the bricks of one k-step for consecutive row blocks are adjacent
-  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * C::KST * g.rba * kBrickBytes;
-  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KST * g.rbb * kBrickBytes;
+  constexpr int BB = C::BRICK_BYTES;
+  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * C::KST * g.rba * BB;
+  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KST * g.rbb * BB;
   const uint32_t voff = lane * 16;
 #pragma unroll
   for (int i = 0; i < C::A_PW; ++i) {
     const int id = wave * C::A_PW + i;
     const int rb = min(tm * (C::BM / kBrickRows) + id / C::KST, g.rba - 1);
-    dma_brick(pa + ((int64_t)(id % C::KST) * g.rba + rb) * kBrickBytes, voff, stage_lds + id * kBrickBytes);
+#pragma unroll
+    for (int h = 0; h < C::COPIES; ++h)
+      dma_brick(pa + ((int64_t)(id % C::KST) * g.rba + rb) * BB + h * kBrickBytes, voff,
+                stage_lds + id * BB + h * kBrickBytes);
   }
 #pragma unroll
   for (int i = 0; i < C::B_LO + (C::B_XTRA ? 1 : 0); ++i) {
     const int id = wave + i * C::NW;
     if (i == C::B_LO && wave >= C::B_XTRA) break;
     const int cb = min(tn * (C::BN / kBrickRows) + id / C::KST, g.rbb - 1);
-    dma_brick(pb + ((int64_t)(id % C::KST) * g.rbb + cb) * kBrickBytes, voff,
-              stage_lds + (C::A_BRICKS + id) * kBrickBytes);
+#pragma unroll
+    for (int h = 0; h < C::COPIES; ++h)
+      dma_brick(pb + ((int64_t)(id % C::KST) * g.rbb + cb) * BB + h * kBrickBytes, voff,
+                stage_lds + (C::A_BRICKS + id) * BB + h * kBrickBytes);
   }
 }
 
@@ -297,6 +319,22 @@ __device__ __forceinline__ v8i frag(const uint8_t* p) {
   const int4 x = *reinterpret_cast<const int4*>(p);
   v8i v = {x.x, x.y, x.z, x.w, 0, 0, 0, 0};
   return v;
+}
+
+// A lane's 32 E4M3 elements (32 bytes) of an E4M3 brick.
+__device__ __forceinline__ v8i frag8(const uint8_t* p) {
+  const int4 x = *reinterpret_cast<const int4*>(p);
+  const int4 y = *reinterpret_cast<const int4*>(p + 16);
+  v8i v = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+  return v;
+}
+
+template <int FMT>
+__device__ __forceinline__ v8i frag_fmt(const uint8_t* brick, int lane) {
+  if constexpr (FMT == 0)
+    return frag(brick + lane * 16);
+  else
+    return frag8(brick + lane * 32);
 }
 
 // The wave's operand fragments for one k-step (64 reduction indices) of a stage.
@@ -310,14 +348,21 @@ __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, in
                                            int wn, int lane) {
 #pragma unroll
   for (int i = 0; i < C::BMW; ++i)
-    f.a[i] = frag(stage + ((wm * C::BMW + i) * C::KST + ks) * kBrickBytes + lane * 16);
+    f.a[i] = frag_fmt<C::FMT>(stage + ((wm * C::BMW + i) * C::KST + ks) * C::BRICK_BYTES, lane);
 #pragma unroll
   for (int j = 0; j < C::BNW; ++j)
-    f.b[j] = frag(stage + (C::A_BRICKS + (wn * C::BNW + j) * C::KST + ks) * kBrickBytes + lane * 16);
+    f.b[j] = frag_fmt<C::FMT>(stage + (C::A_BRICKS + (wn * C::BNW + j) * C::KST + ks) * C::BRICK_BYTES, lane);
 }
 
 __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
   acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 4, 4, 0, kScale2, 0, kScale2);
+}
+
+// E4M3 x E4M3 (format selects 0): the stored E4M3 values are the integers
+// themselves, so both block scales are 2^0 (byte 127).
+constexpr uint32_t kScale1 = 0x7f7f7f7fu;
+__device__ __forceinline__ void mfma_block8(v16f& acc, const v8i& a, const v8i& b) {
+  acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 0, 0, 0, kScale1, 0, kScale1);
 }
 
 #ifndef AWE_GEMM_GROUP_M
@@ -435,7 +480,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
 #pragma unroll
           for (int i = 0; i < C::BMW; ++i)
 #pragma unroll
-            for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], cur.a[i], cur.b[j]);
+            for (int j = 0; j < C::BNW; ++j) {
+              if constexpr (C::FMT == 0)
+                mfma_block(acc[i][j], cur.a[i], cur.b[j]);
+              else
+                mfma_block8(acc[i][j], cur.a[i], cur.b[j]);
+            }
           __builtin_amdgcn_sched_barrier(0);
         }
         buf = nbuf;
@@ -479,6 +529,7 @@ using Cfg8w64x96 = Cfg<4, 2, 2, 3, 2, 4>;    // 256 x 192, 8 waves (2 per SIMD)
 using Cfg4w128x64k4 = Cfg<2, 2, 4, 2, 4, 3>; // 256 x 128, 4 waves, 4 k-steps per stage
 using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps per stage
 using Cfg8w64x64k4p2 = Cfg<4, 2, 2, 2, 4, 3, 2>;  // as above, fragments read 2 k-steps ahead
+using Cfg8w64x64e4m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 1>;  // 256 x 128, 8 waves, E4M3 operands
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;
@@ -610,11 +661,11 @@ awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
   if (e.transposed)
     hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,
-                       e.nplanes, e.planes, e.plane_stride, e.flag, lut);
+                       e.nplanes, e.nplanes8, e.planes, e.plane_stride, e.flag, lut);
   else
     hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,
-                       e.nplanes, e.planes, e.plane_stride, e.flag, lut);
+                       e.nplanes, e.nplanes8, e.planes, e.plane_stride, e.flag, lut);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) {
     set_error(std::string("encode launch: ") + hipGetErrorString(err));
@@ -663,6 +714,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.log2D = L.log2D;
   g.modulus = L.modulus;
   g.outer = L.outer;
+  if (L.fp8) return launch_tile<Cfg8w64x64e4m3>(g, L, stream);
   switch (choose_cfg(L.M, L.N)) {
     case 0: return launch_tile<Cfg4w128x64>(g, L, stream);
     case 2: return launch_tile<Cfg8w64x96>(g, L, stream);

@@ -187,6 +187,37 @@ void define_fp16(Scheme& s) {
   s.wide = true;
 }
 
+// INT8 x INT8 with 2 FP8 products and 1 FP4 product (App. A): A = 13 h + 5 eps,
+// planes h, h + eps (E4M3) and eps (E2M1); AB = 104 P1 + 65 P2 - 40 P3.  The two
+// E4M3 products form one launch group, the E2M1 product another (outer 1).
+void define_fp8fp4(Scheme& s) {
+  s.p = s.q = 2;
+  s.w[0] = s.v[0] = 13;
+  s.w[1] = s.v[1] = 5;
+  s.na = s.nb = 3;
+  for (auto* pl : {&s.alpha, &s.beta}) {
+    set_plane(*pl, 0, {1, 0});
+    set_plane(*pl, 1, {1, 1});
+    set_plane(*pl, 2, {0, 1});
+  }
+  s.fmt_a[0] = s.fmt_a[1] = s.fmt_b[0] = s.fmt_b[1] = kFmtE4M3;
+  s.r = 3;
+  const int64_t l[3] = {104, 65, -40};
+  for (int k = 0; k < 3; ++k) {
+    s.pa[k] = s.pb[k] = k;
+    s.ell[k] = l[k];
+    s.lgroup[k] = k < 2 ? 0 : 1;
+  }
+  s.n_lgroups = 2;
+  s.louter[0] = s.louter[1] = 1;
+  s.lfmt[0] = kFmtE4M3;
+  s.lfmt[1] = kFmtE2M1;
+  s.limb_rule = kRuleFp8Fp4;
+  s.cap_a = s.cap_b = 14;
+  s.xmin_a = s.xmin_b = -128;
+  s.xmax_a = s.xmax_b = 127;
+}
+
 // ---- limb tuples ----------------------------------------------------------
 struct Tuple {
   int a[kMaxLimbs];
@@ -275,7 +306,10 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
 
   std::vector<Tuple> best(nx);
   std::vector<char> have(nx, 0);
-  if (s.modulus == 0) {
+  if (s.modulus == 0 && s.limb_rule == kRuleFp8Fp4) {
+    // the rule encodes every input of the range; no admissible-tuple search
+    (sideA ? s.coverage_a : s.coverage_b) = std::min(-xmin, xmax);
+  } else if (s.modulus == 0) {
     // values of w.a over the admissible tuples, for the coverage (Sec. 4.2)
     int64_t span = 0;
     for (int i = 0; i < p; ++i) span += 12 * (int64_t)std::abs(wts[i]);
@@ -289,7 +323,21 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
     while (X < span && hit[X + 1 + span] && hit[-(X + 1) + span]) ++X;
     (sideA ? s.coverage_a : s.coverage_b) = (int32_t)X;
   }
-  if (sideA ? s.positional13_a : s.positional13_b) {
+  if (s.limb_rule == kRuleFp8Fp4) {
+    // App. A: x = 13 h + 5 eps with eps the element of {0, +-1, +-2, +-3, +-4, +-6, +-8} in
+    // the residue class 5^-1 x mod 13 (the set holds each class once), h = (x - 5 eps) / 13
+    static const int kEps[13] = {0, 1, -1, 2, -2, 3, -3, 4, -4, 6, -6, 8, -8};
+    for (int x = xmin; x <= xmax; ++x) {
+      for (int e : kEps)
+        if (pmod(5 * e - x, 13) == 0) {
+          Tuple t{};
+          t.a[0] = (x - 5 * e) / 13;
+          t.a[1] = e;
+          best[x - xmin] = t;
+          have[x - xmin] = 1;
+        }
+    }
+  } else if (sideA ? s.positional13_a : s.positional13_b) {
     for (int x = xmin; x <= xmax; ++x) {
       int d[3];
       base13_digits(x, d);
@@ -318,6 +366,18 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
       return false;
     }
 
+  // Packed codes: the leading E4M3 planes take 8 bits each, then 4 bits per E2M1 plane.
+  const uint8_t* fmt = sideA ? s.fmt_a : s.fmt_b;
+  const int n8 = s.planes8(sideA);
+  for (int k = n8; k < np; ++k)
+    if (fmt[k] != kFmtE2M1) {
+      *msg = "E4M3 planes must precede the E2M1 planes";
+      return false;
+    }
+  if (8 * n8 + 4 * (np - n8) > 31) {
+    *msg = "packed codes exceed 31 bits";
+    return false;
+  }
   int cmax = 0;
   for (int b = 0; b < nt; ++b) {
     const int x = s.table_value(sideA, b);
@@ -328,17 +388,18 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
       int pv = plane_value(planes[k], a, p);
       val[b][k] = pv;
       cmax = std::max(cmax, std::abs(pv));
-      int code = e2m1_code(pv);
+      const bool f8 = k < n8;
+      int code = f8 ? e4m3_code(pv) : e2m1_code(pv);
       if (code < 0 || std::abs(pv) > cap) {
-        *msg = "stored value outside S or above the cap";
+        *msg = f8 ? "stored value not an E4M3 integer or above the cap" : "stored value outside S or above the cap";
         return false;
       }
-      packed |= (uint32_t)code << (4 * k);
+      packed |= (uint32_t)code << (f8 ? 8 * k : 8 * n8 + 4 * (k - n8));
     }
     // round trip: the limbs reproduce the input (Sec. 3.2), or its residue (Sec. 5.3)
     int64_t back = 0;
     for (int i = 0; i < p; ++i) {
-      if (!in_S(a[i])) {
+      if (s.limb_rule != kRuleFp8Fp4 && !in_S(a[i])) {
         *msg = "limb outside S";
         return false;
       }
@@ -391,9 +452,25 @@ void derive_bounds(Scheme& s) {
   const int64_t denom = (int64_t)s.n_g * s.c_a * s.c_b;
   s.k_star = (int64_t(1) << 24) / denom;
   // The fold multiplies each FP32 partial by its coefficient with a signed
-  // 24-bit multiply, so a partial must stay within 2^23 - 1 in magnitude.
-  int64_t seg = ((int64_t(1) << 23) - 1) / denom;
-  s.k_seg = seg / kKPad * kKPad;
+  // 24-bit multiply, so a partial must stay within 2^23 - 1 in magnitude.  Each
+  // launch group may use its own planes' bounds (the E2M1 product of the FP8 +
+  // FP4 scheme has c = 8 while its E4M3 products have c = 14).
+  s.k_seg = INT64_MAX;
+  for (int g = 0; g < s.n_lgroups; ++g) {
+    int64_t worst = 1;
+    for (int k = 0; k < s.r; ++k) {
+      if (s.lgroup[k] != g) continue;
+      int ca = 0, cb = 0;
+      for (int b = 0; b < s.table_size(true); ++b)
+        if (!(s.lut_a[b] & kLutInvalid)) ca = std::max(ca, std::abs(s.val_a[b][s.pa[k]]));
+      for (int b = 0; b < s.table_size(false); ++b)
+        if (!(s.lut_b[b] & kLutInvalid)) cb = std::max(cb, std::abs(s.val_b[b][s.pb[k]]));
+      worst = std::max<int64_t>(worst, (int64_t)ca * cb);
+    }
+    const int64_t seg = ((int64_t(1) << 23) - 1) / ((int64_t)s.n_g * worst) / kKPad * kKPad;
+    s.lkseg[g] = seg;
+    s.k_seg = std::min(s.k_seg, seg);
+  }
 }
 
 // Every launch group must reconstruct D times an integer on its own (its
@@ -401,6 +478,11 @@ void derive_bounds(Scheme& s) {
 // that the shift by log2 D can be applied per launch; its inner coefficients
 // must fit the kernel's signed 24-bit fold multiply.
 bool check_launch_groups(const Scheme& s, std::string* msg) {
+  for (int k = 0; k < s.r; ++k)
+    if (s.fmt_a[s.pa[k]] != s.lfmt[s.lgroup[k]] || s.fmt_b[s.pb[k]] != s.lfmt[s.lgroup[k]]) {
+      *msg = "a product's planes do not have its launch group's format";
+      return false;
+    }
   for (int g = 0; g < s.n_lgroups; ++g) {
     int64_t cm[kMaxLimbs][kMaxLimbs] = {};
     for (int k = 0; k < s.r; ++k) {
@@ -549,6 +631,19 @@ std::map<std::pair<int, int>, std::string> g_fail;
 
 }  // namespace
 
+// E4M3 code of a small integer (|v| <= 16 is exact: 3 mantissa bits after the
+// leading one), or -1: sign bit 7, exponent field (bias 7) bits 6..3, mantissa 2..0.
+int e4m3_code(int v) {
+  const int a = std::abs(v);
+  if (a == 0) return 0;
+  if (a > 16) return -1;
+  int e = 31 - __builtin_clz((unsigned)a);  // floor(log2 a)
+  const int frac = a - (1 << e);            // a = 2^e (1 + m / 8)
+  if ((frac << 3) % (1 << e) != 0) return -1;
+  const int m = (frac << 3) >> e;
+  return (v < 0 ? 0x80 : 0) | ((e + 7) << 3) | m;
+}
+
 int e2m1_code(int s) {
   int a = std::abs(s);
   for (int i = 0; i < 8; ++i)
@@ -563,7 +658,7 @@ int64_t plane_stride_bytes(int64_t rows, int64_t K) {
 }
 
 const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std::string* msg) {
-  if (enc < AWE_ENC_B13 || enc > AWE_ENC_FP16) {
+  if (enc < AWE_ENC_B13 || enc > AWE_ENC_FP8FP4) {
     *st = AWE_ERR_INVALID_VALUE;
     *msg = "unknown encoding";
     return nullptr;
@@ -596,6 +691,7 @@ const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std:
     case AWE_ENC_AWE4: define_awe4(*s); break;
     case AWE_ENC_TERNARY: define_ternary(*s); break;
     case AWE_ENC_FP16: define_fp16(*s); break;
+    case AWE_ENC_FP8FP4: define_fp8fp4(*s); break;
     case AWE_ENC_MOD:
       ok = define_mod(*s, modulus, &m);
       if (!ok) fail = AWE_ERR_UNSUPPORTED;

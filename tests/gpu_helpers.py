@@ -22,21 +22,58 @@ def to_dev(x):
     return torch.from_numpy(np.ascontiguousarray(x)).to(device())
 
 
-def decode_planes(buf, nplanes, rows, K):
-    """Stored planes (uint8 numpy) -> int64 array [nplanes, rows, K] of doubled values; padding checked."""
+def _e4m3_table():
+    """Value of every E4M3 code (OCP FP8: sign, 4 exponent bits with bias 7, 3 mantissa bits)."""
+    v = np.zeros(256)
+    for c in range(256):
+        e, m = (c >> 3) & 15, c & 7
+        mag = (m / 8.0) * 2.0 ** -6 if e == 0 else (1 + m / 8.0) * 2.0 ** (e - 7)
+        v[c] = -mag if c & 0x80 else mag
+    return v
+
+
+E4M3 = _e4m3_table()
+
+
+def _decode_e2m1(raw, R32, KS, Kp):
+    # raw [KS, R32, 64 lanes, 16 bytes] -> [R32*32, Kp] doubled values
+    raw = raw.transpose(1, 0, 2, 3)
+    nib = np.stack([raw & 0xF, raw >> 4], axis=-1).reshape(R32, KS, 2, 32, 32)
+    val = E2M1_MAG[nib & 7] * np.where(nib & 8, -1, 1)
+    return val.transpose(0, 3, 1, 2, 4).reshape(R32 * 32, Kp)
+
+
+def _decode_e4m3(raw, R32, KS, Kp):
+    # raw [KS, R32, 64 lanes, 32 bytes] -> [R32*32, Kp] values (integers)
+    raw = raw.transpose(1, 0, 2, 3).reshape(R32, KS, 2, 32, 32)
+    val = E4M3[raw]
+    assert np.array_equal(val, np.round(val)), "E4M3 planes hold integers"
+    return val.astype(np.int64).transpose(0, 3, 1, 2, 4).reshape(R32 * 32, Kp)
+
+
+def decode_planes(buf, nplanes, rows, K, formats=None):
+    """Stored planes (uint8 numpy) -> int64 array [nplanes, rows, K]: doubled values for E2M1
+    planes, the integers for E4M3 planes (formats: list of "e2m1"/"e4m3", default all E2M1);
+    every padding element checked to hold code 0."""
+    formats = formats or ["e2m1"] * nplanes
     R32 = -(-rows // 32)
     from paper_2609_24519_amd import awe
     Kp = -(-K // awe.K_PAD) * awe.K_PAD
     KS = Kp // 64
-    stride = R32 * KS * 1024
-    # k-step major: brick (rb, ks) at (ks * R32 + rb) * 1024
-    raw = np.asarray(buf[: nplanes * stride], dtype=np.uint8).reshape(nplanes, KS, R32, 64, 16)
-    raw = raw.transpose(0, 2, 1, 3, 4)
-    nib = np.stack([raw & 0xF, raw >> 4], axis=-1).reshape(nplanes, R32, KS, 2, 32, 32)
-    val = E2M1_MAG[nib & 7] * np.where(nib & 8, -1, 1)
-    # [p, rb, ks, h, t, j] -> [p, rb, t, ks, h, j]
-    full = val.transpose(0, 1, 4, 2, 3, 5).reshape(nplanes, R32 * 32, Kp)
-    pad = full.copy()
-    pad[:, :rows, :K] = 0
-    assert not pad.any(), "padding must hold code 0"
-    return full[:, :rows, :K]
+    unit = R32 * KS * 1024
+    out = []
+    off = 0
+    buf = np.asarray(buf, dtype=np.uint8)
+    for f in formats:
+        # k-step major: brick (rb, ks) at (ks * R32 + rb) * brick bytes
+        if f == "e4m3":
+            full = _decode_e4m3(buf[off: off + 2 * unit].reshape(KS, R32, 64, 32), R32, KS, Kp)
+            off += 2 * unit
+        else:
+            full = _decode_e2m1(buf[off: off + unit].reshape(KS, R32, 64, 16), R32, KS, Kp)
+            off += unit
+        pad = full.copy()
+        pad[:rows, :K] = 0
+        assert not pad.any(), "padding must hold code 0"
+        out.append(full[:rows, :K])
+    return np.stack(out) if out else np.zeros((0, rows, K), np.int64)

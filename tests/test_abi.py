@@ -16,7 +16,7 @@ from oracle import modm, schemes as sc
 from paper_2609_24519_amd import awe
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
-         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16}
+         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4}
 
 
 @lru_cache(maxsize=None)
@@ -56,6 +56,8 @@ def test_encoding_info_matches_oracle(name):
     assert info["k_seg"] % awe.K_PAD == 0 and 0 < info["k_seg"] <= info["k_star"]
     assert info["k_seg"] * s.n_g * c_a * c_b < 2 ** 23
     assert info["range_a"] == s.range_a and info["range_b"] == s.range_b
+    assert info["formats_a"] == (s.formats_a or ["e2m1"] * len(s.planes_a))
+    assert info["formats_b"] == (s.formats_b or ["e2m1"] * len(s.planes_b))
 
 
 def test_coverages(paper):

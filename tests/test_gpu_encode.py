@@ -11,7 +11,7 @@ from tests.gpu_helpers import decode_planes, to_dev
 pytestmark = pytest.mark.gpu
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
-         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16}
+         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4}
 
 
 def _dtype(lo, hi):
@@ -27,7 +27,8 @@ def _encode(enc, m, side, X, rows, K, flag=None):
     xd = to_dev(X)
     awe.encode(enc, m, side, xd, rows, K, X.shape[1], planes, flag)
     torch.cuda.synchronize()
-    return decode_planes(planes.cpu().numpy(), npl, rows, K)
+    fmts = info["formats_a"] if side == awe.SIDE_A else info["formats_b"]
+    return decode_planes(planes.cpu().numpy(), npl, rows, K, fmts)
 
 
 @pytest.mark.parametrize("name", sorted(EXACT))

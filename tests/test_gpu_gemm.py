@@ -15,7 +15,7 @@ from tests.gpu_helpers import to_dev
 
 pytestmark = pytest.mark.gpu
 
-EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4, awe.ENC_TERNARY]
+EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4, awe.ENC_TERNARY, awe.ENC_FP8FP4]
 
 
 def _run_exact(enc, A, B, out=torch.int32):
@@ -208,3 +208,18 @@ def test_fp16_12_products(shape, out):
     C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_FP16, out)
     torch.cuda.synchronize()
     assert np.array_equal(C.cpu().numpy().astype(np.int64), og.gemm_i64_wide(A, B))
+
+
+
+def test_fp8fp4_4096_sampled():
+    # App. A's 2 FP8 + 1 FP4 scheme at 4096 x 4096 x 8192, int32 C, sampled tiles; the two
+    # E4M3 products and the E2M1 product run as two launches adding into C
+    M = N = 4096
+    K = 8192
+    A, B = inputs.int8_pair(M, N, K, seed=4)
+    C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_FP8FP4, torch.int32)
+    torch.cuda.synchronize()
+    Ch = C.cpu().numpy()
+    for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=6):
+        ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
+        assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)

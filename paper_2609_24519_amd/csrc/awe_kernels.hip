@@ -227,6 +227,10 @@ struct GemmArgs {
   int32_t c64, accumulate, log2D, modulus;
   int32_t tiles_m, tiles_n;
   int64_t outer;  // C (+)= outer * (sum / D)
+  // Tiles n_full .. tiles_m * tiles_n - 1 (the ragged last round of workgroups) are
+  // each computed by `split` workgroups over consecutive parts of the reduction range,
+  // which add their exact partial results into C (zeroed beforehand) with atomics.
+  int32_t n_full, split;
 };
 
 // Position in the reduction stream: product p, k-tile t, current fold segment [cs, ce).
@@ -237,14 +241,14 @@ struct Cursor {
 // Advance to the next stage; saturates on the last stage of the launch (the
 // copies issued past the end re-read that stage into a buffer nobody reads,
 // which keeps the number of copies in flight the same for every stage).
-__device__ __forceinline__ void cursor_next(Cursor& c, const GemmArgs& g) {
+__device__ __forceinline__ void cursor_next(Cursor& c, const GemmArgs& g, int t_end) {
   const int t1 = c.t + 1;
   const bool end_t = t1 == c.ce;
   const int p1 = c.p + (end_t ? 1 : 0);
   const bool end_p = end_t && p1 == g.r;
-  const bool end_all = end_p && c.ce == g.t_end;
+  const bool end_all = end_p && c.ce == t_end;
   const int ncs = end_p ? c.ce : c.cs;
-  const int nce = end_p ? min(c.ce + g.ts, g.t_end) : c.ce;
+  const int nce = end_p ? min(c.ce + g.ts, t_end) : c.ce;
   c.t = end_all ? c.t : (end_t ? ncs : t1);
   c.p = end_all ? c.p : (end_p ? 0 : p1);
   c.cs = end_all ? c.cs : ncs;
@@ -374,9 +378,8 @@ __device__ __forceinline__ void mfma_block8(v16f& acc, const v8i& a, const v8i& 
 // once cover a compact block of C and share their A rows and B columns in
 // that XCD's L2.
 __device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& tm, int& tn) {
-  const int nb = g.tiles_m * g.tiles_n;
   int lin = bid;
-  if ((nb & 7) == 0) lin = (bid & 7) * (nb >> 3) + (bid >> 3);
+  if (bid < g.n_full && (g.n_full & 7) == 0) lin = (bid & 7) * (g.n_full >> 3) + (bid >> 3);
   const int per_group = AWE_GEMM_GROUP_M * g.tiles_n;
   const int grp = lin / per_group;
   const int first = grp * AWE_GEMM_GROUP_M;
@@ -411,13 +414,55 @@ __device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col
   }
 }
 
+// A part of a split tile: its exact partial (a whole number of reduction
+// indices with all products, so a multiple of D) is added atomically into C,
+// which the host zeroed (or which holds an earlier launch's sum).
+__device__ __forceinline__ void add_output(const GemmArgs& g, int row, int col, int32_t val) {
+  if (row >= g.M || col >= g.N) return;
+  const int64_t off = (int64_t)row * g.ldc + col;
+  const int64_t t = (int64_t)(val >> g.log2D) * g.outer;
+  if (g.c64)
+    atomicAdd(reinterpret_cast<unsigned long long*>(g.C) + off, (unsigned long long)t);
+  else
+    atomicAdd(reinterpret_cast<int32_t*>(g.C) + off, (int32_t)t);
+}
+
+// Zeroes the C region of the split tiles before the parts add into it.
+__global__ __launch_bounds__(256) void zero_tiles_kernel(GemmArgs g, int bm, int bn, int esize) {
+  int tm, tn;
+  tile_of_block(g, g.n_full + blockIdx.x, tm, tn);
+  const int rows = min(bm, g.M - tm * bm), cols = min(bn, g.N - tn * bn);
+  uint8_t* base = reinterpret_cast<uint8_t*>(g.C);
+  for (int i = threadIdx.x; i < rows * cols; i += blockDim.x) {
+    const int r = i / cols, c = i - r * cols;
+    const int64_t off = ((int64_t)(tm * bm + r) * g.ldc + tn * bn + c) * esize;
+    if (esize == 8)
+      *reinterpret_cast<int64_t*>(base + off) = 0;
+    else
+      *reinterpret_cast<int32_t*>(base + off) = 0;
+  }
+}
+
 template <class C>
 __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // Which tile, and which part of the reduction range: the workgroups past n_full
+  // share the ragged last round's tiles, `split` to a tile.
+  int tile = blockIdx.x, part = -1;
+  int t_beg = g.t_begin, t_end = g.t_end;
+  if (tile >= g.n_full) {
+    const int rel = tile - g.n_full;
+    tile = g.n_full + rel / g.split;
+    part = rel % g.split;
+    const int per = (g.t_end - g.t_begin + g.split - 1) / g.split;
+    t_beg = g.t_begin + part * per;
+    t_end = min(g.t_end, t_beg + per);
+    if (t_beg >= t_end) return;  // the host splits only ranges of at least 2 stages per part
+  }
   int tm, tn;
-  tile_of_block(g, blockIdx.x, tm, tn);
+  tile_of_block(g, tile, tm, tn);
   const int wm = wave / C::WN, wn = wave % C::WN;
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
 
@@ -434,12 +479,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
       }
 
   constexpr int NSTAGE = C::NSTAGE;
-  Cursor nxt{0, g.t_begin, g.t_begin, min(g.t_begin + g.ts, g.t_end)};
+  Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
   // Prologue: stages 0 .. NSTAGE-1 fill the whole ring.
 #pragma unroll
   for (int i = 0; i < NSTAGE; ++i) {
     load_stage<C>(g, nxt, lds0 + i * C::STAGE_BYTES, tm, tn, wave, lane);
-    cursor_next(nxt, g);
+    cursor_next(nxt, g, t_end);
   }
   wait_stages<C, NSTAGE - 1>(wave);
   block_barrier();
@@ -455,8 +500,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
   // were issued by then), barrier, refill stage s's buffer with stage s+NSTAGE.
   // The barrier sits between two groups of MFMAs.
   int buf = 0;
-  for (int cs = g.t_begin; cs < g.t_end; cs += g.ts) {
-    const int ce = min(cs + g.ts, g.t_end);
+  for (int cs = t_beg; cs < t_end; cs += g.ts) {
+    const int ce = min(cs + g.ts, t_end);
     for (int p = 0; p < g.r; ++p) {
       for (int t = cs; t < ce; ++t) {
         const uint32_t cur_off = buf * C::STAGE_BYTES;
@@ -468,7 +513,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
             wait_lgkm0();
             block_barrier();
             load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
-            cursor_next(nxt, g);
+            cursor_next(nxt, g, t_end);
           }
           const int kr = ks + PD;  // k-step whose fragments are read now
           if (kr < C::KST)
@@ -517,8 +562,13 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < C::BNW; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        store_output(g, row0 + i * 32 + 8 * (v >> 2) + (v & 3), col0 + j * 32, iacc[i][j][v]);
+      for (int v = 0; v < 16; ++v) {
+        const int row = row0 + i * 32 + 8 * (v >> 2) + (v & 3), col = col0 + j * 32;
+        if (part < 0)
+          store_output(g, row, col, iacc[i][j][v]);
+        else
+          add_output(g, row, col, iacc[i][j][v]);
+      }
 }
 
 // The tile configurations the launcher chooses from: waves (M x N), 32x32
@@ -530,6 +580,7 @@ using Cfg4w128x64k4 = Cfg<2, 2, 4, 2, 4, 3>; // 256 x 128, 4 waves, 4 k-steps pe
 using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps per stage
 using Cfg8w64x64k4p2 = Cfg<4, 2, 2, 2, 4, 3, 2>;  // as above, fragments read 2 k-steps ahead
 using Cfg8w64x64e4m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 1>;  // 256 x 128, 8 waves, E4M3 operands
+using Cfg8w64x96k4 = Cfg<4, 2, 2, 3, 4, 2>;         // 256 x 192, 8 waves, 4 k-steps, 2 stages
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;
@@ -540,28 +591,44 @@ __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, in
   }
 }
 
-// Tile configuration for a problem.  AWE_GEMM_CFG (0: 256x128 with 4 waves,
-// 1: 256x128 with 8 waves, 2: 256x192 with 8 waves, 3 and 4: as 0 and 1 with
-// 4 k-steps per stage, 5: as 4 with fragments read two k-steps ahead)
-// overrides the choice.  Otherwise: 256x128 on 8 waves with 4 k-steps per
-// stage and fragments read two k-steps ahead, or 256x192 when its rounds of
-// workgroups (each about 1.37 times as long as a 256x128 round, measured at
-// 8192^3) finish sooner, which happens when the 128-wide tiling leaves a
-// ragged last round.
-int choose_cfg(int64_t M, int64_t N) {
-  const char* e = getenv("AWE_GEMM_CFG");
-  const int forced = e ? atoi(e) : -1;
-  if (forced >= 0 && forced <= 5) return forced;
+// Compute units of the current device (AWE_GEMM_CUS overrides the count used
+// for planning the rounds of workgroups; it changes no result).
+int compute_units() {
+  const char* e = getenv("AWE_GEMM_CUS");
+  if (e && atoi(e) > 0) return atoi(e);
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) {
     int v = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
       cus = v;
   }
+  return cus;
+}
+
+// Rounds of workgroups for `tiles` tiles on `cus` CUs, with the ragged last
+// round split as launch_tile does.
+double rounds(int64_t tiles, int cus) {
+  const int64_t full = tiles / cus, rem = tiles % cus;
+  if (rem == 0) return (double)full;
+  const int64_t S = std::min<int64_t>(cus / rem, 4);
+  return (double)full + (full > 0 && S >= 2 ? 1.0 / S : 1.0);
+}
+
+// Tile configuration for a problem.  AWE_GEMM_CFG (0: 256x128 with 4 waves,
+// 1: 256x128 with 8 waves, 2: 256x192 with 8 waves, 3 and 4: as 0 and 1 with
+// 4 k-steps per stage, 5: as 4 with fragments read two k-steps ahead, 6:
+// 256x192 with 4 k-steps per stage in 2 stages) overrides the choice.
+// Otherwise: configuration 5, or 6 when its rounds of workgroups (each about
+// 1.33 times as long as a round of 5, measured at 8192^3) finish clearly sooner.
+int choose_cfg(int64_t M, int64_t N) {
+  const char* e = getenv("AWE_GEMM_CFG");
+  const int forced = e ? atoi(e) : -1;
+  if (forced >= 0 && forced <= 6) return forced;
+  const int cus = compute_units();
   const int64_t tm = (M + 255) / 256;
-  const double t128 = (double)((tm * ((N + 127) / 128) + cus - 1) / cus);
-  const double t192 = (double)((tm * ((N + 191) / 192) + cus - 1) / cus) * 1.37;
-  return t192 < t128 ? 2 : 5;
+  const double t128 = rounds(tm * ((N + 127) / 128), cus);
+  const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.33;
+  return t192 < 0.97 * t128 ? 6 : 5;
 }
 
 template <class C>
@@ -572,8 +639,35 @@ awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
   g.ts = (int32_t)(L.k_seg / C::KT);
   g.tiles_m = (int32_t)tiles_m;
   g.tiles_n = (int32_t)tiles_n;
-  const int64_t blocks = tiles_m * tiles_n;
-  if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;
+  const int64_t tiles = tiles_m * tiles_n;
+  if (tiles > 0x3fffffffLL) return AWE_ERR_UNSUPPORTED;
+  // A ragged last round of workgroups (rem tiles on cus CUs) is split along the
+  // reduction: each of its tiles is computed by S = min(cus / rem, 4) workgroups
+  // over consecutive parts of the range, so that round takes about 1/S of a
+  // tile's time.  Residues need the whole sum before their reduction mod m and
+  // are never split.
+  const int cus = compute_units();
+  const int stages = g.t_end - g.t_begin;
+  g.n_full = (int32_t)tiles;
+  g.split = 1;
+  if (!L.modulus && tiles > cus && tiles % cus != 0) {
+    const int64_t rem = tiles % cus;
+    const int S = (int)std::min<int64_t>(cus / rem, 4);
+    if (S >= 2 && stages >= 2 * S) {
+      g.n_full = (int32_t)(tiles - rem);
+      g.split = S;
+    }
+  }
+  const int64_t blocks = g.n_full + (tiles - g.n_full) * g.split;
+  if (g.split > 1 && !L.accumulate) {
+    hipLaunchKernelGGL(zero_tiles_kernel, dim3((unsigned)(tiles - g.n_full)), dim3(256), 0, stream, g,
+                       C::BM, C::BN, g.c64 ? 8 : 4);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) {
+      set_error(std::string("zero launch: ") + hipGetErrorString(err));
+      return AWE_ERR_HIP;
+    }
+  }
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<C>),
@@ -721,6 +815,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 3: return launch_tile<Cfg4w128x64k4>(g, L, stream);
     case 4: return launch_tile<Cfg8w64x64k4>(g, L, stream);
     case 5: return launch_tile<Cfg8w64x64k4p2>(g, L, stream);
+    case 6: return launch_tile<Cfg8w64x96k4>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }

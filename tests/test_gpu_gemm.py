@@ -161,7 +161,7 @@ def test_mod_forced_segments():
     assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
 
 
-@pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4", "5"])
+@pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4", "5", "6"])
 @pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13, awe.ENC_TERNARY])
 def test_every_tile_configuration(monkeypatch, cfg, enc):
     # AWE_GEMM_CFG forces one of the GEMM's tile configurations (256x128 on 4 or 8
@@ -223,3 +223,27 @@ def test_fp8fp4_4096_sampled():
     for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=6):
         ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
         assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)
+
+
+@pytest.mark.parametrize("cfg,cus", [("5", "12"), ("6", "16")])
+@pytest.mark.parametrize("enc,out", [(awe.ENC_AWE6, torch.int32), (awe.ENC_AWE4, torch.int64),
+                                     (awe.ENC_FP8FP4, torch.int32), (awe.ENC_FP16, torch.int64)])
+def test_split_last_round(monkeypatch, cfg, cus, enc, out):
+    # AWE_GEMM_CUS plans the rounds of workgroups for fewer CUs, so that this shape has a
+    # ragged last round (30 tiles on 12 CUs, 20 tiles on 16) whose tiles are split along
+    # the reduction into parts that add into C with atomics; the result must stay exact
+    # (for D = 2, with launch groups adding into C, and with E4M3 operands)
+    monkeypatch.setenv("AWE_GEMM_CFG", cfg)
+    monkeypatch.setenv("AWE_GEMM_CUS", cus)
+    M, N, K = 1100, 700, 2100
+    if enc == awe.ENC_FP16:
+        rng = np.random.default_rng(8)
+        A = inputs.uniform(rng, (M, K), -2048, 2047, np.int16)
+        B = inputs.uniform(rng, (K, N), -2048, 2047, np.int16)
+        ref = og.gemm_i64_wide(A, B)
+    else:
+        A, B = _operands(enc, M, N, K, seed=12)
+        ref = og.gemm_i64(A, B)
+    C = awe.matmul_exact(to_dev(A), to_dev(B), enc, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy().astype(np.int64), ref)

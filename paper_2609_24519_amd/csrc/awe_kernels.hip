@@ -40,6 +40,7 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
                                                      int64_t plane_stride, int32_t* flag,
                                                      LutArg lut) {
   __shared__ uint32_t slut[256];
+  __shared__ uint8_t tblk[kTransposed ? 4 : 1][kTransposed ? 64 * 32 : 1];  // per-wave input block
   slut[threadIdx.x] = lut.v[threadIdx.x];
   __syncthreads();
   const int lane = threadIdx.x & 63;
@@ -64,8 +65,25 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
       for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? slut[src[j]] : 0u;
     }
   } else {
+    // B side, K x N row-major: the brick needs the 64 x 32 block of B at rows
+    // (reduction indices) ks*64 .. +63 and columns rb*32 .. +31.  Lane l loads row
+    // ks*64 + l (32 contiguous bytes, two 16-byte loads) into this wave's slice of
+    // LDS; lane 32 h + t then reads column t of rows 32 h .. 32 h + 31.
+    uint8_t* tw = tblk[threadIdx.x >> 6];
+    const int64_t kr = ks * kBrickK + lane;
+    const int64_t n0 = rb * kBrickRows;
+    const uint8_t* src = x + kr * ld + n0;
+    if (kr < K && n0 + 32 <= rows && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+      *reinterpret_cast<uint4*>(tw + lane * 32) = *reinterpret_cast<const uint4*>(src);
+      *reinterpret_cast<uint4*>(tw + lane * 32 + 16) = *reinterpret_cast<const uint4*>(src + 16);
+    } else {
+      for (int c = 0; c < 32; ++c) tw[lane * 32 + c] = (kr < K && n0 + c < rows) ? src[c] : 0;
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+    const uint8_t* col = tw + (lane >> 5) * 32 * 32 + (lane & 31);
 #pragma unroll
-    for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? slut[x[(k0 + j) * ld + row]] : 0u;
+    for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? slut[col[j * 32]] : 0u;
   }
   uint32_t bad = 0;
 #pragma unroll
@@ -427,19 +445,21 @@ __device__ __forceinline__ void add_output(const GemmArgs& g, int row, int col, 
     atomicAdd(reinterpret_cast<int32_t*>(g.C) + off, (int32_t)t);
 }
 
-// Zeroes the C region of the split tiles before the parts add into it.
+// Zeroes the C region of the split tiles before the parts add into it: block
+// (x, y) clears rows y, y + gridDim.y, ... of split tile x, consecutive threads
+// on consecutive columns.
 __global__ __launch_bounds__(256) void zero_tiles_kernel(GemmArgs g, int bm, int bn, int esize) {
   int tm, tn;
   tile_of_block(g, g.n_full + blockIdx.x, tm, tn);
   const int rows = min(bm, g.M - tm * bm), cols = min(bn, g.N - tn * bn);
-  uint8_t* base = reinterpret_cast<uint8_t*>(g.C);
-  for (int i = threadIdx.x; i < rows * cols; i += blockDim.x) {
-    const int r = i / cols, c = i - r * cols;
-    const int64_t off = ((int64_t)(tm * bm + r) * g.ldc + tn * bn + c) * esize;
-    if (esize == 8)
-      *reinterpret_cast<int64_t*>(base + off) = 0;
-    else
-      *reinterpret_cast<int32_t*>(base + off) = 0;
+  for (int r = blockIdx.y; r < rows; r += gridDim.y) {
+    const int64_t row = (int64_t)(tm * bm + r) * g.ldc + tn * bn;
+    for (int c = threadIdx.x; c < cols; c += blockDim.x) {
+      if (esize == 8)
+        reinterpret_cast<int64_t*>(g.C)[row + c] = 0;
+      else
+        reinterpret_cast<int32_t*>(g.C)[row + c] = 0;
+    }
   }
 }
 
@@ -660,7 +680,7 @@ awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
   }
   const int64_t blocks = g.n_full + (tiles - g.n_full) * g.split;
   if (g.split > 1 && !L.accumulate) {
-    hipLaunchKernelGGL(zero_tiles_kernel, dim3((unsigned)(tiles - g.n_full)), dim3(256), 0, stream, g,
+    hipLaunchKernelGGL(zero_tiles_kernel, dim3((unsigned)(tiles - g.n_full), 32), dim3(256), 0, stream, g,
                        C::BM, C::BN, g.c64 ? 8 : 4);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) {

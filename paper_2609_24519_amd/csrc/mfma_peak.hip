@@ -57,9 +57,9 @@ extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
     if (e == hipSuccess) e = hipEventSynchronize(e1);
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
   }
-  if (e0) hipEventDestroy(e0);
-  if (e1) hipEventDestroy(e1);
-  hipFree(sink);
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipFree(sink);
   if (e != hipSuccess) return (int)e;
   const double flop = (double)cus * waves_per_cu * iters * kMfmaPerIter * kFlopPerMfma;
   *tflops = flop / ((double)ms * 1e-3) / 1e12;

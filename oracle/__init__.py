@@ -11,7 +11,9 @@ and the CPU-baseline leg of ``bench.py`` may import or execute it.
                  loaded through ctypes.
 * ``schemes`` -- the paper's encodings (storable set, limb tables, planes,
                  reconstruction coefficients, coverage, K*), the scheme
-                 identity and the run-time procedure in plain numpy int64.
+                 identity and the run-time procedure in plain numpy int64;
+                 also the INT8 x INT8 variant in 3 E2M3 (FP6) products that
+                 the Karatsuba threshold of Sec. 3.3 admits.
 * ``modm``    -- the congruence (mod m) schemes and their tables.
 * ``crt``     -- residues and the Chinese-remainder reconstruction of a
                  residue number system, in Python integers.

@@ -258,6 +258,71 @@ PAPER_SCHEMES = {"b13": b13, "awe6": awe6, "awe6_alt": awe6_alt, "awe4": awe4, "
 
 
 # ---------------------------------------------------------------------------
+# E2M3 (OCP MX FP6): sign bit 5, 2 exponent bits (bias 1), 3 mantissa bits;
+# every one of the 64 codes is finite.
+# ---------------------------------------------------------------------------
+def e2m3_value(code):
+    sign = -1.0 if code & 0x20 else 1.0
+    e = (code >> 3) & 3
+    m = code & 7
+    if e == 0:  # subnormal: m / 8 * 2^(1 - bias)
+        return sign * (m / 8.0)
+    return sign * (1.0 + m / 8.0) * 2.0 ** (e - 1)
+
+
+def e2m3_code(v):
+    """Code of an exactly representable value (searched over all codes)."""
+    for c in range(64):
+        if e2m3_value(c) == v and not (v == 0 and c & 0x20):
+            return c
+    raise ValueError("%r is not an E2M3 value" % (v,))
+
+
+def contiguous_half_width(values, scale):
+    """Largest X such that every integer in [-X, X] is scale times a value of the format
+    (the contiguous integer part that Sec. 3.3 measures)."""
+    ints = {int(scale * v) for v in values if float(scale * v).is_integer()}
+    X = 0
+    while X + 1 in ints and -(X + 1) in ints:
+        X += 1
+    return X
+
+
+# Integers n of an E2M3 plane are stored as the E2M3 value n / 8; a block scale of
+# 2^3 on each operand restores n_a n_b in every product (Sec. 4.5 form of the scale).
+FP6_SCALE = 8
+
+
+def fp6k3_limbs(x):
+    """x = a0 + 16 a1 with the balanced base-16 digit a0 in [-8, 7]."""
+    a0 = (x + 8) % 16 - 8
+    return (a0, (x - a0) // 16)
+
+
+def fp6k3():
+    """INT8 x INT8 in 3 E2M3 (FP6) products: one Karatsuba-type step on base-16 limbs.
+
+    Sec. 3.3: a Karatsuba-type step forms a product of limb sums, and the sums must be
+    storable; for a format with an m-bit significand the contiguous integer part is
+    [-2^(m+1), 2^(m+1)], wide enough only from m = 3.  E2M3 has m = 3: with n stored as
+    n / 8 it holds every integer of [-16, 16].  Base-16 limbs of an INT8 value lie in
+    [-8, 8], so a0 + a1 fits.  With P1 = a0 b0, P2 = a1 b1, P3 = (a0 + a1)(b0 + b1):
+    AB = P1 + 16 (P3 - P1 - P2) + 256 P2 = -15 P1 + 240 P2 + 16 P3, D = 1.
+    Not one of the paper's catalogued schemes: the same construction on the FP6 format.
+    """
+    planes = [(1, 0), (0, 1), (1, 1)]
+    prods = [(pl, pl, l) for pl, l in zip(planes, (-15, 240, 16))]
+    s = Scheme("fp6k3", (1, 16), (1, 16), prods, 1, 16, 16, INT8_RANGE, INT8_RANGE)
+    s.limb_rule = {"a": fp6k3_limbs, "b": fp6k3_limbs}
+    s.formats_a = s.formats_b = ["e2m3", "e2m3", "e2m3"]
+    return s
+
+
+VARIANT_SCHEMES = {"fp6k3": fp6k3}
+ALL_SCHEMES = dict(PAPER_SCHEMES, **VARIANT_SCHEMES)
+
+
+# ---------------------------------------------------------------------------
 # Identity checks (Sec. 4.2 coefficient-matrix equation; Sec. 4.7 all pairs)
 # ---------------------------------------------------------------------------
 def coefficient_matrix(s):

@@ -250,3 +250,57 @@ def test_fp8fp4_scheme(paper):
     A = rng.integers(-128, 127, (9, 70), endpoint=True)
     B = rng.integers(-128, 127, (70, 6), endpoint=True)
     assert np.array_equal(sc.scheme_gemm(s, A, B), A @ B)
+
+
+def test_e2m3_format_facts(paper):
+    # OCP MX FP6 E2M3: 1.0, the largest value 7.5 and the smallest subnormal 0.125
+    one, big, smin = paper["e2m3.codes"]
+    assert sc.e2m3_value(one) == 1.0 and sc.e2m3_value(big) == 7.5 and sc.e2m3_value(smin) == 0.125
+    vals = [sc.e2m3_value(c) for c in range(64)]
+    assert max(vals) == 7.5 and min(vals) == -7.5 and len(set(vals)) == 63  # +0 and -0 coincide
+
+
+def test_contiguous_part_threshold(paper):
+    # Sec. 3.3: a format with an m-bit significand holds the contiguous integer range
+    # [-2^(m+1), 2^(m+1)] (at the scale that makes its smallest step 1); E2M1 (m = 1)
+    # gives S's [-4, 4], E2M3 and E4M3 (m = 3) give [-16, 16], the first wide enough
+    # for a Karatsuba-type step.
+    e2m1 = sc.E2M1_VALUES + tuple(-v for v in sc.E2M1_VALUES)
+    assert sc.contiguous_half_width(e2m1, 2) == paper["contiguous.S"][0]
+    assert sc.contiguous_half_width(e2m1, 2) == 2 ** (1 + 1)
+    m = paper["karatsuba.min_m"][0]
+    e2m3 = [sc.e2m3_value(c) for c in range(64)]
+    assert sc.contiguous_half_width(e2m3, sc.FP6_SCALE) == 2 ** (m + 1)
+    assert sc.contiguous_half_width([sc.e4m3_value(c) for c in range(256)], 1) == 2 ** (m + 1)
+    # base-16 limb sums of INT8 values need [-16, 16]: inside E2M3's part, outside S's
+    sums = {sum(sc.fp6k3_limbs(x)) for x in range(-128, 128)}
+    assert max(abs(v) for v in sums) <= 2 ** (m + 1)
+    assert max(abs(v) for v in sums) > paper["contiguous.S"][0]
+
+
+def test_fp6k3_scheme():
+    s = sc.fp6k3()
+    limbs = sc.limb_table(s, "a")
+    assert all(a0 + 16 * a1 == x and -8 <= a0 <= 7 and -8 <= a1 <= 8 for x, (a0, a1) in limbs.items())
+    assert sc.coefficient_identity_holds(s)
+    assert sc.brute_force_pairs(s)  # all 65,536 int8 pairs
+    caps = (sc.stored_cap(s, "a"), sc.stored_cap(s, "b"))
+    assert caps == (15, 15)
+    assert sc.k_star(1, *caps) == 74565
+    # every plane value is n with n / 8 an E2M3 value, coded as sign bit 5 | |n|
+    _, T = sc.plane_table(s, "a")
+    for n in np.unique(T):
+        assert sc.e2m3_value(sc.e2m3_code(n / sc.FP6_SCALE)) * sc.FP6_SCALE == n
+        assert sc.e2m3_code(n / sc.FP6_SCALE) == (0x20 if n < 0 else 0) | abs(int(n))
+    rng = np.random.default_rng(11)
+    A = rng.integers(-128, 127, (9, 70), endpoint=True)
+    B = rng.integers(-128, 127, (70, 6), endpoint=True)
+    assert np.array_equal(sc.scheme_gemm(s, A, B), A @ B)
+
+
+@pytest.mark.parametrize("k,delta", [(0, 1), (1, -1), (2, 1)])
+def test_fp6k3_mutation_caught(k, delta):
+    s = sc.fp6k3()
+    bad = _mutate_ell(s, k, s.products[k][2] + delta)
+    assert not sc.coefficient_identity_holds(bad)
+    assert not sc.brute_force_pairs(bad)

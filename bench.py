@@ -160,6 +160,17 @@ def main():
             "gemm_ms": round(fgemm_ms, 4),
             "gemm_exact_TOPS": round(ops / (fgemm_ms * 1e-3) / 1e12, 2),
             "fp4_equiv_peak_frac": round(5 * ops / (fgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
+        # INT8 x INT8 in 3 E2M3 (FP6) products on the same A and B (one Karatsuba-type step,
+        # which Sec. 3.3 admits from a 3-bit significand); E2M3 MFMAs run at the E2M1 rate
+        sinfo, swall, senc_ms, sgemm_ms = run(awe.ENC_FP6K3, max(3, args.steps // 2), 2)
+        line["fp6k3_3_fp6_products"] = {
+            "ms_per_step": round(swall / max(3, args.steps // 2) * 1e3, 4),
+            "exact_TOPS": round(ops / (swall / max(3, args.steps // 2)) / 1e12, 2),
+            "encode_ms": round(senc_ms, 4),
+            "gemm_ms": round(sgemm_ms, 4),
+            "gemm_exact_TOPS": round(ops / (sgemm_ms * 1e-3) / 1e12, 2),
+            "fp6_TFLOPs": round(sinfo["r"] * ops / (sgemm_ms * 1e-3) / 1e12, 1),
+            "fp6_peak_frac": round(sinfo["r"] * ops / (sgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
         # {0, +-1} x INT8 (Sec. 6.2) on the same B: 3 products
         At = torch.from_numpy(inputs.int8_pair(M, 8, K, seed=5, a_range=(-1, 1))[0]).to(dev)
         tinfo, pta, ptb = setup(awe.ENC_TERNARY)
@@ -299,6 +310,16 @@ def mfma_sustained(iters=20000):
             return {"error": "HIP error %d" % rc}
         out["%d_waves_per_cu_TFLOPs" % waves] = round(tf.value, 1)
         out["%d_waves_frac_of_peak" % waves] = round(tf.value / FP4_PEAK_TFLOPS, 4)
+    # the same probe with E2M3 (FP6) and E4M3 (FP8) operands, 8 waves per CU: the data
+    # sheet lists FP6 at the FP4 rate and FP8 at half of it
+    lib.awe_mfma_peak_fmt.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_double)]
+    for fmt, name in ((2, "e2m3"), (0, "e4m3")):
+        tf = ctypes.c_double(0.0)
+        rc = lib.awe_mfma_peak_fmt(fmt, 8, iters, ctypes.byref(tf))
+        if rc != 0:
+            return {"error": "HIP error %d" % rc}
+        out["%s_8_waves_per_cu_TFLOPs" % name] = round(tf.value, 1)
     return out
 
 

@@ -48,6 +48,14 @@
  * owning bytes L*32 .. L*32+31, byte j the OCP E4M3 code of element j (the integer
  * itself: every stored value has |v| <= 14).  An E4M3 plane takes two strides, and a
  * side stores its E4M3 planes before its E2M1 planes.
+ * E2M3 (FP6) planes (AWE_ENC_FP6K3) take 1.5 strides each and are grouped in 3072-byte
+ * units of two consecutive k-steps: unit (rb, u) at byte (u * ceil(rows/32) + rb) * 3072
+ * covers rows rb*32 .. rb*32+31 and reduction indices u*128 .. u*128+127.  Lane L's 32
+ * elements of k-step 2u + i (i in {0,1}, the same rows and indices as lane L of an E2M1
+ * brick) form a 192-bit word, element j in bits 6j .. 6j+5; its first 16 bytes sit at
+ * byte i*1024 + L*16 of the unit and its last 8 bytes at byte 2048 + i*512 + L*8.  Each
+ * 6-bit field is the OCP E2M3 code of n/8 for the stored integer n (|n| <= 16):
+ * bit 5 the sign, bits 4..0 the value |n| itself.
  */
 #ifndef AWE_H
 #define AWE_H
@@ -86,9 +94,13 @@ typedef enum awe_encoding {
                           w = v = (1, 9, 71, 639), D = 2 (App. A).  Both operands are int16 in
                           [-2048, 2047]; the products run as four launches, one per outer weight
                           71^(k+l), each adding its share into C. */
-  AWE_ENC_FP8FP4 = 8   /* INT8 x INT8 with 2 FP8 (E4M3) products and 1 FP4 product (App. A):
+  AWE_ENC_FP8FP4 = 8,  /* INT8 x INT8 with 2 FP8 (E4M3) products and 1 FP4 product (App. A):
                           A = 13 h + 5 eps, planes h, h + eps (E4M3, 2 KiB bricks, see the
                           layout above) and eps (E2M1); AB = 104 P1 + 65 P2 - 40 P3. */
+  AWE_ENC_FP6K3 = 9    /* INT8 x INT8 in 3 E2M3 (FP6) products: A = a0 + 16 a1 with a0 in [-8, 7],
+                          planes a0, a1, a0 + a1 (within [-15, 15], inside E2M3's contiguous
+                          integer range, the Karatsuba condition of Sec. 3.3);
+                          AB = -15 P1 + 240 P2 + 16 P3.  Not a catalogued scheme of the paper. */
 } awe_encoding;
 
 typedef enum awe_side { AWE_SIDE_A = 0, AWE_SIDE_B = 1 } awe_side;
@@ -121,7 +133,7 @@ typedef struct awe_encoding_info {
   int32_t group[AWE_MAX_PRODUCTS];/* accumulator shared by product k (equal ell_k) */
   int64_t k_star;                 /* floor(2^24 / (n_g c_a c_b)), Sec. 3.4 */
   int64_t k_seg;                  /* default fold segment of the GEMM (<= k_star), multiple of AWE_K_PAD */
-  int32_t format_a[AWE_MAX_PLANES];  /* element format of stored A plane k: 0 E2M1, 1 E4M3 */
+  int32_t format_a[AWE_MAX_PLANES];  /* element format of stored A plane k: 0 E2M1, 1 E4M3, 2 E2M3 */
   int32_t format_b[AWE_MAX_PLANES];
 } awe_encoding_info;
 

@@ -18,10 +18,13 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "awe.h")
 
 # awe_status
 OK, ERR_INVALID_VALUE, ERR_UNSUPPORTED, ERR_OVERFLOW, ERR_WORKSPACE, ERR_HIP, ERR_TABLE = range(7)
+_FORMATS = ("e2m1", "e4m3", "e2m3")  # element format codes of awe_encoding_info
 # awe_encoding
-ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY, ENC_FP16, ENC_FP8FP4 = 1, 2, 3, 4, 5, 6, 7, 8
+ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY, ENC_FP16, ENC_FP8FP4, ENC_FP6K3 = \
+    1, 2, 3, 4, 5, 6, 7, 8, 9
 ENCODINGS = {"b13": ENC_B13, "awe6": ENC_AWE6, "awe6_alt": ENC_AWE6ALT, "awe4": ENC_AWE4, "mod": ENC_MOD,
-             "ternary": ENC_TERNARY, "fp16_12": ENC_FP16, "fp8fp4": ENC_FP8FP4}
+             "ternary": ENC_TERNARY, "fp16_12": ENC_FP16, "fp8fp4": ENC_FP8FP4,
+             "fp6k3": ENC_FP6K3}
 # awe_side, awe_dtype
 SIDE_A, SIDE_B = 0, 1
 I32, I64 = 0, 1
@@ -152,8 +155,8 @@ def get_encoding_info(enc, modulus=0):
         "pair_a": list(info.pair_a[:r]), "pair_b": list(info.pair_b[:r]),
         "ell": list(info.ell[:r]), "group": list(info.group[:r]),
         "k_star": info.k_star, "k_seg": info.k_seg,
-        "formats_a": ["e4m3" if f else "e2m1" for f in info.format_a[:info.planes_a]],
-        "formats_b": ["e4m3" if f else "e2m1" for f in info.format_b[:info.planes_b]],
+        "formats_a": [_FORMATS[f] for f in info.format_a[:info.planes_a]],
+        "formats_b": [_FORMATS[f] for f in info.format_b[:info.planes_b]],
     }
 
 

@@ -33,7 +33,7 @@ const Scheme* scheme_or_fail(awe_encoding enc, int32_t modulus, awe_status* st) 
 }
 
 size_t side_bytes(const Scheme& s, bool sideA, int64_t rows, int64_t K) {
-  return (size_t)s.plane_units(sideA, sideA ? s.na : s.nb) * (size_t)plane_stride_bytes(rows, K);
+  return (size_t)s.plane_halves(sideA, sideA ? s.na : s.nb) * (size_t)(plane_stride_bytes(rows, K) / 2);
 }
 
 // Largest reduction length (multiple of kKPad) one GEMM launch may cover so that
@@ -109,12 +109,12 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
   for (int64_t k0 = 0; k0 < kp; k0 += step) {
     for (int g = 0; g < s.n_lgroups; ++g) {
       // the group's planes share one format; address them from the first plane of it
-      L.fp8 = s.lfmt[g] == kFmtE4M3;
-      const int first_a = L.fp8 ? 0 : s.planes8(true), first_b = L.fp8 ? 0 : s.planes8(false);
-      L.planes_a = reinterpret_cast<const uint8_t*>(pa) + s.plane_units(true, first_a) * unit_a;
-      L.planes_b = reinterpret_cast<const uint8_t*>(pb) + s.plane_units(false, first_b) * unit_b;
-      L.stride_a = (L.fp8 ? 2 : 1) * unit_a;
-      L.stride_b = (L.fp8 ? 2 : 1) * unit_b;
+      L.fmt = s.lfmt[g];
+      const int first_a = s.first_plane(true, L.fmt), first_b = s.first_plane(false, L.fmt);
+      L.planes_a = reinterpret_cast<const uint8_t*>(pa) + s.plane_halves(true, first_a) * (unit_a / 2);
+      L.planes_b = reinterpret_cast<const uint8_t*>(pb) + s.plane_halves(false, first_b) * (unit_b / 2);
+      L.stride_a = fmt_halves(L.fmt) * (unit_a / 2);
+      L.stride_b = fmt_halves(L.fmt) * (unit_b / 2);
       L.k_seg = own_seg ? s.lkseg[g] : k_seg;
       L.r = 0;
       L.fold_mask = 0;
@@ -158,6 +158,7 @@ awe_status encode_impl(const Scheme& s, awe_side side, const void* x, int64_t ro
   e.is_unsigned = sideA ? s.a_unsigned : s.b_unsigned;
   e.nplanes = sideA ? s.na : s.nb;
   e.nplanes8 = s.planes8(sideA);
+  e.fp6 = (sideA ? s.fmt_a : s.fmt_b)[0] == kFmtE2M3;
   e.planes = reinterpret_cast<uint8_t*>(planes);
   e.plane_stride = plane_stride_bytes(rows, K);
   e.flag = flag;

@@ -26,8 +26,11 @@ constexpr uint32_t kLutInvalid = 0x80000000u;
 constexpr int kWideValues = 4096;
 
 // Plane element formats and limb rules.
-constexpr uint8_t kFmtE2M1 = 0, kFmtE4M3 = 1;
-constexpr int kRuleChoice = 0, kRuleBase13 = 1, kRuleFp8Fp4 = 2;
+constexpr uint8_t kFmtE2M1 = 0, kFmtE4M3 = 1, kFmtE2M3 = 2;
+constexpr int kRuleChoice = 0, kRuleBase13 = 1, kRuleFp8Fp4 = 2, kRuleBase16 = 3;
+
+// Storage of one plane of a format, in halves of an E2M1 plane's stride.
+inline int fmt_halves(uint8_t f) { return f == kFmtE4M3 ? 4 : (f == kFmtE2M3 ? 3 : 2); }
 
 // One scheme (Definition 4.1 of the paper, or its mod-m congruence form)
 // together with the encoding tables derived from it.
@@ -52,7 +55,8 @@ struct Scheme {
   uint8_t lfmt[kMaxProducts] = {};    // element format of group g's operands (kFmt*)
   int64_t lkseg[kMaxProducts] = {};   // fold segment of group g (from its own plane bounds)
   // Element format of every stored plane; planes of one side are stored in this
-  // order, E4M3 planes (twice the bytes) before E2M1 planes.
+  // order, E4M3 planes (twice the bytes) before E2M1 planes.  A side with E2M3
+  // planes (1.5 times the bytes) holds only E2M3 planes.
   uint8_t fmt_a[kMaxPlanes] = {}, fmt_b[kMaxPlanes] = {};
   int limb_rule = 0;                  // kRule*: how an input's limbs are chosen
   int log2D = 0;
@@ -66,10 +70,18 @@ struct Scheme {
     while (n < (sideA ? na : nb) && (sideA ? fmt_a : fmt_b)[n]) ++n;
     return n;
   }
-  // Plane k's offset in units of one E2M1 plane (an E4M3 plane counts 2).
-  int plane_units(bool sideA, int k) const {
-    const int n8 = planes8(sideA);
-    return k <= n8 ? 2 * k : 2 * n8 + (k - n8);
+  // Plane k's byte offset in halves of one E2M1 plane stride.
+  int plane_halves(bool sideA, int k) const {
+    int h = 0;
+    for (int j = 0; j < k; ++j) h += fmt_halves((sideA ? fmt_a : fmt_b)[j]);
+    return h;
+  }
+  // First stored plane of format f on a side (the planes of one format are adjacent).
+  int first_plane(bool sideA, uint8_t f) const {
+    const int n = sideA ? na : nb;
+    for (int k = 0; k < n; ++k)
+      if ((sideA ? fmt_a : fmt_b)[k] == f) return k;
+    return n;
   }
 
   // derived by build_tables()
@@ -104,6 +116,9 @@ int e2m1_code(int s);
 // E4M3 code of an integer with |v| <= 16, or -1.
 int e4m3_code(int v);
 
+// E2M3 code of v / 8 for an integer with |v| <= 16, or -1.
+int e2m3_code(int v);
+
 // Bytes of one plane of `rows` x `K`.
 int64_t plane_stride_bytes(int64_t rows, int64_t K);
 
@@ -115,6 +130,7 @@ struct EncodeLaunch {
   bool is_unsigned;
   int nplanes;
   int nplanes8;         // the first nplanes8 planes are E4M3 (8-bit codes), the rest E2M1
+  bool fp6;             // every plane is E2M3 (8-bit fields of the table, 3072-byte units)
   uint8_t* planes;
   int64_t plane_stride;
   int32_t* flag;
@@ -135,7 +151,7 @@ struct GemmLaunch {
   int32_t pa[kMaxProducts], pb[kMaxProducts];
   int32_t fold_ell[kMaxProducts];  // coefficient applied when the accumulator is folded after product k
   int64_t outer;                   // the launch adds outer * (sum / D) into C
-  bool fp8;                        // operands are E4M3 planes (else E2M1)
+  uint8_t fmt;                     // element format of both operands' planes (kFmt*)
   uint32_t fold_mask;              // bit k: fold after product k
   int64_t k_seg;                   // fold segment length (multiple of kKPad)
   int64_t k_begin, k_end;          // reduction range of this launch (multiples of kKPad)

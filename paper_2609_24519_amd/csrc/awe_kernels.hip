@@ -36,7 +36,8 @@ template <bool kTransposed>
 __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__ x, int64_t rows,
                                                      int64_t K, int64_t ld, int64_t KS,
                                                      int64_t R32, int64_t nbricks, int nplanes,
-                                                     int nplanes8, uint8_t* __restrict__ planes,
+                                                     int nplanes8, bool fp6,
+                                                     uint8_t* __restrict__ planes,
                                                      int64_t plane_stride, int32_t* flag,
                                                      LutArg lut) {
   __shared__ uint32_t slut[256];
@@ -89,6 +90,28 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
 #pragma unroll
   for (int j = 0; j < 32; ++j) bad |= e[j];
   if ((bad & kLutInvalid) && flag != nullptr) atomicOr(flag, 1);
+
+  if (fp6) {
+    // E2M3 planes (1.5 plane strides each) in 3 KiB units of two k-steps: lane L's 32
+    // six-bit codes form 6 dwords, the first 4 at i*1024 + 16 L and the last 2 at
+    // 2048 + i*512 + 8 L of the unit (i = ks & 1).
+    uint8_t* unit = planes + ((ks >> 1) * R32 + rb) * (3 * kBrickBytes);
+    const int i = (int)(ks & 1);
+    for (int p = 0; p < nplanes; ++p) {
+      uint32_t d[6] = {0, 0, 0, 0, 0, 0};
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        const uint32_t c = (e[j] >> (8 * p)) & 0x3fu;
+        const int bit = 6 * j;
+        d[bit >> 5] |= c << (bit & 31);
+        if ((bit & 31) > 26) d[(bit >> 5) + 1] |= c >> (32 - (bit & 31));
+      }
+      uint8_t* u = unit + p * (3 * plane_stride / 2);
+      *reinterpret_cast<uint4*>(u + i * 1024 + lane * 16) = make_uint4(d[0], d[1], d[2], d[3]);
+      *reinterpret_cast<uint2*>(u + 2048 + i * 512 + lane * 8) = make_uint2(d[4], d[5]);
+    }
+    return;
+  }
 
   // E4M3 planes (2 KiB bricks, 32 bytes per lane) first, then the E2M1 planes; an E4M3
   // plane occupies two plane strides.
@@ -207,23 +230,27 @@ struct Cfg {
   static constexpr int PD = PD_;
   static constexpr int NSETS = PD == 1 ? 2 : KST;
   static_assert(PD >= 1 && PD < NSETS && KST % NSETS == 0, "fragment prefetch distance");
-  // Operand element format: 0 E2M1 (1 KiB bricks, 16 bytes per lane), 1 E4M3
-  // (2 KiB bricks, 32 bytes per lane; a brick takes two 1 KiB copies).
+  // Operand element format and its storage unit: 0 E2M1, one k-step in 1 KiB (16 bytes
+  // per lane); 1 E4M3, one k-step in 2 KiB (32 bytes per lane); 2 E2M3, two k-steps in
+  // 3 KiB (24 bytes per lane and k-step).  Units move as 1 KiB copies.
   static constexpr int FMT = FMT_;
-  static constexpr int BRICK_BYTES = kBrickBytes << FMT;
-  static constexpr int COPIES = 1 << FMT;  // 1 KiB copies per brick
+  static constexpr int UK = FMT == 2 ? 2 : 1;  // k-steps per unit
+  static constexpr int UNIT_BYTES = FMT == 0 ? kBrickBytes : (FMT == 1 ? 2 * kBrickBytes : 3 * kBrickBytes);
+  static constexpr int COPIES = UNIT_BYTES / kBrickBytes;
+  static constexpr int KU = KST / UK;          // units per row block and stage
+  static_assert(KST % UK == 0, "a stage holds whole units");
   static constexpr int NW = WM * WN;
   static constexpr int THREADS = 64 * NW;
   static constexpr int BM = WM * BMW * 32, BN = WN * BNW * 32;
-  static constexpr int A_BRICKS = (BM / kBrickRows) * KST;  // per stage: row blocks x k-steps
-  static constexpr int B_BRICKS = (BN / kBrickRows) * KST;
-  static constexpr int STAGE_BYTES = (A_BRICKS + B_BRICKS) * BRICK_BYTES;
+  static constexpr int A_UNITS = (BM / kBrickRows) * KU;  // per stage: row blocks x units
+  static constexpr int B_UNITS = (BN / kBrickRows) * KU;
+  static constexpr int STAGE_BYTES = (A_UNITS + B_UNITS) * UNIT_BYTES;
   static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES;
-  // copies per wave and stage: A bricks evenly, B bricks round-robin (the first
-  // B_BRICKS % NW waves take one more)
-  static constexpr int A_PW = A_BRICKS / NW;
-  static constexpr int B_LO = B_BRICKS / NW, B_XTRA = B_BRICKS % NW;
-  static_assert(A_BRICKS % NW == 0, "A bricks must split evenly over the waves");
+  // copies per wave and stage: A units evenly, B units round-robin (the first
+  // B_UNITS % NW waves take one more)
+  static constexpr int A_PW = A_UNITS / NW;
+  static constexpr int B_LO = B_UNITS / NW, B_XTRA = B_UNITS % NW;
+  static_assert(A_UNITS % NW == 0, "A units must split evenly over the waves");
   static_assert(kKPad % KT == 0, "a stage must divide the reduction padding");
 };
 
@@ -305,35 +332,35 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 
 __device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// The copies of one stage: wave w takes A bricks A_PW w .. A_PW w + A_PW - 1
-// and B bricks w, w + NW, ... (brick id = KST * row block + k-step).
+// The copies of one stage: wave w takes A units A_PW w .. A_PW w + A_PW - 1
+// and B units w, w + NW, ... (unit id = KU * row block + unit of the stage).
 template <class C>
 __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
                                            int tm, int tn, int wave, int lane) {
   const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u), kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
-  // k-step major planes: the bricks of one k-step for consecutive row blocks are adjacent
-  constexpr int BB = C::BRICK_BYTES;
-  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * C::KST * g.rba * BB;
-  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KST * g.rbb * BB;
+  // k-step major planes: the units of one k-step (pair) for consecutive row blocks are adjacent
+  constexpr int UB = C::UNIT_BYTES;
+  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * C::KU * g.rba * UB;
+  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KU * g.rbb * UB;
   const uint32_t voff = lane * 16;
 #pragma unroll
   for (int i = 0; i < C::A_PW; ++i) {
     const int id = wave * C::A_PW + i;
-    const int rb = min(tm * (C::BM / kBrickRows) + id / C::KST, g.rba - 1);
+    const int rb = min(tm * (C::BM / kBrickRows) + id / C::KU, g.rba - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pa + ((int64_t)(id % C::KST) * g.rba + rb) * BB + h * kBrickBytes, voff,
-                stage_lds + id * BB + h * kBrickBytes);
+      dma_brick(pa + ((int64_t)(id % C::KU) * g.rba + rb) * UB + h * kBrickBytes, voff,
+                stage_lds + id * UB + h * kBrickBytes);
   }
 #pragma unroll
   for (int i = 0; i < C::B_LO + (C::B_XTRA ? 1 : 0); ++i) {
     const int id = wave + i * C::NW;
     if (i == C::B_LO && wave >= C::B_XTRA) break;
-    const int cb = min(tn * (C::BN / kBrickRows) + id / C::KST, g.rbb - 1);
+    const int cb = min(tn * (C::BN / kBrickRows) + id / C::KU, g.rbb - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pb + ((int64_t)(id % C::KST) * g.rbb + cb) * BB + h * kBrickBytes, voff,
-                stage_lds + (C::A_BRICKS + id) * BB + h * kBrickBytes);
+      dma_brick(pb + ((int64_t)(id % C::KU) * g.rbb + cb) * UB + h * kBrickBytes, voff,
+                stage_lds + (C::A_UNITS + id) * UB + h * kBrickBytes);
   }
 }
 
@@ -351,12 +378,24 @@ __device__ __forceinline__ v8i frag8(const uint8_t* p) {
   return v;
 }
 
+// A lane's 32 E2M3 elements (24 bytes) of k-step i of an E2M3 unit: dwords 0..3 at
+// i*1024 + 16 L, dwords 4..5 at 2048 + i*512 + 8 L.
+__device__ __forceinline__ v8i frag6(const uint8_t* unit, int i, int lane) {
+  const int4 x = *reinterpret_cast<const int4*>(unit + i * 1024 + lane * 16);
+  const int2 y = *reinterpret_cast<const int2*>(unit + 2048 + i * 512 + lane * 8);
+  v8i v = {x.x, x.y, x.z, x.w, y.x, y.y, 0, 0};
+  return v;
+}
+
+// Fragment of k-step i of a unit.
 template <int FMT>
-__device__ __forceinline__ v8i frag_fmt(const uint8_t* brick, int lane) {
+__device__ __forceinline__ v8i frag_fmt(const uint8_t* unit, int i, int lane) {
   if constexpr (FMT == 0)
-    return frag(brick + lane * 16);
+    return frag(unit + lane * 16);
+  else if constexpr (FMT == 1)
+    return frag8(unit + lane * 32);
   else
-    return frag8(brick + lane * 32);
+    return frag6(unit, i, lane);
 }
 
 // The wave's operand fragments for one k-step (64 reduction indices) of a stage.
@@ -368,12 +407,13 @@ struct Frags {
 template <class C>
 __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, int ks, int wm,
                                            int wn, int lane) {
+  const int u = ks / C::UK, i = ks % C::UK;
 #pragma unroll
-  for (int i = 0; i < C::BMW; ++i)
-    f.a[i] = frag_fmt<C::FMT>(stage + ((wm * C::BMW + i) * C::KST + ks) * C::BRICK_BYTES, lane);
+  for (int ia = 0; ia < C::BMW; ++ia)
+    f.a[ia] = frag_fmt<C::FMT>(stage + ((wm * C::BMW + ia) * C::KU + u) * C::UNIT_BYTES, i, lane);
 #pragma unroll
   for (int j = 0; j < C::BNW; ++j)
-    f.b[j] = frag_fmt<C::FMT>(stage + (C::A_BRICKS + (wn * C::BNW + j) * C::KST + ks) * C::BRICK_BYTES, lane);
+    f.b[j] = frag_fmt<C::FMT>(stage + (C::A_UNITS + (wn * C::BNW + j) * C::KU + u) * C::UNIT_BYTES, i, lane);
 }
 
 __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
@@ -385,6 +425,13 @@ __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b
 constexpr uint32_t kScale1 = 0x7f7f7f7fu;
 __device__ __forceinline__ void mfma_block8(v16f& acc, const v8i& a, const v8i& b) {
   acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 0, 0, 0, kScale1, 0, kScale1);
+}
+
+// E2M3 x E2M3 (format selects 2): a stored integer n is the E2M3 value n / 8, so
+// both block scales are 2^3 (byte 130) and each product of codes is n_a n_b.
+constexpr uint32_t kScale8 = 0x82828282u;
+__device__ __forceinline__ void mfma_block6(v16f& acc, const v8i& a, const v8i& b) {
+  acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 2, 2, 0, kScale8, 0, kScale8);
 }
 
 #ifndef AWE_GEMM_GROUP_M
@@ -548,8 +595,10 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
             for (int j = 0; j < C::BNW; ++j) {
               if constexpr (C::FMT == 0)
                 mfma_block(acc[i][j], cur.a[i], cur.b[j]);
-              else
+              else if constexpr (C::FMT == 1)
                 mfma_block8(acc[i][j], cur.a[i], cur.b[j]);
+              else
+                mfma_block6(acc[i][j], cur.a[i], cur.b[j]);
             }
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -601,6 +650,11 @@ using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps pe
 using Cfg8w64x64k4p2 = Cfg<4, 2, 2, 2, 4, 3, 2>;  // as above, fragments read 2 k-steps ahead
 using Cfg8w64x64e4m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 1>;  // 256 x 128, 8 waves, E4M3 operands
 using Cfg8w64x96k4 = Cfg<4, 2, 2, 3, 4, 2>;         // 256 x 192, 8 waves, 4 k-steps, 2 stages
+// E2M3 operands (3 KiB units of two k-steps)
+using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
+using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
+using Cfg4w128x64e2m3 = Cfg<2, 2, 4, 2, 2, 3, 1, 2>;  // 256 x 128, 4 waves, 2 k-steps, 3 stages
+using Cfg8w64x64k4e2m3 = Cfg<4, 2, 2, 2, 4, 2, 1, 2>; // 256 x 128, 8 waves, 4 k-steps, 2 stages
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;
@@ -649,6 +703,17 @@ int choose_cfg(int64_t M, int64_t N) {
   const double t128 = rounds(tm * ((N + 127) / 128), cus);
   const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.33;
   return t192 < 0.97 * t128 ? 6 : 5;
+}
+
+// Tile configuration for E2M3 operands: AWE_GEMM_CFG_E2M3 (0: 256x128 with 8 waves in
+// 3 stages, 1: as 0 in 4 stages, 2: 256x128 with 4 waves, 3: as 0 with 4 k-steps per
+// stage in 2 stages) overrides the default 0.  (256x192 on 8 waves would need more
+// than the 256 registers a wave has at 2 waves per SIMD: its 6-register E2M3 fragments
+// spill.)
+int choose_cfg_e2m3() {
+  const char* e = getenv("AWE_GEMM_CFG_E2M3");
+  const int forced = e ? atoi(e) : -1;
+  return forced >= 0 && forced <= 3 ? forced : 0;
 }
 
 template <class C>
@@ -775,11 +840,11 @@ awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
   if (e.transposed)
     hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,
-                       e.nplanes, e.nplanes8, e.planes, e.plane_stride, e.flag, lut);
+                       e.nplanes, e.nplanes8, e.fp6, e.planes, e.plane_stride, e.flag, lut);
   else
     hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,
-                       e.nplanes, e.nplanes8, e.planes, e.plane_stride, e.flag, lut);
+                       e.nplanes, e.nplanes8, e.fp6, e.planes, e.plane_stride, e.flag, lut);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) {
     set_error(std::string("encode launch: ") + hipGetErrorString(err));
@@ -828,7 +893,15 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.log2D = L.log2D;
   g.modulus = L.modulus;
   g.outer = L.outer;
-  if (L.fp8) return launch_tile<Cfg8w64x64e4m3>(g, L, stream);
+  if (L.fmt == kFmtE4M3) return launch_tile<Cfg8w64x64e4m3>(g, L, stream);
+  if (L.fmt == kFmtE2M3) {
+    switch (choose_cfg_e2m3()) {
+      case 1: return launch_tile<Cfg8w64x64s4e2m3>(g, L, stream);
+      case 2: return launch_tile<Cfg4w128x64e2m3>(g, L, stream);
+      case 3: return launch_tile<Cfg8w64x64k4e2m3>(g, L, stream);
+      default: return launch_tile<Cfg8w64x64e2m3>(g, L, stream);
+    }
+  }
   switch (choose_cfg(L.M, L.N)) {
     case 0: return launch_tile<Cfg4w128x64>(g, L, stream);
     case 2: return launch_tile<Cfg8w64x96>(g, L, stream);

@@ -218,6 +218,35 @@ void define_fp8fp4(Scheme& s) {
   s.xmax_a = s.xmax_b = 127;
 }
 
+// INT8 x INT8 in 3 E2M3 (FP6) products: a Karatsuba-type step (Sec. 3.3 gives its
+// condition, limb sums inside the format's contiguous integer range, met from a 3-bit
+// significand) on balanced base-16 limbs: A = a0 + 16 a1 with a0 in [-8, 7], planes
+// a0, a1, a0 + a1 (all within 15); AB = -15 P1 + 240 P2 + 16 P3 with P1 = a0 b0,
+// P2 = a1 b1, P3 = (a0 + a1)(b0 + b1), D = 1.
+void define_fp6k3(Scheme& s) {
+  s.p = s.q = 2;
+  s.w[0] = s.v[0] = 1;
+  s.w[1] = s.v[1] = 16;
+  s.na = s.nb = 3;
+  for (auto* pl : {&s.alpha, &s.beta}) {
+    set_plane(*pl, 0, {1, 0});
+    set_plane(*pl, 1, {0, 1});
+    set_plane(*pl, 2, {1, 1});
+  }
+  for (int k = 0; k < 3; ++k) s.fmt_a[k] = s.fmt_b[k] = kFmtE2M3;
+  s.r = 3;
+  const int64_t l[3] = {-15, 240, 16};
+  for (int k = 0; k < 3; ++k) {
+    s.pa[k] = s.pb[k] = k;
+    s.ell[k] = l[k];
+  }
+  s.lfmt[0] = kFmtE2M3;
+  s.limb_rule = kRuleBase16;
+  s.cap_a = s.cap_b = 16;
+  s.xmin_a = s.xmin_b = -128;
+  s.xmax_a = s.xmax_b = 127;
+}
+
 // ---- limb tuples ----------------------------------------------------------
 struct Tuple {
   int a[kMaxLimbs];
@@ -306,7 +335,8 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
 
   std::vector<Tuple> best(nx);
   std::vector<char> have(nx, 0);
-  if (s.modulus == 0 && s.limb_rule == kRuleFp8Fp4) {
+  const bool by_rule = s.limb_rule == kRuleFp8Fp4 || s.limb_rule == kRuleBase16;
+  if (s.modulus == 0 && by_rule) {
     // the rule encodes every input of the range; no admissible-tuple search
     (sideA ? s.coverage_a : s.coverage_b) = std::min(-xmin, xmax);
   } else if (s.modulus == 0) {
@@ -337,6 +367,15 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
           have[x - xmin] = 1;
         }
     }
+  } else if (s.limb_rule == kRuleBase16) {
+    // x = a0 + 16 a1 with the balanced digit a0 in [-8, 7]
+    for (int x = xmin; x <= xmax; ++x) {
+      Tuple t{};
+      t.a[0] = (int)pmod(x + 8, 16) - 8;
+      t.a[1] = (x - t.a[0]) / 16;
+      best[x - xmin] = t;
+      have[x - xmin] = 1;
+    }
   } else if (sideA ? s.positional13_a : s.positional13_b) {
     for (int x = xmin; x <= xmax; ++x) {
       int d[3];
@@ -366,12 +405,15 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
       return false;
     }
 
-  // Packed codes: the leading E4M3 planes take 8 bits each, then 4 bits per E2M1 plane.
+  // Packed codes: the leading E4M3 planes take 8 bits each, then 4 bits per E2M1 plane;
+  // a side of E2M3 planes (only those) takes 8 bits per plane.
   const uint8_t* fmt = sideA ? s.fmt_a : s.fmt_b;
-  const int n8 = s.planes8(sideA);
-  for (int k = n8; k < np; ++k)
-    if (fmt[k] != kFmtE2M1) {
-      *msg = "E4M3 planes must precede the E2M1 planes";
+  const bool f6 = fmt[0] == kFmtE2M3;
+  const int n8 = f6 ? np : s.planes8(sideA);
+  for (int k = 0; k < np; ++k)
+    if (f6 ? fmt[k] != kFmtE2M3 : (k >= n8 && fmt[k] != kFmtE2M1)) {
+      *msg = f6 ? "E2M3 planes cannot be mixed with other formats"
+                : "E4M3 planes must precede the E2M1 planes";
       return false;
     }
   if (8 * n8 + 4 * (np - n8) > 31) {
@@ -389,9 +431,11 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
       val[b][k] = pv;
       cmax = std::max(cmax, std::abs(pv));
       const bool f8 = k < n8;
-      int code = f8 ? e4m3_code(pv) : e2m1_code(pv);
+      int code = f6 ? e2m3_code(pv) : (f8 ? e4m3_code(pv) : e2m1_code(pv));
       if (code < 0 || std::abs(pv) > cap) {
-        *msg = f8 ? "stored value not an E4M3 integer or above the cap" : "stored value outside S or above the cap";
+        *msg = f6   ? "stored value outside E2M3's integer range or above the cap"
+               : f8 ? "stored value not an E4M3 integer or above the cap"
+                    : "stored value outside S or above the cap";
         return false;
       }
       packed |= (uint32_t)code << (f8 ? 8 * k : 8 * n8 + 4 * (k - n8));
@@ -399,7 +443,7 @@ bool build_side(Scheme& s, bool sideA, std::string* msg) {
     // round trip: the limbs reproduce the input (Sec. 3.2), or its residue (Sec. 5.3)
     int64_t back = 0;
     for (int i = 0; i < p; ++i) {
-      if (s.limb_rule != kRuleFp8Fp4 && !in_S(a[i])) {
+      if (!by_rule && !in_S(a[i])) {
         *msg = "limb outside S";
         return false;
       }
@@ -644,6 +688,15 @@ int e4m3_code(int v) {
   return (v < 0 ? 0x80 : 0) | ((e + 7) << 3) | m;
 }
 
+// E2M3 code of v / 8 (|v| <= 16): the subnormals m / 8 and the first binade
+// 1 + m / 8 give |v| = 0 .. 15 as the 5-bit field itself, and 16 / 8 = 2 is
+// exponent field 2 with mantissa 0, again the field value 16; bit 5 is the sign.
+int e2m3_code(int v) {
+  const int a = std::abs(v);
+  if (a > 16) return -1;
+  return (v < 0 ? 0x20 : 0) | a;
+}
+
 int e2m1_code(int s) {
   int a = std::abs(s);
   for (int i = 0; i < 8; ++i)
@@ -658,7 +711,7 @@ int64_t plane_stride_bytes(int64_t rows, int64_t K) {
 }
 
 const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std::string* msg) {
-  if (enc < AWE_ENC_B13 || enc > AWE_ENC_FP8FP4) {
+  if (enc < AWE_ENC_B13 || enc > AWE_ENC_FP6K3) {
     *st = AWE_ERR_INVALID_VALUE;
     *msg = "unknown encoding";
     return nullptr;
@@ -692,6 +745,7 @@ const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std:
     case AWE_ENC_TERNARY: define_ternary(*s); break;
     case AWE_ENC_FP16: define_fp16(*s); break;
     case AWE_ENC_FP8FP4: define_fp8fp4(*s); break;
+    case AWE_ENC_FP6K3: define_fp6k3(*s); break;
     case AWE_ENC_MOD:
       ok = define_mod(*s, modulus, &m);
       if (!ok) fail = AWE_ERR_UNSUPPORTED;

@@ -1,5 +1,5 @@
 // Sustained rate of the GEMM's instruction, the scaled 32x32x64 MFMA with E2M1
-// operands and FP32 accumulation, when every wave issues independent MFMAs
+// (or E2M3, E4M3) operands and FP32 accumulation, when every wave issues independent MFMAs
 // from registers and touches no memory in the loop.  It gives the practical
 // ceiling the GEMM kernel is compared with next to the data-sheet peak (which
 // assumes the peak engine clock under full MFMA load).  Benchmark helper only:
@@ -16,14 +16,17 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 constexpr int kMfmaPerIter = 16;
 constexpr double kFlopPerMfma = 2.0 * 32 * 32 * 64;
 
+// Operand formats as the MFMA's format selects: 4 E2M1 (scale 2^1), 2 E2M3 (2^3), 0 E4M3 (2^0).
+template <int FMT>
 __global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float* sink) {
+  constexpr uint32_t kScale = FMT == 4 ? 0x80808080u : (FMT == 2 ? 0x82828282u : 0x7f7f7f7fu);
   v16f c[4] = {};
-  const v8i a = {(int)threadIdx.x, 0x11111111, 0x22222222, 0x33333333, 0, 0, 0, 0};
+  const v8i a = {(int)threadIdx.x, 0x11111111, 0x22222222, 0x33333333, 0x04040404, 0x05050505, 0, 0};
   for (int it = 0; it < iters; ++it) {
 #pragma unroll
     for (int m = 0; m < kMfmaPerIter; ++m)
-      c[m & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, a, c[m & 3], 4, 4, 0, 0x80808080,
-                                                                0, 0x80808080);
+      c[m & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, a, c[m & 3], FMT, FMT, 0, kScale,
+                                                                0, kScale);
   }
   const float s = c[0][0] + c[1][0] + c[2][0] + c[3][0];
   if (s == 0.125f) sink[blockIdx.x] = s;  // never true in practice; keeps the MFMAs live
@@ -31,10 +34,10 @@ __global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float* sink) 
 
 }  // namespace
 
-// Runs one workgroup of `waves_per_cu` waves (1..8) per compute unit for
-// `iters` iterations of 16 MFMAs per wave after one warm-up launch, and
-// writes the achieved dense FP4 rate in TFLOP/s.  Returns 0, or a HIP error code.
-extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
+namespace {
+
+template <int FMT>
+int run_peak(int waves_per_cu, int iters, double* tflops) {
   if (waves_per_cu < 1 || waves_per_cu > 8 || iters < 1 || tflops == nullptr) return (int)hipErrorInvalidValue;
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -46,11 +49,11 @@ extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
   float ms = 0.f;
   const dim3 grid(cus), block(64 * waves_per_cu);
   if ((e = hipEventCreate(&e0)) == hipSuccess && (e = hipEventCreate(&e1)) == hipSuccess) {
-    hipLaunchKernelGGL(mfma_peak_kernel, grid, block, 0, nullptr, iters, sink);
+    hipLaunchKernelGGL(mfma_peak_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
     e = hipGetLastError();
     if (e == hipSuccess) e = hipEventRecord(e0, nullptr);
     if (e == hipSuccess) {
-      hipLaunchKernelGGL(mfma_peak_kernel, grid, block, 0, nullptr, iters, sink);
+      hipLaunchKernelGGL(mfma_peak_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
       e = hipGetLastError();
     }
     if (e == hipSuccess) e = hipEventRecord(e1, nullptr);
@@ -64,4 +67,23 @@ extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
   const double flop = (double)cus * waves_per_cu * iters * kMfmaPerIter * kFlopPerMfma;
   *tflops = flop / ((double)ms * 1e-3) / 1e12;
   return 0;
+}
+
+}  // namespace
+
+// Runs one workgroup of `waves_per_cu` waves (1..8) per compute unit for
+// `iters` iterations of 16 MFMAs per wave after one warm-up launch, and
+// writes the achieved dense FP4 rate in TFLOP/s.  Returns 0, or a HIP error code.
+extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
+  return run_peak<4>(waves_per_cu, iters, tflops);
+}
+
+// As awe_mfma_peak for operand format `fmt` (4 E2M1, 2 E2M3, 0 E4M3).
+extern "C" int awe_mfma_peak_fmt(int fmt, int waves_per_cu, int iters, double* tflops) {
+  switch (fmt) {
+    case 4: return run_peak<4>(waves_per_cu, iters, tflops);
+    case 2: return run_peak<2>(waves_per_cu, iters, tflops);
+    case 0: return run_peak<0>(waves_per_cu, iters, tflops);
+    default: return (int)hipErrorInvalidValue;
+  }
 }

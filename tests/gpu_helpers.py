@@ -35,6 +35,19 @@ def _e4m3_table():
 E4M3 = _e4m3_table()
 
 
+def _e2m3_table():
+    """Value of every E2M3 code (OCP MX FP6: sign bit 5, 2 exponent bits with bias 1, 3 mantissa bits)."""
+    v = np.zeros(64)
+    for c in range(64):
+        e, m = (c >> 3) & 3, c & 7
+        mag = m / 8.0 if e == 0 else (1 + m / 8.0) * 2.0 ** (e - 1)
+        v[c] = -mag if c & 0x20 else mag
+    return v
+
+
+E2M3 = _e2m3_table()
+
+
 def _decode_e2m1(raw, R32, KS, Kp):
     # raw [KS, R32, 64 lanes, 16 bytes] -> [R32*32, Kp] doubled values
     raw = raw.transpose(1, 0, 2, 3)
@@ -51,10 +64,24 @@ def _decode_e4m3(raw, R32, KS, Kp):
     return val.astype(np.int64).transpose(0, 3, 1, 2, 4).reshape(R32 * 32, Kp)
 
 
+def _decode_e2m3(raw, R32, KS, Kp):
+    # raw [KS/2 units, R32, 3072 bytes] -> [R32*32, Kp] integers n (stored as n / 8)
+    U = KS // 2
+    lo = raw[:, :, :2048].reshape(U, R32, 2, 64, 16)
+    hi = raw[:, :, 2048:].reshape(U, R32, 2, 64, 8)
+    words = np.concatenate([lo, hi], axis=-1)                    # [U, R32, i, lane, 24 bytes]
+    bits = np.unpackbits(words, axis=-1, bitorder="little")      # [..., 192], bit b of the word
+    codes = (bits.reshape(U, R32, 2, 64, 32, 6) << np.arange(6, dtype=np.uint8)).sum(-1)
+    val = E2M3[codes] * 8
+    assert np.array_equal(val, np.round(val)), "E2M3 planes hold integers / 8"
+    val = val.astype(np.int64).reshape(U, R32, 2, 2, 32, 32)    # [u, rb, i, h, t, j]
+    return val.transpose(1, 4, 0, 2, 3, 5).reshape(R32 * 32, Kp)
+
+
 def decode_planes(buf, nplanes, rows, K, formats=None):
     """Stored planes (uint8 numpy) -> int64 array [nplanes, rows, K]: doubled values for E2M1
-    planes, the integers for E4M3 planes (formats: list of "e2m1"/"e4m3", default all E2M1);
-    every padding element checked to hold code 0."""
+    planes, the integers for E4M3 and E2M3 planes (formats: list of "e2m1"/"e4m3"/"e2m3",
+    default all E2M1); every padding element checked to hold code 0."""
     formats = formats or ["e2m1"] * nplanes
     R32 = -(-rows // 32)
     from paper_2609_24519_amd import awe
@@ -69,6 +96,9 @@ def decode_planes(buf, nplanes, rows, K, formats=None):
         if f == "e4m3":
             full = _decode_e4m3(buf[off: off + 2 * unit].reshape(KS, R32, 64, 32), R32, KS, Kp)
             off += 2 * unit
+        elif f == "e2m3":  # units of two k-steps: unit (rb, u) at (u * R32 + rb) * 3072
+            full = _decode_e2m3(buf[off: off + 3 * unit // 2].reshape(KS // 2, R32, 3072), R32, KS, Kp)
+            off += 3 * unit // 2
         else:
             full = _decode_e2m1(buf[off: off + unit].reshape(KS, R32, 64, 16), R32, KS, Kp)
             off += unit

@@ -16,7 +16,8 @@ from oracle import modm, schemes as sc
 from paper_2609_24519_amd import awe
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
-         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4}
+         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4,
+         "fp6k3": awe.ENC_FP6K3}
 
 
 @lru_cache(maxsize=None)
@@ -40,7 +41,7 @@ def test_exports_every_declared_symbol():
 
 @pytest.mark.parametrize("name", sorted(EXACT))
 def test_encoding_info_matches_oracle(name):
-    s = sc.PAPER_SCHEMES[name]()
+    s = sc.ALL_SCHEMES[name]()
     info = awe.get_encoding_info(EXACT[name])
     assert info["r"] == s.r
     assert info["w"] == s.w and info["v"] == s.v
@@ -68,7 +69,7 @@ def test_coverages(paper):
 
 @pytest.mark.parametrize("name", sorted(EXACT))
 def test_plane_tables_match_oracle(name):
-    s = sc.PAPER_SCHEMES[name]()
+    s = sc.ALL_SCHEMES[name]()
     for side, oside in ((awe.SIDE_A, "a"), (awe.SIDE_B, "b")):
         lo, T = awe.get_plane_table(EXACT[name], 0, side)
         olo, OT = sc.plane_table(s, oside)

@@ -11,7 +11,8 @@ from tests.gpu_helpers import decode_planes, to_dev
 pytestmark = pytest.mark.gpu
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
-         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4}
+         "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4,
+         "fp6k3": awe.ENC_FP6K3}
 
 
 def _dtype(lo, hi):
@@ -34,7 +35,7 @@ def _encode(enc, m, side, X, rows, K, flag=None):
 @pytest.mark.parametrize("name", sorted(EXACT))
 @pytest.mark.parametrize("rows,K", [(32, 128), (70, 200), (1, 1), (257, 333)])
 def test_encode_matches_oracle(name, rows, K):
-    s = sc.PAPER_SCHEMES[name]()
+    s = sc.ALL_SCHEMES[name]()
     rng = np.random.default_rng(rows * 1000 + K)
     A = inputs.uniform(rng, (rows, K), *s.range_a, dtype=_dtype(*s.range_a))
     got = _encode(EXACT[name], 0, awe.SIDE_A, A, rows, K)

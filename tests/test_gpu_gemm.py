@@ -15,7 +15,8 @@ from tests.gpu_helpers import to_dev
 
 pytestmark = pytest.mark.gpu
 
-EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4, awe.ENC_TERNARY, awe.ENC_FP8FP4]
+EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4, awe.ENC_TERNARY, awe.ENC_FP8FP4,
+         awe.ENC_FP6K3]
 
 
 def _run_exact(enc, A, B, out=torch.int32):
@@ -60,7 +61,7 @@ def test_extremes():
     M, N, K = 64, 96, 2048
     A, B = inputs.stress_operands(M, N, K, seed=3)
     ref = og.gemm_i64(A, B)
-    for enc in (awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT):
+    for enc in (awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_FP8FP4, awe.ENC_FP6K3):
         assert np.array_equal(_run_exact(enc, A, B).astype(np.int64), ref), enc
     A4 = np.where(A < 0, -8, 7).astype(np.int8)
     assert np.array_equal(_run_exact(awe.ENC_AWE4, A4, B).astype(np.int64), og.gemm_i64(A4, B))
@@ -227,7 +228,8 @@ def test_fp8fp4_4096_sampled():
 
 @pytest.mark.parametrize("cfg,cus", [("5", "12"), ("6", "16")])
 @pytest.mark.parametrize("enc,out", [(awe.ENC_AWE6, torch.int32), (awe.ENC_AWE4, torch.int64),
-                                     (awe.ENC_FP8FP4, torch.int32), (awe.ENC_FP16, torch.int64)])
+                                     (awe.ENC_FP8FP4, torch.int32), (awe.ENC_FP16, torch.int64),
+                                     (awe.ENC_FP6K3, torch.int32)])
 def test_split_last_round(monkeypatch, cfg, cus, enc, out):
     # AWE_GEMM_CUS plans the rounds of workgroups for fewer CUs, so that this shape has a
     # ragged last round (30 tiles on 12 CUs, 20 tiles on 16) whose tiles are split along
@@ -247,3 +249,33 @@ def test_split_last_round(monkeypatch, cfg, cus, enc, out):
     C = awe.matmul_exact(to_dev(A), to_dev(B), enc, out)
     torch.cuda.synchronize()
     assert np.array_equal(C.cpu().numpy().astype(np.int64), ref)
+
+
+@pytest.mark.parametrize("cfg", ["0", "1", "2", "3"])
+def test_every_e2m3_tile_configuration(monkeypatch, cfg):
+    # AWE_GEMM_CFG_E2M3 forces one of the E2M3 tile configurations (256x128 on 8 waves
+    # in 3 or 4 stages, on 4 waves, with 4 k-steps per stage); each must be exact, also
+    # with a forced fold segment of one K_PAD
+    monkeypatch.setenv("AWE_GEMM_CFG_E2M3", cfg)
+    M, N, K = 300, 420, 1100
+    A, B = _operands(awe.ENC_FP6K3, M, N, K, seed=int(cfg) + 70)
+    ref = og.gemm_i64(A, B)
+    assert np.array_equal(_run_exact(awe.ENC_FP6K3, A, B).astype(np.int64), ref)
+    pa, pb = _planes(awe.ENC_FP6K3, 0, A, B)
+    C = torch.empty((M, N), dtype=torch.int64, device="cuda")
+    awe.gemm_planes(awe.ENC_FP6K3, 0, M, N, K, pa, pb, C, N, awe.I64, awe.K_PAD)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy(), ref)
+
+
+def test_fp6k3_8192_sampled():
+    # INT8 x INT8 in 3 E2M3 products at 8192^3 (the benchmark's shape and launch), int32 C,
+    # sampled 128 x 128 tiles plus the four corner tiles
+    M = N = K = 8192
+    A, B = inputs.int8_pair(M, N, K, seed=0)
+    C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_FP6K3, torch.int32)
+    torch.cuda.synchronize()
+    Ch = C.cpu().numpy()
+    for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=1):
+        ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
+        assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)

@@ -40,7 +40,47 @@ def parse():
     p.add_argument("--no-context", action="store_true", help="skip base-13 and INT8 context")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain 1 GiB device copy (the reference for rocprofv3 byte counters)")
+    p.add_argument("--clock-sample", action="store_true",
+                   help="also read the engine clocks and socket power (amd-smi) while the GEMM and the "
+                        "MFMA probes run in a loop")
     return p.parse_args()
+
+
+CLOCK_PHASES = ("gemm", "probe_static", "probe_varied")
+
+
+def start_clock_sampler(tmpdir):
+    """Child process (started before the GPU is touched) that waits for each phase's marker
+    file, lets the load settle for 2 s, reads `amd-smi metric -c -p` once and signals done."""
+    import shutil
+    import subprocess
+
+    smi = "/opt/rocm/bin/amd-smi" if os.path.exists("/opt/rocm/bin/amd-smi") else shutil.which("amd-smi")
+    if not smi:
+        return None
+    lines = []
+    for ph in CLOCK_PHASES:
+        lines.append('for i in $(seq 600); do [ -f "{d}/go_{p}" ] && break; sleep 0.1; done; sleep 2; '
+                     'timeout 20 "{smi}" metric -c -p > "{d}/smi_{p}.txt" 2>&1; touch "{d}/done_{p}"'
+                     .format(d=tmpdir, p=ph, smi=smi))
+    return subprocess.Popen(["bash", "-c", "; ".join(lines)], stdout=subprocess.DEVNULL,
+                            stderr=subprocess.DEVNULL)
+
+
+def read_smi(path):
+    """Mean GFX (per-XCD) engine clock and socket power from an `amd-smi metric -c -p` dump."""
+    import re
+
+    try:
+        text = open(path).read()
+    except OSError:
+        return {"error": "no amd-smi output"}
+    clks = [int(m.group(2)) for m in re.finditer(r"GFX_(\d+):\s*\n\s*CLK:\s*(\d+)\s*MHz", text)]
+    pw = re.search(r"SOCKET_POWER:\s*([\d.]+)\s*W", text)
+    if not clks:
+        return {"error": "no GFX clocks in amd-smi output"}
+    return {"gfx_clock_mhz_mean": round(sum(clks) / len(clks), 1), "gfx_clock_mhz_min": min(clks),
+            "gfx_clock_mhz_max": max(clks), "socket_power_w": float(pw.group(1)) if pw else None}
 
 
 def main():
@@ -49,6 +89,11 @@ def main():
         print("bench.py runs on one GPU only: the library has no multi-GPU path; use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
+    sampler = None
+    if args.clock_sample:
+        import tempfile
+        clock_dir = tempfile.mkdtemp(prefix="awe_clock_")
+        sampler = start_clock_sampler(clock_dir)
     import numpy as np
     import torch
 
@@ -192,9 +237,13 @@ def main():
         line["fp16_12_products"] = fp16_context(dev, M)
         line["ozaki2_int53"] = ozaki2_context(dev)
         probe = mfma_sustained()
-        if probe:
+        if probe and "error" not in probe:
             probe["gemm_frac_of_8_wave_rate"] = round(gemm_tflops / probe["8_waves_per_cu_TFLOPs"], 4)
+            probe["gemm_frac_of_varied_operand_rate"] = round(
+                gemm_tflops / probe["varied_operands_8_waves_per_cu_TFLOPs"], 4)
         line["mfma_sustained"] = probe
+    if sampler is not None:
+        line["clock_under_load"] = clock_under_load(sampler, clock_dir, awe, M, N, K, stream)
     if args.calibrate_copy:
         src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -292,8 +341,9 @@ def ozaki2_context(dev, M=4096, N=4096, K=16384):
 
 def mfma_sustained(iters=20000):
     """Dense FP4 rate of the GEMM's MFMA issued back to back from registers with 8 and
-    with 4 waves per compute unit (libawe_probe.so): the practical ceiling, at the clock
-    the chip holds under full MFMA load, next to the data-sheet peak."""
+    with 4 waves per compute unit (libawe_probe.so), with constant operands and with operands
+    that change between MFMAs: the practical ceilings, at the clock the chip holds under full
+    MFMA load, next to the data-sheet peak."""
     import ctypes
 
     from paper_2609_24519_amd import build as hip_build
@@ -320,6 +370,75 @@ def mfma_sustained(iters=20000):
         if rc != 0:
             return {"error": "HIP error %d" % rc}
         out["%s_8_waves_per_cu_TFLOPs" % name] = round(tf.value, 1)
+    # E2M1 operands that change between MFMAs, as real data does: the matrix unit then draws
+    # more power and the clock falls under the board's power limit (a longer run, so that the
+    # clock has settled)
+    lib.awe_mfma_peak_varied.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    best = 0.0
+    for _ in range(2):
+        tf = ctypes.c_double(0.0)
+        rc = lib.awe_mfma_peak_varied(8, 10 * iters, ctypes.byref(tf))
+        if rc != 0:
+            return {"error": "HIP error %d" % rc}
+        best = tf.value
+    out["varied_operands_8_waves_per_cu_TFLOPs"] = round(best, 1)
+    out["varied_operands_frac_of_peak"] = round(best / FP4_PEAK_TFLOPS, 4)
+    return out
+
+
+def clock_under_load(sampler, d, awe, M, N, K, stream):
+    """Runs the AWE6 GEMM, then the FP4 MFMA probe with constant and with changing operands,
+    each in a loop until the sampler has read the clocks and power under that load."""
+    import ctypes
+
+    import torch
+
+    from paper_2609_24519_amd import build as hip_build
+    from paper_2609_24519_amd import inputs
+
+    out = {}
+    enc = awe.ENC_AWE6
+    A_h, B_h = inputs.int8_pair(M, N, K, seed=0)
+    A = torch.from_numpy(A_h).cuda()
+    B = torch.from_numpy(B_h).cuda()
+    C = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, M, K), dtype=torch.uint8, device="cuda")
+    pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, N, K), dtype=torch.uint8, device="cuda")
+    awe.encode(enc, 0, awe.SIDE_A, A, M, K, K, pa, None, stream)
+    awe.encode(enc, 0, awe.SIDE_B, B, N, K, N, pb, None, stream)
+    lib = ctypes.CDLL(hip_build.PROBE_LIB)
+    for f in (lib.awe_mfma_peak, lib.awe_mfma_peak_varied):
+        f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    for ph in CLOCK_PHASES:
+        open(os.path.join(d, "go_" + ph), "w").close()
+        t0 = time.time()
+        rates = []
+        while not os.path.exists(os.path.join(d, "done_" + ph)) and time.time() - t0 < 90:
+            if ph == "gemm":
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(20):
+                    awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I32, 0, stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                rates.append(6 * 2.0 * M * N * K / (e0.elapsed_time(e1) / 20 * 1e-3) / 1e12)
+            else:
+                tf = ctypes.c_double(0.0)
+                fn = lib.awe_mfma_peak if ph == "probe_static" else lib.awe_mfma_peak_varied
+                if fn(8, 100000, ctypes.byref(tf)) != 0:
+                    break
+                rates.append(tf.value)
+        r = read_smi(os.path.join(d, "smi_" + ph + ".txt"))
+        if rates:
+            r["fp4_TFLOPs"] = round(sum(rates[1:] or rates) / len(rates[1:] or rates), 1)
+            if "gfx_clock_mhz_mean" in r:
+                peak_at_clock = 256 * 16384 * r["gfx_clock_mhz_mean"] * 1e6 / 1e12
+                r["frac_of_peak_at_this_clock"] = round(r["fp4_TFLOPs"] / peak_at_clock, 4)
+        out[ph] = r
+    try:
+        sampler.wait(timeout=30)
+    except Exception:  # noqa: BLE001 - the sampler is best effort
+        sampler.kill()
     return out
 
 

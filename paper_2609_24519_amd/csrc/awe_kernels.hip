@@ -663,6 +663,8 @@ using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps pe
 using Cfg8w64x64k4p2 = Cfg<4, 2, 2, 2, 4, 3, 2>;  // as above, fragments read 2 k-steps ahead
 using Cfg8w64x64e4m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 1>;  // 256 x 128, 8 waves, E4M3 operands
 using Cfg8w64x96k4 = Cfg<4, 2, 2, 3, 4, 2>;         // 256 x 192, 8 waves, 4 k-steps, 2 stages
+using Cfg8w64x96s5 = Cfg<4, 2, 2, 3, 2, 5>;         // 256 x 192, 8 waves, 2 k-steps, 5 stages
+using Cfg8w64x96k4p0 = Cfg<4, 2, 2, 3, 4, 2, 0>;    // as 6, fragments read in place
 // E2M3 operands (3 KiB units of two k-steps)
 using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
 using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
@@ -711,7 +713,7 @@ double rounds(int64_t tiles, int cus) {
 int choose_cfg(int64_t M, int64_t N) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
-  if (forced >= 0 && forced <= 6) return forced;
+  if (forced >= 0 && forced <= 8) return forced;
   const int cus = compute_units();
   const int64_t tm = (M + 255) / 256;
   const double t128 = rounds(tm * ((N + 127) / 128), cus);
@@ -923,6 +925,8 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 4: return launch_tile<Cfg8w64x64k4>(g, L, stream);
     case 5: return launch_tile<Cfg8w64x64k4p2>(g, L, stream);
     case 6: return launch_tile<Cfg8w64x96k4>(g, L, stream);
+    case 7: return launch_tile<Cfg8w64x96s5>(g, L, stream);
+    case 8: return launch_tile<Cfg8w64x96k4p0>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }

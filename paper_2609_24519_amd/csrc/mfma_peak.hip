@@ -32,11 +32,38 @@ __global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float* sink) 
   if (s == 0.125f) sink[blockIdx.x] = s;  // never true in practice; keeps the MFMAs live
 }
 
+// E2M1 MFMAs whose operands change from one MFMA to the next (four A and four B
+// register sets of per-lane pseudo-random codes, cycled), so the matrix unit
+// switches as it does on real data; the constant operands above switch far less and
+// draw less power, which lets the clock stay higher.
+__global__ __launch_bounds__(512) void mfma_varied_kernel(int iters, float* sink) {
+  v16f c[4] = {};
+  v8i a[4], b[4];
+  uint32_t h = 0x9e3779b9u * (threadIdx.x + 1) + 0x85ebca6bu * blockIdx.x;
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      h ^= h << 13; h ^= h >> 17; h ^= h << 5;  // xorshift32
+      a[s][j] = (int)h;
+      h ^= h << 13; h ^= h >> 17; h ^= h << 5;
+      b[s][j] = (int)h;
+    }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int m = 0; m < kMfmaPerIter; ++m)
+      c[m & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[m & 3], b[(m >> 2) & 3], c[m & 3], 4, 4,
+                                                                0, 0x80808080, 0, 0x80808080);
+  }
+  const float s = c[0][0] + c[1][0] + c[2][0] + c[3][0];
+  if (s == 0.125f) sink[blockIdx.x] = s;  // keeps the MFMAs live
+}
+
 }  // namespace
 
 namespace {
 
-template <int FMT>
+template <int FMT, bool kVaried = false>
 int run_peak(int waves_per_cu, int iters, double* tflops) {
   if (waves_per_cu < 1 || waves_per_cu > 8 || iters < 1 || tflops == nullptr) return (int)hipErrorInvalidValue;
   int dev = 0, cus = 0;
@@ -49,13 +76,16 @@ int run_peak(int waves_per_cu, int iters, double* tflops) {
   float ms = 0.f;
   const dim3 grid(cus), block(64 * waves_per_cu);
   if ((e = hipEventCreate(&e0)) == hipSuccess && (e = hipEventCreate(&e1)) == hipSuccess) {
-    hipLaunchKernelGGL(mfma_peak_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
-    e = hipGetLastError();
+    auto launch = [&]() {
+      if (kVaried)
+        hipLaunchKernelGGL(mfma_varied_kernel, grid, block, 0, nullptr, iters, sink);
+      else
+        hipLaunchKernelGGL(mfma_peak_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
+      return hipGetLastError();
+    };
+    e = launch();
     if (e == hipSuccess) e = hipEventRecord(e0, nullptr);
-    if (e == hipSuccess) {
-      hipLaunchKernelGGL(mfma_peak_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
-      e = hipGetLastError();
-    }
+    if (e == hipSuccess) e = launch();
     if (e == hipSuccess) e = hipEventRecord(e1, nullptr);
     if (e == hipSuccess) e = hipEventSynchronize(e1);
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
@@ -76,6 +106,11 @@ int run_peak(int waves_per_cu, int iters, double* tflops) {
 // writes the achieved dense FP4 rate in TFLOP/s.  Returns 0, or a HIP error code.
 extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
   return run_peak<4>(waves_per_cu, iters, tflops);
+}
+
+// As awe_mfma_peak with E2M1 operands that change between MFMAs (realistic switching).
+extern "C" int awe_mfma_peak_varied(int waves_per_cu, int iters, double* tflops) {
+  return run_peak<4, true>(waves_per_cu, iters, tflops);
 }
 
 // As awe_mfma_peak for operand format `fmt` (4 E2M1, 2 E2M3, 0 E4M3).

@@ -40,6 +40,9 @@ def parse():
     p.add_argument("--no-context", action="store_true", help="skip base-13 and INT8 context")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain 1 GiB device copy (the reference for rocprofv3 byte counters)")
+    p.add_argument("--ozaki2-only", type=int, default=0, metavar="CALLS",
+                   help="only run the residue-number-system route (the ozaki2_int53 context) CALLS "
+                        "times and print its timing (for kernel traces of that route)")
     p.add_argument("--clock-sample", action="store_true",
                    help="also read the engine clocks and socket power (amd-smi) while the GEMM and the "
                         "MFMA probes run in a loop")
@@ -104,6 +107,9 @@ def main():
         hip_build.build()
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.ozaki2_only:
+        print(json.dumps({"ozaki2_int53": ozaki2_context(dev, reps=args.ozaki2_only)}), flush=True)
+        return
     M = N = K = args.size
     A_h, B_h = inputs.int8_pair(M, N, K, seed=0)
     A = torch.from_numpy(A_h).to(dev)
@@ -293,7 +299,7 @@ def fp16_context(dev, n):
     return out
 
 
-def ozaki2_context(dev, M=4096, N=4096, K=16384):
+def ozaki2_context(dev, M=4096, N=4096, K=16384, reps=3):
     """The residue route of Sec. 5.3 as the integer layer of Ozaki scheme II: exact product of
     53-bit integer matrices through the 23-modulus FP64-significand set (60 FP4 products),
     awe_gemm_crt end to end (residues, mod-m GEMMs, reconstruction to 128-bit words and the
@@ -322,7 +328,6 @@ def ozaki2_context(dev, M=4096, N=4096, K=16384):
     run()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 3
     e0.record(stream)
     for _ in range(reps):
         run()

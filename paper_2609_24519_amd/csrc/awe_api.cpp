@@ -237,9 +237,12 @@ awe_status rns_setup(const int32_t* moduli, int32_t n, ResidueParams* rp, CrtPar
     for (int j = 0; j < n; ++j) {
       const uint32_t m = (uint32_t)moduli[j];
       rp->m[j] = m;
-      rp->minv[j] = 0xffffffffu / m;
-      rp->p32[j] = (uint32_t)((uint64_t(1) << 32) % m);
-      rp->p64[j] = (uint32_t)(((unsigned __int128)1 << 64) % m);
+      rp->inv[j] = 1.0f / (float)m;
+      rp->dinv[j] = 1.0 / (double)m;
+      rp->w16[j] = (uint32_t)((uint64_t(1) << 16) % m);
+      rp->w32[j] = (uint32_t)((uint64_t(1) << 32) % m);
+      rp->w48[j] = (uint32_t)((uint64_t(1) << 48) % m);
+      rp->negc[j] = (m - (uint32_t)(((unsigned __int128)1 << 64) % m)) % m;
     }
   }
   if (cp) {
@@ -247,16 +250,16 @@ awe_status rns_setup(const int32_t* moduli, int32_t n, ResidueParams* rp, CrtPar
     cp->n = n;
     for (int j = 0; j < n; ++j) {
       const uint32_t m = (uint32_t)moduli[j];
-      cp->m[j] = m;
-      cp->minv[j] = 0xffffffffu / m;
+      cp->mod[j].m = m;
+      cp->mod[j].inv = 1.0f / (float)m;
       uint64_t pj = 1;  // m_0 ... m_{j-1} mod m
       for (int i = 0; i < j; ++i) {
-        cp->c[i][j] = (uint8_t)pj;
+        cp->c[j][i] = (uint8_t)pj;
         pj = pj * (uint32_t)moduli[i] % m;
       }
-      cp->d[j] = inverse_mod((uint32_t)pj, m);
+      cp->mod[j].d = inverse_mod((uint32_t)pj, m);
       const uint32_t most = (uint32_t)(kMaxModuli - 1) * 255u * 255u;  // largest subtracted sum
-      cp->off[j] = (most / m + 1) * m;
+      cp->mod[j].off = (most / m + 1) * m;
     }
     cp->M_lo = (uint64_t)M;
     cp->M_hi = (uint64_t)(M >> 64);

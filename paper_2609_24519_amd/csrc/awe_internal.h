@@ -170,23 +170,29 @@ constexpr int kMaxModuli = AWE_MAX_MODULI;
 struct ResidueParams {
   int32_t n;
   uint32_t m[kMaxModuli];
-  uint32_t minv[kMaxModuli];  // floor((2^32 - 1) / m)
-  uint32_t p32[kMaxModuli];   // 2^32 mod m
-  uint32_t p64[kMaxModuli];   // 2^64 mod m
+  float inv[kMaxModuli];      // 1/m in fp32
+  double dinv[kMaxModuli];    // 1/m in fp64
+  uint32_t w16[kMaxModuli];   // 2^16 mod m
+  uint32_t w32[kMaxModuli];   // 2^32 mod m
+  uint32_t w48[kMaxModuli];   // 2^48 mod m
+  uint32_t negc[kMaxModuli];  // -2^64 mod m, in [0, m)
 };
 awe_status launch_residues(const int64_t* x, int64_t rows, int64_t cols, int64_t ld, int64_t bound,
                            const ResidueParams& P, uint8_t* out, int64_t out_stride, int32_t* flag,
                            hipStream_t stream);
 
-struct CrtParams {
-  int32_t n;
-  uint32_t m[kMaxModuli];
-  uint32_t minv[kMaxModuli];
-  uint32_t d[kMaxModuli];       // (m_0 ... m_{j-1})^-1 mod m_j
-  uint32_t off[kMaxModuli];     // multiple of m_j above any subtracted digit sum
-  uint8_t c[kMaxModuli][kMaxModuli];  // c[i][j] = (m_0 ... m_{i-1}) mod m_j, i < j
+struct CrtModulus {
+  uint32_t m;
+  float inv;     // 1/m in fp32
+  uint32_t d;    // (m_0 ... m_{j-1})^-1 mod m_j
+  uint32_t off;  // multiple of m_j above any subtracted digit sum
+};
+struct alignas(16) CrtParams {
+  uint8_t c[kMaxModuli][kMaxModuli];  // c[j][i] = (m_0 ... m_{i-1}) mod m_j, i < j (row j: digit j's)
+  CrtModulus mod[kMaxModuli];
   uint64_t M_lo, M_hi;          // M = m_0 ... m_{n-1} < 2^127
   uint64_t half_lo, half_hi;    // floor(M / 2)
+  int32_t n;
 };
 awe_status launch_crt(const int32_t* res, int64_t res_stride, int64_t rows, int64_t cols,
                       int64_t ld_res, const CrtParams& P, int64_t* c128, double* c64, int64_t ldc,

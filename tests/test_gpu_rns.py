@@ -31,16 +31,25 @@ def _words_to_ints(c128):
                     dtype=object).reshape(c128.shape[:-1])
 
 
-@pytest.mark.parametrize("shape", [(1, 1), (37, 129), (300, 65), (64, 1000)])
-def test_residues(shape):
-    rows, cols = shape
+@pytest.mark.parametrize("bits", [63, 53])
+@pytest.mark.parametrize("shape", [(1, 1), (37, 129), (300, 65), (64, 1000), (3, 16, 0), (70, 256, 0),
+                                   (5, 48, 16), (4, 40, 8)])
+def test_residues(shape, bits):
+    # (rows, cols[, ld - cols]): ld = cols + 3 reads entry by entry; cols and ld multiples
+    # of 16 take the 16-entry vector path, whose groups of entries below 2^53 in magnitude
+    # take the double-precision route (bits = 53: mostly those, with 2^53 itself and the
+    # int64 ends mixed in)
+    rows, cols = shape[:2]
+    pad = shape[2] if len(shape) > 2 else 3
     # every modulus of the FP64 set, plus the extremes of the allowed range (residues
     # need no coprimality)
     ms = _moduli() + [2, 3, 255, 256]
-    rng = np.random.default_rng(rows * 7 + cols)
-    x = rng.integers(-(1 << 63), (1 << 63) - 1, size=(rows, cols), dtype=np.int64, endpoint=True)
-    x.ravel()[: min(6, x.size)] = [-(1 << 63), (1 << 63) - 1, -1, 0, B53, -B53][: min(6, x.size)]
-    ld = cols + 3
+    rng = np.random.default_rng(rows * 7 + cols + bits)
+    lim = (1 << bits) - 1
+    x = rng.integers(-lim - (bits == 63), lim, size=(rows, cols), dtype=np.int64, endpoint=True)
+    edges = [-(1 << 63), (1 << 63) - 1, -1, 0, B53, -B53, 1 << 53, -(1 << 53)]
+    x.ravel()[: min(len(edges), x.size)] = edges[: min(len(edges), x.size)]
+    ld = cols + pad
     xp = np.zeros((rows, ld), dtype=np.int64)
     xp[:, :cols] = x
     xd = to_dev(xp)
@@ -68,9 +77,12 @@ def test_residues_range_flag():
     assert np.array_equal(out.cpu().numpy(), ocrt.residues(x[0], 13))
 
 
-@pytest.mark.parametrize("moduli", ["fp64", [3, 5, 7], [256, 255, 253, 251]])
+@pytest.mark.parametrize("moduli", ["fp64", "fp64_12", [3, 5, 7], [256, 255, 253, 251], [97], [256, 255],
+                                    [13, 11, 9, 7, 5, 256, 251, 241, 239, 233]])
 def test_crt_reconstruction(moduli):
-    ms = _moduli() if moduli == "fp64" else moduli
+    # 1 to 23 moduli: every digit-group shape of the Horner step (1, 2 or 3 digits in the top
+    # group) and all three kernel widths (up to 8, 16 and 32 moduli)
+    ms = _moduli() if moduli == "fp64" else (_moduli()[:12] if moduli == "fp64_12" else moduli)
     M = ocrt.modulus_product(ms)
     rng = np.random.default_rng(len(ms))
     rows, cols = 33, 70

@@ -49,7 +49,7 @@ def parse():
     return p.parse_args()
 
 
-CLOCK_PHASES = ("gemm", "probe_static", "probe_varied")
+CLOCK_PHASES = ("gemm", "gemm_e2m3", "probe_static", "probe_varied", "probe_varied_e2m3")
 
 
 def start_clock_sampler(tmpdir):
@@ -388,12 +388,22 @@ def mfma_sustained(iters=20000):
         best = tf.value
     out["varied_operands_8_waves_per_cu_TFLOPs"] = round(best, 1)
     out["varied_operands_frac_of_peak"] = round(best / FP4_PEAK_TFLOPS, 4)
+    lib.awe_mfma_peak_varied_fmt.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                             ctypes.POINTER(ctypes.c_double)]
+    for fmt, name in ((2, "e2m3"), (0, "e4m3")):
+        for _ in range(2):
+            tf = ctypes.c_double(0.0)
+            rc = lib.awe_mfma_peak_varied_fmt(fmt, 8, 10 * iters, ctypes.byref(tf))
+            if rc != 0:
+                return {"error": "HIP error %d" % rc}
+        out["%s_varied_operands_8_waves_per_cu_TFLOPs" % name] = round(tf.value, 1)
     return out
 
 
 def clock_under_load(sampler, d, awe, M, N, K, stream):
-    """Runs the AWE6 GEMM, then the FP4 MFMA probe with constant and with changing operands,
-    each in a loop until the sampler has read the clocks and power under that load."""
+    """Runs the AWE6 GEMM, the 3-product E2M3 GEMM, then the MFMA probe with constant and with
+    changing E2M1 operands and with changing E2M3 operands, each in a loop until the sampler has
+    read the clocks and power under that load.  The rates are FP4/FP6 FLOP/s (r 2MNK / t)."""
     import ctypes
 
     import torch
@@ -402,35 +412,46 @@ def clock_under_load(sampler, d, awe, M, N, K, stream):
     from paper_2609_24519_amd import inputs
 
     out = {}
-    enc = awe.ENC_AWE6
     A_h, B_h = inputs.int8_pair(M, N, K, seed=0)
     A = torch.from_numpy(A_h).cuda()
     B = torch.from_numpy(B_h).cuda()
     C = torch.empty((M, N), dtype=torch.int32, device="cuda")
-    pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, M, K), dtype=torch.uint8, device="cuda")
-    pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, N, K), dtype=torch.uint8, device="cuda")
-    awe.encode(enc, 0, awe.SIDE_A, A, M, K, K, pa, None, stream)
-    awe.encode(enc, 0, awe.SIDE_B, B, N, K, N, pb, None, stream)
+    planes = {}
+    for enc in (awe.ENC_AWE6, awe.ENC_FP6K3):
+        pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, M, K), dtype=torch.uint8, device="cuda")
+        pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, N, K), dtype=torch.uint8, device="cuda")
+        awe.encode(enc, 0, awe.SIDE_A, A, M, K, K, pa, None, stream)
+        awe.encode(enc, 0, awe.SIDE_B, B, N, K, N, pb, None, stream)
+        planes[enc] = (pa, pb, awe.get_encoding_info(enc)["r"])
     lib = ctypes.CDLL(hip_build.PROBE_LIB)
     for f in (lib.awe_mfma_peak, lib.awe_mfma_peak_varied):
         f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    lib.awe_mfma_peak_varied_fmt.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                             ctypes.POINTER(ctypes.c_double)]
     for ph in CLOCK_PHASES:
         open(os.path.join(d, "go_" + ph), "w").close()
         t0 = time.time()
         rates = []
         while not os.path.exists(os.path.join(d, "done_" + ph)) and time.time() - t0 < 90:
-            if ph == "gemm":
+            if ph.startswith("gemm"):
+                enc = awe.ENC_FP6K3 if ph == "gemm_e2m3" else awe.ENC_AWE6
+                pa, pb, r = planes[enc]
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
                 for _ in range(20):
                     awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I32, 0, stream)
                 e1.record(stream)
                 torch.cuda.synchronize()
-                rates.append(6 * 2.0 * M * N * K / (e0.elapsed_time(e1) / 20 * 1e-3) / 1e12)
+                rates.append(r * 2.0 * M * N * K / (e0.elapsed_time(e1) / 20 * 1e-3) / 1e12)
             else:
                 tf = ctypes.c_double(0.0)
-                fn = lib.awe_mfma_peak if ph == "probe_static" else lib.awe_mfma_peak_varied
-                if fn(8, 100000, ctypes.byref(tf)) != 0:
+                if ph == "probe_static":
+                    rc = lib.awe_mfma_peak(8, 100000, ctypes.byref(tf))
+                elif ph == "probe_varied":
+                    rc = lib.awe_mfma_peak_varied(8, 100000, ctypes.byref(tf))
+                else:
+                    rc = lib.awe_mfma_peak_varied_fmt(2, 8, 100000, ctypes.byref(tf))
+                if rc != 0:
                     break
                 rates.append(tf.value)
         r = read_smi(os.path.join(d, "smi_" + ph + ".txt"))
@@ -464,10 +485,11 @@ def gemm_traffic():
     return None if k is None else round(k["fetch_bytes"] + k["write_bytes"])
 
 
-def cpu_baseline(A_h, B_h, target_s=10.0):
+def cpu_baseline(A_h, B_h, target_s=15.0):
     """The oracle (plain int64 triple loop, OpenMP over rows) on a bounded sample of
-    the same workload: a block of rows of C over the full N and K, sized from a short
-    calibration run to take about ``target_s`` seconds, scaled to exact TOPS."""
+    the same workload: a block of rows of C over the full N and K, sized from two short
+    calibration runs (the first warms the threads and caches) to take about ``target_s``
+    seconds, scaled to exact TOPS."""
     import numpy as np
 
     from oracle import gemm as og
@@ -476,10 +498,11 @@ def cpu_baseline(A_h, B_h, target_s=10.0):
         og.build()
     K, N = B_h.shape
     threads = og.num_threads()
-    rows = max(threads, 16)
-    t0 = time.perf_counter()
-    og.gemm_i64(np.ascontiguousarray(A_h[:rows]), B_h)
-    dt = time.perf_counter() - t0
+    rows = max(2 * threads, 32)
+    for _ in range(2):
+        t0 = time.perf_counter()
+        og.gemm_i64(np.ascontiguousarray(A_h[:rows]), B_h)
+        dt = time.perf_counter() - t0
     rows = int(min(A_h.shape[0], max(rows, rows * target_s / max(dt, 1e-3))))
     rows = max(threads, rows // threads * threads)
     sub = np.ascontiguousarray(A_h[:rows])

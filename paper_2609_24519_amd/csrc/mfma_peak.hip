@@ -32,11 +32,13 @@ __global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float* sink) 
   if (s == 0.125f) sink[blockIdx.x] = s;  // never true in practice; keeps the MFMAs live
 }
 
-// E2M1 MFMAs whose operands change from one MFMA to the next (four A and four B
+// MFMAs whose operands change from one MFMA to the next (four A and four B
 // register sets of per-lane pseudo-random codes, cycled), so the matrix unit
 // switches as it does on real data; the constant operands above switch far less and
 // draw less power, which lets the clock stay higher.
+template <int FMT>
 __global__ __launch_bounds__(512) void mfma_varied_kernel(int iters, float* sink) {
+  constexpr uint32_t kScale = FMT == 4 ? 0x80808080u : (FMT == 2 ? 0x82828282u : 0x7f7f7f7fu);
   v16f c[4] = {};
   v8i a[4], b[4];
   uint32_t h = 0x9e3779b9u * (threadIdx.x + 1) + 0x85ebca6bu * blockIdx.x;
@@ -52,8 +54,8 @@ __global__ __launch_bounds__(512) void mfma_varied_kernel(int iters, float* sink
   for (int it = 0; it < iters; ++it) {
 #pragma unroll
     for (int m = 0; m < kMfmaPerIter; ++m)
-      c[m & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[m & 3], b[(m >> 2) & 3], c[m & 3], 4, 4,
-                                                                0, 0x80808080, 0, 0x80808080);
+      c[m & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[m & 3], b[(m >> 2) & 3], c[m & 3], FMT,
+                                                                FMT, 0, kScale, 0, kScale);
   }
   const float s = c[0][0] + c[1][0] + c[2][0] + c[3][0];
   if (s == 0.125f) sink[blockIdx.x] = s;  // keeps the MFMAs live
@@ -78,7 +80,7 @@ int run_peak(int waves_per_cu, int iters, double* tflops) {
   if ((e = hipEventCreate(&e0)) == hipSuccess && (e = hipEventCreate(&e1)) == hipSuccess) {
     auto launch = [&]() {
       if (kVaried)
-        hipLaunchKernelGGL(mfma_varied_kernel, grid, block, 0, nullptr, iters, sink);
+        hipLaunchKernelGGL(mfma_varied_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
       else
         hipLaunchKernelGGL(mfma_peak_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
       return hipGetLastError();
@@ -111,6 +113,16 @@ extern "C" int awe_mfma_peak(int waves_per_cu, int iters, double* tflops) {
 // As awe_mfma_peak with E2M1 operands that change between MFMAs (realistic switching).
 extern "C" int awe_mfma_peak_varied(int waves_per_cu, int iters, double* tflops) {
   return run_peak<4, true>(waves_per_cu, iters, tflops);
+}
+
+// As awe_mfma_peak_varied for operand format `fmt` (4 E2M1, 2 E2M3, 0 E4M3).
+extern "C" int awe_mfma_peak_varied_fmt(int fmt, int waves_per_cu, int iters, double* tflops) {
+  switch (fmt) {
+    case 4: return run_peak<4, true>(waves_per_cu, iters, tflops);
+    case 2: return run_peak<2, true>(waves_per_cu, iters, tflops);
+    case 0: return run_peak<0, true>(waves_per_cu, iters, tflops);
+    default: return (int)hipErrorInvalidValue;
+  }
 }
 
 // As awe_mfma_peak for operand format `fmt` (4 E2M1, 2 E2M3, 0 E4M3).

@@ -125,6 +125,12 @@ def _dispatch_counters(paths):
     return out
 
 
+# Engine clock under the GEMM (amd-smi, `bench.py --clock-sample`) and the CU count, for
+# turning per-chip cycle counters into per-CU rates and shares of the kernel's cycles.
+CLOCK_HZ = 2.05e9
+CUS = 256
+
+
 def counters(out_md, fp4_flop, command, paths):
     fp4_flop = float(fp4_flop)
     data = _dispatch_counters(paths)
@@ -161,6 +167,16 @@ def counters(out_md, fp4_flop, command, paths):
             if "TCP_TCC_READ_REQ_LATENCY" in m:
                 lines.append("| mean L2 read latency (cycles) | %.0f |" % (
                     m["TCP_TCC_READ_REQ_LATENCY"] / max(m["TCP_TCC_READ_REQ"], 1.0)))
+                # Little's law: requests in flight = total latency / elapsed cycles
+                cyc = m["_ns"] * 1e-9 * CLOCK_HZ
+                lines.append("| L1 -> L2 reads in flight per CU at %.2f GHz (total latency / cycles / CUs) "
+                             "| %.1f |" % (CLOCK_HZ / 1e9, m["TCP_TCC_READ_REQ_LATENCY"] / cyc / CUS))
+        for c, label in (("TCP_PENDING_STALL_CYCLES", "L1 cycles stalled on pending misses, per CU"),
+                         ("TA_ADDR_STALLED_BY_TC_CYCLES", "address unit cycles stalled by L1, per CU")):
+            if c in m:
+                cyc = m["_ns"] * 1e-9 * CLOCK_HZ
+                lines.append("| %s (%s) | %.4g (%.0f %% of the cycles at %.2f GHz) |" % (
+                    label, c, m[c] / CUS, 100.0 * m[c] / CUS / cyc, CLOCK_HZ / 1e9))
         lines.append("")
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")

@@ -12,8 +12,9 @@ and the CPU-baseline leg of ``bench.py`` may import or execute it.
 * ``schemes`` -- the paper's encodings (storable set, limb tables, planes,
                  reconstruction coefficients, coverage, K*), the scheme
                  identity and the run-time procedure in plain numpy int64;
-                 also the INT8 x INT8 variant in 3 E2M3 (FP6) products that
-                 the Karatsuba threshold of Sec. 3.3 admits.
+                 also the INT8 x INT8 variants in E2M3 (FP6) products: 3 by
+                 the Karatsuba step that Sec. 3.3 admits, and 4 whose limb
+                 weights ride in the E8M0 block scales (Sec. 4.5).
 * ``modm``    -- the congruence (mod m) schemes and their tables.
 * ``crt``     -- residues and the Chinese-remainder reconstruction of a
                  residue number system, in Python integers.

@@ -318,7 +318,44 @@ def fp6k3():
     return s
 
 
-VARIANT_SCHEMES = {"fp6k3": fp6k3}
+def e8m0_value(code):
+    """OCP MX E8M0 scale: 2^(code - 127) for code 0..254 (255 is NaN); powers of two only."""
+    if code == 255:
+        return float("nan")
+    return 2.0 ** (code - 127)
+
+
+def fp6p4():
+    """INT8 x INT8 in 4 E2M3 products with the limb weights in the block scales (Sec. 4.5).
+
+    The same base-16 limbs as fp6k3, x = a0 + 16 a1, but every limb pair is its own product:
+    AB = a0 b0 + 16 a0 b1 + 16 a1 b0 + 256 a1 b1.  The weights are powers of two, which an
+    E8M0 scale represents (Sec. 4.5), so each product's weight 16^(i+j) can ride in the
+    scales of its two operands and all four products add into one FP32 accumulator.
+    """
+    planes = [(1, 0), (0, 1)]
+    prods = [(planes[i], planes[j], 16 ** (i + j)) for i in range(2) for j in range(2)]
+    s = Scheme("fp6p4", (1, 16), (1, 16), prods, 1, 16, 16, INT8_RANGE, INT8_RANGE)
+    s.limb_rule = {"a": fp6k3_limbs, "b": fp6k3_limbs}
+    s.formats_a = s.formats_b = ["e2m3", "e2m3"]
+    return s
+
+
+def shared_accumulator_kstar(s, F=24):
+    """Sec. 3.4's condition for one FP32 accumulator that receives every product with its
+    weight: each reduction index adds at most sum_k |ell_k| c_A(k) c_B(k) in magnitude
+    (c the largest |value| of the product's planes), so partial sums stay exact integers
+    for floor(2^F / that) indices."""
+    _, TA = plane_table(s, "a")
+    _, TB = plane_table(s, "b")
+    ca = np.abs(TA).max(axis=0)
+    cb = np.abs(TB).max(axis=0)
+    per_index = sum(abs(l) * int(ca[s.planes_a.index(a)]) * int(cb[s.planes_b.index(b)])
+                    for a, b, l in s.products)
+    return (2 ** F) // per_index, per_index
+
+
+VARIANT_SCHEMES = {"fp6k3": fp6k3, "fp6p4": fp6p4}
 ALL_SCHEMES = dict(PAPER_SCHEMES, **VARIANT_SCHEMES)
 
 

@@ -304,3 +304,54 @@ def test_fp6k3_mutation_caught(k, delta):
     bad = _mutate_ell(s, k, s.products[k][2] + delta)
     assert not sc.coefficient_identity_holds(bad)
     assert not sc.brute_force_pairs(bad)
+
+
+def test_e8m0_scale_format(paper):
+    # OCP MX E8M0: an exponent with bias 127 and no significand, so powers of two only
+    one, lo, hi, nan = paper["e8m0.codes"]
+    assert sc.e8m0_value(one) == 1.0 and sc.e8m0_value(lo) == 2.0 ** -127 and sc.e8m0_value(hi) == 2.0 ** 127
+    assert sc.e8m0_value(nan) != sc.e8m0_value(nan)
+    values = {sc.e8m0_value(c) for c in range(255)}
+    assert all(v == 2.0 ** round(np.log2(v)) for v in values)
+
+
+def test_weights_in_scales(paper):
+    # Sec. 4.5: a limb weight can ride in an E8M0 scale only if it is a power of two; AWE6's
+    # weights (1, 29, 37) cannot (the paper's example), the base-16 weights of fp6p4 can, with
+    # plane i of each operand carrying 16^i on top of the 2^3 that stores n as n / 8
+    scales = {sc.e8m0_value(c) for c in range(255)}
+    assert [w in scales for w in sc.awe6().w] == [True, False, False]
+    s = sc.fp6p4()
+    for a, b, l in s.products:
+        i, j = a.index(1), b.index(1)
+        sa = sc.e8m0_value(127 + 3 + 4 * i)
+        sb = sc.e8m0_value(127 + 3 + 4 * j)
+        assert sa in scales and sb in scales
+        assert (sa / sc.FP6_SCALE) * (sb / sc.FP6_SCALE) == l
+
+
+def test_fp6p4_scheme():
+    s = sc.fp6p4()
+    assert s.r == 4 and s.planes_a == [(1, 0), (0, 1)]
+    assert sc.coefficient_identity_holds(s)
+    assert sc.brute_force_pairs(s)  # all 65,536 int8 pairs
+    # one shared accumulator: each reduction index adds at most (8 + 16*8)^2 = 18496, which
+    # the input pair x = y = 120 (a0 = -8, a1 = 8) attains; K* = floor(2^24 / 18496)
+    kstar, per_index = sc.shared_accumulator_kstar(s)
+    assert (kstar, per_index) == (907, 136 * 136)
+    lo, TA = sc.plane_table(s, "a")
+    terms = sum(abs(l) * np.outer(np.abs(TA[:, s.planes_a.index(a)]), np.abs(TA[:, s.planes_a.index(b)]))
+                for a, b, l in s.products)
+    assert terms.max() == per_index and terms[120 - lo, 120 - lo] == per_index
+    rng = np.random.default_rng(13)
+    A = rng.integers(-128, 127, (9, 70), endpoint=True)
+    B = rng.integers(-128, 127, (70, 6), endpoint=True)
+    assert np.array_equal(sc.scheme_gemm(s, A, B), A @ B)
+
+
+@pytest.mark.parametrize("k", range(4))
+def test_fp6p4_mutation_caught(k):
+    s = sc.fp6p4()
+    bad = _mutate_ell(s, k, 2 * s.products[k][2])
+    assert not sc.coefficient_identity_holds(bad)
+    assert not sc.brute_force_pairs(bad)

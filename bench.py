@@ -49,7 +49,7 @@ def parse():
     return p.parse_args()
 
 
-CLOCK_PHASES = ("gemm", "gemm_e2m3", "probe_static", "probe_varied", "probe_varied_e2m3")
+CLOCK_PHASES = ("gemm", "gemm_e2m3", "gemm_e2m3_scaled", "probe_static", "probe_varied", "probe_varied_e2m3")
 
 
 def start_clock_sampler(tmpdir):
@@ -222,6 +222,17 @@ def main():
             "gemm_exact_TOPS": round(ops / (sgemm_ms * 1e-3) / 1e12, 2),
             "fp6_TFLOPs": round(sinfo["r"] * ops / (sgemm_ms * 1e-3) / 1e12, 1),
             "fp6_peak_frac": round(sinfo["r"] * ops / (sgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
+        # the same limbs with the weights in the block scales (Sec. 4.5): 4 E2M3 products into
+        # one accumulator, each stage bringing both planes of each side once
+        pinfo, pwall, penc_ms, pgemm_ms = run(awe.ENC_FP6P4, max(3, args.steps // 2), 2)
+        line["fp6p4_4_fp6_products_weights_in_scales"] = {
+            "ms_per_step": round(pwall / max(3, args.steps // 2) * 1e3, 4),
+            "exact_TOPS": round(ops / (pwall / max(3, args.steps // 2)) / 1e12, 2),
+            "encode_ms": round(penc_ms, 4),
+            "gemm_ms": round(pgemm_ms, 4),
+            "gemm_exact_TOPS": round(ops / (pgemm_ms * 1e-3) / 1e12, 2),
+            "fp6_TFLOPs": round(pinfo["r"] * ops / (pgemm_ms * 1e-3) / 1e12, 1),
+            "fp6_peak_frac": round(pinfo["r"] * ops / (pgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
         # {0, +-1} x INT8 (Sec. 6.2) on the same B: 3 products
         At = torch.from_numpy(inputs.int8_pair(M, 8, K, seed=5, a_range=(-1, 1))[0]).to(dev)
         tinfo, pta, ptb = setup(awe.ENC_TERNARY)
@@ -401,9 +412,10 @@ def mfma_sustained(iters=20000):
 
 
 def clock_under_load(sampler, d, awe, M, N, K, stream):
-    """Runs the AWE6 GEMM, the 3-product E2M3 GEMM, then the MFMA probe with constant and with
-    changing E2M1 operands and with changing E2M3 operands, each in a loop until the sampler has
-    read the clocks and power under that load.  The rates are FP4/FP6 FLOP/s (r 2MNK / t)."""
+    """Runs the AWE6 GEMM, the 3-product E2M3 GEMM, the 4-product E2M3 GEMM with the weights in
+    the scales, then the MFMA probe with constant and with changing E2M1 operands and with
+    changing E2M3 operands, each in a loop until the sampler has read the clocks and power under
+    that load.  The rates are FP4/FP6 FLOP/s (r 2MNK / t)."""
     import ctypes
 
     import torch
@@ -417,7 +429,7 @@ def clock_under_load(sampler, d, awe, M, N, K, stream):
     B = torch.from_numpy(B_h).cuda()
     C = torch.empty((M, N), dtype=torch.int32, device="cuda")
     planes = {}
-    for enc in (awe.ENC_AWE6, awe.ENC_FP6K3):
+    for enc in (awe.ENC_AWE6, awe.ENC_FP6K3, awe.ENC_FP6P4):
         pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, M, K), dtype=torch.uint8, device="cuda")
         pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, N, K), dtype=torch.uint8, device="cuda")
         awe.encode(enc, 0, awe.SIDE_A, A, M, K, K, pa, None, stream)
@@ -434,7 +446,7 @@ def clock_under_load(sampler, d, awe, M, N, K, stream):
         rates = []
         while not os.path.exists(os.path.join(d, "done_" + ph)) and time.time() - t0 < 90:
             if ph.startswith("gemm"):
-                enc = awe.ENC_FP6K3 if ph == "gemm_e2m3" else awe.ENC_AWE6
+                enc = {"gemm_e2m3": awe.ENC_FP6K3, "gemm_e2m3_scaled": awe.ENC_FP6P4}.get(ph, awe.ENC_AWE6)
                 pa, pb, r = planes[enc]
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(stream)

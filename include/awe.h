@@ -97,10 +97,15 @@ typedef enum awe_encoding {
   AWE_ENC_FP8FP4 = 8,  /* INT8 x INT8 with 2 FP8 (E4M3) products and 1 FP4 product (App. A):
                           A = 13 h + 5 eps, planes h, h + eps (E4M3, 2 KiB bricks, see the
                           layout above) and eps (E2M1); AB = 104 P1 + 65 P2 - 40 P3. */
-  AWE_ENC_FP6K3 = 9    /* INT8 x INT8 in 3 E2M3 (FP6) products: A = a0 + 16 a1 with a0 in [-8, 7],
+  AWE_ENC_FP6K3 = 9,   /* INT8 x INT8 in 3 E2M3 (FP6) products: A = a0 + 16 a1 with a0 in [-8, 7],
                           planes a0, a1, a0 + a1 (within [-15, 15], inside E2M3's contiguous
                           integer range, the Karatsuba condition of Sec. 3.3);
                           AB = -15 P1 + 240 P2 + 16 P3.  Not a catalogued scheme of the paper. */
+  AWE_ENC_FP6P4 = 10   /* INT8 x INT8 in 4 E2M3 products with the limb weights in the block scales
+                          (Sec. 4.5): the limbs of AWE_ENC_FP6K3, planes a0 and a1, every limb pair
+                          a product, AB = a0 b0 + 16 (a0 b1 + a1 b0) + 256 a1 b1; plane i's E8M0
+                          scale carries 16^i, so the four products add into one FP32 accumulator
+                          (K* = floor(2^24 / 136^2) = 907).  Not a catalogued scheme. */
 } awe_encoding;
 
 typedef enum awe_side { AWE_SIDE_A = 0, AWE_SIDE_B = 1 } awe_side;

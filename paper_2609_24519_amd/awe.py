@@ -20,11 +20,11 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "awe.h")
 OK, ERR_INVALID_VALUE, ERR_UNSUPPORTED, ERR_OVERFLOW, ERR_WORKSPACE, ERR_HIP, ERR_TABLE = range(7)
 _FORMATS = ("e2m1", "e4m3", "e2m3")  # element format codes of awe_encoding_info
 # awe_encoding
-ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY, ENC_FP16, ENC_FP8FP4, ENC_FP6K3 = \
-    1, 2, 3, 4, 5, 6, 7, 8, 9
+ENC_B13, ENC_AWE6, ENC_AWE6ALT, ENC_AWE4, ENC_MOD, ENC_TERNARY, ENC_FP16, ENC_FP8FP4, ENC_FP6K3, \
+    ENC_FP6P4 = 1, 2, 3, 4, 5, 6, 7, 8, 9, 10
 ENCODINGS = {"b13": ENC_B13, "awe6": ENC_AWE6, "awe6_alt": ENC_AWE6ALT, "awe4": ENC_AWE4, "mod": ENC_MOD,
              "ternary": ENC_TERNARY, "fp16_12": ENC_FP16, "fp8fp4": ENC_FP8FP4,
-             "fp6k3": ENC_FP6K3}
+             "fp6k3": ENC_FP6K3, "fp6p4": ENC_FP6P4}
 # awe_side, awe_dtype
 SIDE_A, SIDE_B = 0, 1
 I32, I64 = 0, 1

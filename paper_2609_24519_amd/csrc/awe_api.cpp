@@ -118,7 +118,21 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
       L.k_seg = own_seg ? s.lkseg[g] : k_seg;
       L.r = 0;
       L.fold_mask = 0;
-      for (int k = 0; k < s.r; ++k) {
+      L.shared = s.scale_weights;
+      if (L.shared) {
+        // one pass over the reduction: each stage brings both planes of each side and runs
+        // the four pair products into one accumulator, the weights in the scales (2^3 stores
+        // n as n/8 in E2M3, 2^sexp is the plane's weight); folded with coefficient 1
+        for (int k = 0; k < 2; ++k) {
+          L.scale_a[k] = 0x01010101u * (uint32_t)(127 + 3 + s.sexp_a[k]);
+          L.scale_b[k] = 0x01010101u * (uint32_t)(127 + 3 + s.sexp_b[k]);
+        }
+        L.r = 1;
+        L.pa[0] = L.pb[0] = 0;
+        L.fold_ell[0] = 1;
+        L.fold_mask = 1;
+      }
+      for (int k = 0; k < s.r && !L.shared; ++k) {
         if (s.lgroup[k] != g) continue;
         L.pa[L.r] = s.pa[k] - first_a;
         L.pb[L.r] = s.pb[k] - first_b;

@@ -65,6 +65,11 @@ struct Scheme {
   bool positional13_a = false, positional13_b = false;  // base-13 digits with carries instead of the choice rule
   bool a_unsigned = false, b_unsigned = false;  // residues arrive as uint8
   bool wide = false;  // int16 inputs; tables indexed by x - xmin instead of the input byte
+  // Limb weights in the block scales (Sec. 4.5): plane k of a side carries 2^sexp in its
+  // E8M0 scale, every product's ell_k = 2^(sexp_a + sexp_b), and all products add into one
+  // FP32 accumulator (two planes per side, one launch, fold coefficient 1).
+  bool scale_weights = false;
+  int sexp_a[kMaxPlanes] = {}, sexp_b[kMaxPlanes] = {};
   int planes8(bool sideA) const {  // leading E4M3 planes
     int n = 0;
     while (n < (sideA ? na : nb) && (sideA ? fmt_a : fmt_b)[n]) ++n;
@@ -152,6 +157,8 @@ struct GemmLaunch {
   int32_t fold_ell[kMaxProducts];  // coefficient applied when the accumulator is folded after product k
   int64_t outer;                   // the launch adds outer * (sum / D) into C
   uint8_t fmt;                     // element format of both operands' planes (kFmt*)
+  bool shared;                     // two planes per side, every pair one product, one accumulator
+  uint32_t scale_a[2], scale_b[2]; // shared: E8M0 scale byte of plane 0 / 1, replicated 4 times
   uint32_t fold_mask;              // bit k: fold after product k
   int64_t k_seg;                   // fold segment length (multiple of kKPad)
   int64_t k_begin, k_end;          // reduction range of this launch (multiples of kKPad)

@@ -6,6 +6,7 @@
 #include <cstdlib>
 #include <map>
 #include <mutex>
+#include <set>
 #include <string>
 
 #include "awe_internal.h"
@@ -221,7 +222,8 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 // ---------------------------------------------------------------------------
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
-template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0>
+template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0,
+          int NPL_ = 1>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
   static constexpr int KST = KST_;        // k-steps (64 reduction indices each) per stage
@@ -246,8 +248,15 @@ struct Cfg {
   static constexpr int NW = WM * WN;
   static constexpr int THREADS = 64 * NW;
   static constexpr int BM = WM * BMW * 32, BN = WN * BNW * 32;
-  static constexpr int A_UNITS = (BM / kBrickRows) * KU;  // per stage: row blocks x units
-  static constexpr int B_UNITS = (BN / kBrickRows) * KU;
+  // Planes per side in a stage: 1 (one product's planes, product-major stream), or 2 (both
+  // planes of each side; every pair is a product, its weight in the E8M0 scales, all four
+  // into one accumulator).
+  static constexpr int NPL = NPL_;
+  static_assert(NPL == 1 || (NPL == 2 && FMT == 2), "two planes per side: E2M3 with weights in the scales");
+  static constexpr int PA_UNITS = (BM / kBrickRows) * KU;  // per plane and stage: row blocks x units
+  static constexpr int PB_UNITS = (BN / kBrickRows) * KU;
+  static constexpr int A_UNITS = NPL * PA_UNITS;
+  static constexpr int B_UNITS = NPL * PB_UNITS;
   static constexpr int STAGE_BYTES = (A_UNITS + B_UNITS) * UNIT_BYTES;
   static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES;
   // copies per wave and stage: A units evenly, B units round-robin (the first
@@ -276,6 +285,7 @@ struct GemmArgs {
   int32_t c64, accumulate, log2D, modulus;
   int32_t tiles_m, tiles_n;
   int64_t outer;  // C (+)= outer * (sum / D)
+  uint32_t sa[2], sb[2];  // two planes per side: E8M0 scale word of plane 0 / 1 of A and B
   // Tiles n_full .. tiles_m * tiles_n - 1 (the ragged last round of workgroups) are
   // each computed by `split` workgroups over consecutive parts of the reduction range,
   // which add their exact partial results into C (zeroed beforehand) with atomics.
@@ -350,20 +360,22 @@ __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, u
 #pragma unroll
   for (int i = 0; i < C::A_PW; ++i) {
     const int id = wave * C::A_PW + i;
-    const int rb = min(tm * (C::BM / kBrickRows) + id / C::KU, g.rba - 1);
+    const int pl = id / C::PA_UNITS, r = id % C::PA_UNITS;  // plane of the stage, unit in it
+    const int rb = min(tm * (C::BM / kBrickRows) + r / C::KU, g.rba - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pa + ((int64_t)(id % C::KU) * g.rba + rb) * UB + h * kBrickBytes, voff,
+      dma_brick(pa + pl * g.stride_a + ((int64_t)(r % C::KU) * g.rba + rb) * UB + h * kBrickBytes, voff,
                 stage_lds + id * UB + h * kBrickBytes);
   }
 #pragma unroll
   for (int i = 0; i < C::B_LO + (C::B_XTRA ? 1 : 0); ++i) {
     const int id = wave + i * C::NW;
     if (i == C::B_LO && wave >= C::B_XTRA) break;
-    const int cb = min(tn * (C::BN / kBrickRows) + id / C::KU, g.rbb - 1);
+    const int pl = id / C::PB_UNITS, r = id % C::PB_UNITS;
+    const int cb = min(tn * (C::BN / kBrickRows) + r / C::KU, g.rbb - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pb + ((int64_t)(id % C::KU) * g.rbb + cb) * UB + h * kBrickBytes, voff,
+      dma_brick(pb + pl * g.stride_b + ((int64_t)(r % C::KU) * g.rbb + cb) * UB + h * kBrickBytes, voff,
                 stage_lds + (C::A_UNITS + id) * UB + h * kBrickBytes);
   }
 }
@@ -407,7 +419,7 @@ __device__ __forceinline__ v8i frag_fmt(const uint8_t* unit, int i, int lane) {
 // The wave's operand fragments for one k-step (64 reduction indices) of a stage.
 template <class C>
 struct Frags {
-  v8i a[C::BMW], b[C::BNW];
+  v8i a[C::NPL * C::BMW], b[C::NPL * C::BNW];  // plane pl's fragments at pl * BMW (pl * BNW)
 };
 
 template <class C>
@@ -415,11 +427,16 @@ __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, in
                                            int wn, int lane) {
   const int u = ks / C::UK, i = ks % C::UK;
 #pragma unroll
-  for (int ia = 0; ia < C::BMW; ++ia)
-    f.a[ia] = frag_fmt<C::FMT>(stage + ((wm * C::BMW + ia) * C::KU + u) * C::UNIT_BYTES, i, lane);
+  for (int pl = 0; pl < C::NPL; ++pl) {
 #pragma unroll
-  for (int j = 0; j < C::BNW; ++j)
-    f.b[j] = frag_fmt<C::FMT>(stage + (C::A_UNITS + (wn * C::BNW + j) * C::KU + u) * C::UNIT_BYTES, i, lane);
+    for (int ia = 0; ia < C::BMW; ++ia)
+      f.a[pl * C::BMW + ia] = frag_fmt<C::FMT>(
+          stage + (pl * C::PA_UNITS + (wm * C::BMW + ia) * C::KU + u) * C::UNIT_BYTES, i, lane);
+#pragma unroll
+    for (int j = 0; j < C::BNW; ++j)
+      f.b[pl * C::BNW + j] = frag_fmt<C::FMT>(
+          stage + (C::A_UNITS + pl * C::PB_UNITS + (wn * C::BNW + j) * C::KU + u) * C::UNIT_BYTES, i, lane);
+  }
 }
 
 __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
@@ -595,17 +612,30 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
             read_frags<C>(f[kr % NSETS], smem + nbuf * C::STAGE_BYTES, kr - C::KST, wm, wn, lane);
           __builtin_amdgcn_sched_barrier(0);
           const Frags<C>& cur = f[ks % NSETS];
+          if constexpr (C::NPL == 2) {
+            // the four plane pairs, each block's MFMAs four apart in issue order
 #pragma unroll
-          for (int i = 0; i < C::BMW; ++i)
+            for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int j = 0; j < C::BNW; ++j) {
-              if constexpr (C::FMT == 0)
-                mfma_block(acc[i][j], cur.a[i], cur.b[j]);
-              else if constexpr (C::FMT == 1)
-                mfma_block8(acc[i][j], cur.a[i], cur.b[j]);
-              else
-                mfma_block6(acc[i][j], cur.a[i], cur.b[j]);
-            }
+              for (int i = 0; i < C::BMW; ++i)
+#pragma unroll
+                for (int j = 0; j < C::BNW; ++j)
+                  acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                      cur.a[(q >> 1) * C::BMW + i], cur.b[(q & 1) * C::BNW + j], acc[i][j], 2, 2, 0,
+                      (int)g.sa[q >> 1], 0, (int)g.sb[q & 1]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < C::BMW; ++i)
+#pragma unroll
+              for (int j = 0; j < C::BNW; ++j) {
+                if constexpr (C::FMT == 0)
+                  mfma_block(acc[i][j], cur.a[i], cur.b[j]);
+                else if constexpr (C::FMT == 1)
+                  mfma_block8(acc[i][j], cur.a[i], cur.b[j]);
+                else
+                  mfma_block6(acc[i][j], cur.a[i], cur.b[j]);
+              }
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
         if constexpr (PD == 0) {
@@ -626,7 +656,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
           for (int j = 0; j < C::BNW; ++j) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-              iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
+              // (two planes per side: the weights are in the scales, the partial may use
+              // all 24 bits, and it is added unmultiplied)
+              if constexpr (C::NPL == 2)
+                iacc[i][j][v] += (int32_t)acc[i][j][v];
+              else
+                iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
               acc[i][j][v] = 0.0f;
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -671,6 +706,9 @@ using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k
 using Cfg4w128x64e2m3 = Cfg<2, 2, 4, 2, 2, 3, 1, 2>;  // 256 x 128, 4 waves, 2 k-steps, 3 stages
 using Cfg8w64x64k4e2m3 = Cfg<4, 2, 2, 2, 4, 2, 1, 2>; // 256 x 128, 8 waves, 4 k-steps, 2 stages
 using Cfg8w64x96p0e2m3 = Cfg<4, 2, 2, 3, 2, 3, 0, 2>; // 256 x 192, 8 waves, fragments read in place
+// E2M3, two planes per side with the weights in the scales (4 products, one accumulator)
+using Cfg8w64x64sh = Cfg<4, 2, 2, 2, 2, 2, 1, 2, 2>;    // 256 x 128, 8 waves, 2 k-steps, 2 stages
+using Cfg8w64x64shp0 = Cfg<4, 2, 2, 2, 2, 2, 0, 2, 2>;  // as above, fragments read in place
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;
@@ -768,15 +806,22 @@ awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
       return AWE_ERR_HIP;
     }
   }
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<C>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+  {
+    // the LDS ring exceeds the default dynamic LDS limit: raise it once per device
+    static std::mutex mu;
+    static std::set<int> done;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    std::lock_guard<std::mutex> lk(mu);
+    if (e == hipSuccess && !done.count(dev)) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<C>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+      if (e == hipSuccess) done.insert(dev);
+    }
     if (e != hipSuccess) {
       set_error(std::string("gemm LDS attribute: ") + hipGetErrorString(e));
       return AWE_ERR_HIP;
     }
-    attr_set = true;
   }
   hipLaunchKernelGGL(gemm_kernel<C>, dim3((unsigned)blocks), dim3(C::THREADS), C::LDS_BYTES, stream, g);
   hipError_t err = hipGetLastError();
@@ -909,6 +954,16 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   g.modulus = L.modulus;
   g.outer = L.outer;
   if (L.fmt == kFmtE4M3) return launch_tile<Cfg8w64x64e4m3>(g, L, stream);
+  if (L.shared) {
+    for (int k = 0; k < 2; ++k) {
+      g.sa[k] = L.scale_a[k];
+      g.sb[k] = L.scale_b[k];
+    }
+    // AWE_GEMM_CFG_SHARED: 1 reads each k-step's fragments in place
+    const char* e = getenv("AWE_GEMM_CFG_SHARED");
+    if (e && atoi(e) == 1) return launch_tile<Cfg8w64x64shp0>(g, L, stream);
+    return launch_tile<Cfg8w64x64sh>(g, L, stream);
+  }
   if (L.fmt == kFmtE2M3) {
     switch (choose_cfg_e2m3()) {
       case 1: return launch_tile<Cfg8w64x64s4e2m3>(g, L, stream);

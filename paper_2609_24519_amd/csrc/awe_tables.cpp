@@ -247,6 +247,37 @@ void define_fp6k3(Scheme& s) {
   s.xmax_a = s.xmax_b = 127;
 }
 
+// INT8 x INT8 in 4 E2M3 products with the limb weights in the block scales (Sec. 4.5):
+// the limbs of define_fp6k3, planes a0 and a1, every pair (i, j) a product with weight
+// 16^(i+j) = 2^(4 i) 2^(4 j), so plane i's scale carries 2^(4 i).
+void define_fp6p4(Scheme& s) {
+  s.p = s.q = 2;
+  s.w[0] = s.v[0] = 1;
+  s.w[1] = s.v[1] = 16;
+  s.na = s.nb = 2;
+  for (auto* pl : {&s.alpha, &s.beta}) {
+    set_plane(*pl, 0, {1, 0});
+    set_plane(*pl, 1, {0, 1});
+  }
+  for (int k = 0; k < 2; ++k) {
+    s.fmt_a[k] = s.fmt_b[k] = kFmtE2M3;
+    s.sexp_a[k] = s.sexp_b[k] = 4 * k;
+  }
+  s.r = 4;
+  for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 2; ++j) {
+      s.pa[2 * i + j] = i;
+      s.pb[2 * i + j] = j;
+      s.ell[2 * i + j] = int64_t(1) << (4 * (i + j));
+    }
+  s.lfmt[0] = kFmtE2M3;
+  s.scale_weights = true;
+  s.limb_rule = kRuleBase16;
+  s.cap_a = s.cap_b = 16;
+  s.xmin_a = s.xmin_b = -128;
+  s.xmax_a = s.xmax_b = 127;
+}
+
 // ---- limb tuples ----------------------------------------------------------
 struct Tuple {
   int a[kMaxLimbs];
@@ -481,7 +512,30 @@ bool check_identity(const Scheme& s, std::string* msg) {
   return true;
 }
 
+// Largest |value| of plane k over the table's inputs.
+int plane_cap(const Scheme& s, bool sideA, int k) {
+  int c = 0;
+  for (int b = 0; b < s.table_size(sideA); ++b)
+    if (!((sideA ? s.lut_a : s.lut_b)[b] & kLutInvalid))
+      c = std::max(c, std::abs((sideA ? s.val_a : s.val_b)[b][k]));
+  return c;
+}
+
 void derive_bounds(Scheme& s) {
+  if (s.scale_weights) {
+    // One FP32 accumulator receives every product with its weight (Sec. 3.4 for a shared,
+    // weighted accumulator): a reduction index adds at most sum_k ell_k c_A(k) c_B(k).  The
+    // fold adds the accumulator into int32 unmultiplied, so 2^24 is the only bound.
+    int64_t per_index = 0;
+    for (int k = 0; k < s.r; ++k)
+      per_index += std::abs(s.ell[k]) * plane_cap(s, true, s.pa[k]) * plane_cap(s, false, s.pb[k]);
+    s.n_g = s.r;
+    for (int k = 0; k < s.r; ++k) s.group[k] = 0;
+    s.k_star = (int64_t(1) << 24) / per_index;
+    s.k_seg = s.k_star / kKPad * kKPad;
+    s.lkseg[0] = s.k_seg;
+    return;
+  }
   // products with equal coefficients that are adjacent share one accumulator (n_g, Sec. 3.4)
   int g = -1, run = 0;
   s.n_g = 1;
@@ -553,7 +607,26 @@ bool check_launch_groups(const Scheme& s, std::string* msg) {
   return true;
 }
 
+// Weights in the scales: every product's ell_k must be 2^(sexp_a + sexp_b) of its planes,
+// each side two E2M3 planes, every pair of them a product (the kernel's shared mode).
+bool check_scale_weights(const Scheme& s, std::string* msg) {
+  if (!s.scale_weights) return true;
+  if (s.na != 2 || s.nb != 2 || s.r != 4 || s.n_lgroups != 1 || s.fmt_a[0] != kFmtE2M3) {
+    *msg = "weights in scales need two E2M3 planes per side and all four pairs";
+    return false;
+  }
+  for (int k = 0; k < s.r; ++k) {
+    const int e = s.sexp_a[s.pa[k]] + s.sexp_b[s.pb[k]];
+    if (s.pa[k] != k / 2 || s.pb[k] != k % 2 || e < 0 || e > 24 || s.ell[k] != (int64_t(1) << e)) {
+      *msg = "a product's weight is not the product of its planes' scale factors";
+      return false;
+    }
+  }
+  return true;
+}
+
 bool finish(Scheme& s, std::string* msg) {
+  if (!check_scale_weights(s, msg)) return false;
   if (!build_side(s, true, msg) || !build_side(s, false, msg)) return false;
   if (!check_identity(s, msg)) return false;
   if (!check_launch_groups(s, msg)) return false;
@@ -711,7 +784,7 @@ int64_t plane_stride_bytes(int64_t rows, int64_t K) {
 }
 
 const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std::string* msg) {
-  if (enc < AWE_ENC_B13 || enc > AWE_ENC_FP6K3) {
+  if (enc < AWE_ENC_B13 || enc > AWE_ENC_FP6P4) {
     *st = AWE_ERR_INVALID_VALUE;
     *msg = "unknown encoding";
     return nullptr;
@@ -746,6 +819,7 @@ const Scheme* get_scheme(awe_encoding enc, int32_t modulus, awe_status* st, std:
     case AWE_ENC_FP16: define_fp16(*s); break;
     case AWE_ENC_FP8FP4: define_fp8fp4(*s); break;
     case AWE_ENC_FP6K3: define_fp6k3(*s); break;
+    case AWE_ENC_FP6P4: define_fp6p4(*s); break;
     case AWE_ENC_MOD:
       ok = define_mod(*s, modulus, &m);
       if (!ok) fail = AWE_ERR_UNSUPPORTED;

@@ -17,7 +17,7 @@ from paper_2609_24519_amd import awe
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
          "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4,
-         "fp6k3": awe.ENC_FP6K3}
+         "fp6k3": awe.ENC_FP6K3, "fp6p4": awe.ENC_FP6P4}
 
 
 @lru_cache(maxsize=None)
@@ -52,10 +52,16 @@ def test_encoding_info_matches_oracle(name):
     assert [info["beta"][k] for k in info["pair_b"]] == [b for _, b, _ in s.products]
     c_a, c_b = sc.stored_cap(s, "a"), sc.stored_cap(s, "b")
     assert (info["c_a"], info["c_b"]) == (c_a, c_b)
-    assert info["n_g"] == s.n_g
-    assert info["k_star"] == sc.k_star(s.n_g, c_a, c_b)
-    assert info["k_seg"] % awe.K_PAD == 0 and 0 < info["k_seg"] <= info["k_star"]
-    assert info["k_seg"] * s.n_g * c_a * c_b < 2 ** 23
+    if name == "fp6p4":  # weights in the scales: one accumulator for all products
+        kstar, per_index = sc.shared_accumulator_kstar(s)
+        assert info["n_g"] == s.r and info["k_star"] == kstar
+        assert 0 < info["k_seg"] <= kstar and info["k_seg"] % awe.K_PAD == 0
+        assert info["k_seg"] * per_index <= 2 ** 24
+    else:
+        assert info["n_g"] == s.n_g
+        assert info["k_star"] == sc.k_star(s.n_g, c_a, c_b)
+        assert info["k_seg"] % awe.K_PAD == 0 and 0 < info["k_seg"] <= info["k_star"]
+        assert info["k_seg"] * s.n_g * c_a * c_b < 2 ** 23
     assert info["range_a"] == s.range_a and info["range_b"] == s.range_b
     assert info["formats_a"] == (s.formats_a or ["e2m1"] * len(s.planes_a))
     assert info["formats_b"] == (s.formats_b or ["e2m1"] * len(s.planes_b))

@@ -12,7 +12,7 @@ pytestmark = pytest.mark.gpu
 
 EXACT = {"b13": awe.ENC_B13, "awe6": awe.ENC_AWE6, "awe6_alt": awe.ENC_AWE6ALT, "awe4": awe.ENC_AWE4,
          "ternary": awe.ENC_TERNARY, "fp16_12": awe.ENC_FP16, "fp8fp4": awe.ENC_FP8FP4,
-         "fp6k3": awe.ENC_FP6K3}
+         "fp6k3": awe.ENC_FP6K3, "fp6p4": awe.ENC_FP6P4}
 
 
 def _dtype(lo, hi):

@@ -16,7 +16,7 @@ from tests.gpu_helpers import to_dev
 pytestmark = pytest.mark.gpu
 
 EXACT = [awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_AWE4, awe.ENC_TERNARY, awe.ENC_FP8FP4,
-         awe.ENC_FP6K3]
+         awe.ENC_FP6K3, awe.ENC_FP6P4]
 
 
 def _run_exact(enc, A, B, out=torch.int32):
@@ -61,7 +61,7 @@ def test_extremes():
     M, N, K = 64, 96, 2048
     A, B = inputs.stress_operands(M, N, K, seed=3)
     ref = og.gemm_i64(A, B)
-    for enc in (awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_FP8FP4, awe.ENC_FP6K3):
+    for enc in (awe.ENC_B13, awe.ENC_AWE6, awe.ENC_AWE6ALT, awe.ENC_FP8FP4, awe.ENC_FP6K3, awe.ENC_FP6P4):
         assert np.array_equal(_run_exact(enc, A, B).astype(np.int64), ref), enc
     A4 = np.where(A < 0, -8, 7).astype(np.int8)
     assert np.array_equal(_run_exact(awe.ENC_AWE4, A4, B).astype(np.int64), og.gemm_i64(A4, B))
@@ -90,6 +90,8 @@ def _planes(enc, m, A, B):
 @pytest.mark.parametrize("enc", EXACT)
 @pytest.mark.parametrize("kseg", [awe.K_PAD, 2 * awe.K_PAD, 4 * awe.K_PAD])
 def test_forced_fold_segments(enc, kseg):
+    # (capped at the encoding's own segment: the weights-in-scales scheme folds every 768)
+    kseg = min(kseg, awe.get_encoding_info(enc)["k_seg"])
     M, N, K = 130, 260, 2000
     A, B = _operands(enc, M, N, K, seed=11)
     pa, pb = _planes(enc, 0, A, B)
@@ -229,7 +231,7 @@ def test_fp8fp4_4096_sampled():
 @pytest.mark.parametrize("cfg,cus", [("5", "12"), ("6", "16")])
 @pytest.mark.parametrize("enc,out", [(awe.ENC_AWE6, torch.int32), (awe.ENC_AWE4, torch.int64),
                                      (awe.ENC_FP8FP4, torch.int32), (awe.ENC_FP16, torch.int64),
-                                     (awe.ENC_FP6K3, torch.int32)])
+                                     (awe.ENC_FP6K3, torch.int32), (awe.ENC_FP6P4, torch.int32)])
 def test_split_last_round(monkeypatch, cfg, cus, enc, out):
     # AWE_GEMM_CUS plans the rounds of workgroups for fewer CUs, so that this shape has a
     # ragged last round (30 tiles on 12 CUs, 20 tiles on 16) whose tiles are split along
@@ -278,5 +280,39 @@ def test_fp6k3_8192_sampled():
     torch.cuda.synchronize()
     Ch = C.cpu().numpy()
     for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=1):
+        ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
+        assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)
+
+
+@pytest.mark.parametrize("cfg", ["0", "1"])
+def test_shared_accumulator_configurations(monkeypatch, cfg):
+    # INT8 x INT8 in 4 E2M3 products with the weights in the block scales: both tile
+    # configurations (fragments read ahead or in place), the default fold segment and a
+    # forced one of one K_PAD, and the accumulator near its bound: x = y = 120 makes every
+    # reduction index add 18,496 in absolute terms, and the default segment (768 indices)
+    # brings the FP32 accumulator to 14,400 * 768 = 11,059,200 of 2^24
+    monkeypatch.setenv("AWE_GEMM_CFG_SHARED", cfg)
+    M, N, K = 300, 420, 1100
+    A, B = _operands(awe.ENC_FP6P4, M, N, K, seed=int(cfg) + 90)
+    A[:7, :] = 120
+    B[:, :5] = 120
+    ref = og.gemm_i64(A, B)
+    assert np.array_equal(_run_exact(awe.ENC_FP6P4, A, B).astype(np.int64), ref)
+    pa, pb = _planes(awe.ENC_FP6P4, 0, A, B)
+    C = torch.empty((M, N), dtype=torch.int64, device="cuda")
+    awe.gemm_planes(awe.ENC_FP6P4, 0, M, N, K, pa, pb, C, N, awe.I64, awe.K_PAD)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy(), ref)
+
+
+def test_fp6p4_8192_sampled():
+    # the weights-in-scales scheme at 8192^3 (the benchmark's shape and launch), int32 C,
+    # sampled 128 x 128 tiles plus the four corner tiles
+    M = N = K = 8192
+    A, B = inputs.int8_pair(M, N, K, seed=0)
+    C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_FP6P4, torch.int32)
+    torch.cuda.synchronize()
+    Ch = C.cpu().numpy()
+    for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=3):
         ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
         assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)

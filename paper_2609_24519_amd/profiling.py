@@ -1,6 +1,7 @@
 """Summaries of rocprofv3 output for the profiles/ folder.
 
-    python -m paper_2609_24519_amd.profiling stats  <kernel_stats.csv> <out.md> "<command>"
+    python -m paper_2609_24519_amd.profiling stats  <kernel_stats.csv | kernel_trace.csv> <out.md> \
+        "<command>" [<warm-up dispatches to skip, kernel_trace.csv only>]
     python -m paper_2609_24519_amd.profiling traffic <fetch_counter_collection.csv> \\
         <write_counter_collection.csv> <out.json> <out.md> "<fetch command>" "<write command>"
     python -m paper_2609_24519_amd.profiling counters <out.md> <fp4_flop_per_gemm> \\
@@ -42,16 +43,34 @@ def _short(name):
     return name[:60]
 
 
-def stats(csv_path, out_md, command):
+def stats(csv_path, out_md, command, skip=0):
+    """Per-kernel times from a kernel_stats.csv, or from a kernel_trace.csv with the first
+    ``skip`` dispatches of every kernel left out (the untimed warm-up steps of the command,
+    so that the averages cover the same dispatches as the command's own timing)."""
     rows = list(csv.DictReader(open(csv_path)))
     lines = ["# Kernel time summary (rocprofv3 --kernel-trace --stats)", "",
-             "Command: `%s`" % command, "",
-             "| kernel | calls | average (us) | min (us) | max (us) | share |",
-             "|---|---|---|---|---|---|"]
-    for r in rows:
-        lines.append("| %s | %s | %.1f | %.1f | %.1f | %.1f%% |" % (
-            _short(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
-            float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+             "Command: `%s`" % command, ""]
+    if rows and "Start_Timestamp" in rows[0]:
+        per = {}
+        for r in rows:
+            per.setdefault(r["Kernel_Name"], []).append(
+                (int(r["Start_Timestamp"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+        lines += ["Per-dispatch durations from the kernel trace, the first %d dispatches of each kernel "
+                  "(the warm-up steps) left out." % skip, ""]
+        table = []
+        for name, d in per.items():
+            d = [us for _, us in sorted(d)][skip:]
+            if d:
+                table.append((name, len(d), sum(d) / len(d), min(d), max(d), sum(d)))
+        total = sum(t[5] for t in table) or 1.0
+        rows_out = [(n, c, a, lo, hi, 100.0 * t / total) for n, c, a, lo, hi, t in
+                    sorted(table, key=lambda t: -t[5])]
+    else:
+        rows_out = [(r["Name"], int(r["Calls"]), float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+                     float(r["MaxNs"]) / 1e3, float(r["Percentage"])) for r in rows]
+    lines += ["| kernel | calls | average (us) | min (us) | max (us) | share |", "|---|---|---|---|---|---|"]
+    for n, c, a, lo, hi, pct in rows_out:
+        lines.append("| %s | %d | %.1f | %.1f | %.1f | %.1f%% |" % (_short(n), c, a, lo, hi, pct))
     with open(out_md, "w") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -184,7 +203,7 @@ def counters(out_md, fp4_flop, command, paths):
 
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
-        stats(sys.argv[2], sys.argv[3], sys.argv[4])
+        stats(sys.argv[2], sys.argv[3], sys.argv[4], int(sys.argv[5]) if len(sys.argv) > 5 else 0)
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:8])
     elif sys.argv[1] == "counters":

@@ -1,0 +1,53 @@
+"""Host-side checks of the benchmark and profiling helpers (CPU only, no GPU calls)."""
+import csv
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    # the library has no multi-GPU path: --gpus N > 1 exits with a message before touching a GPU
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_read_smi_parses_clocks_and_power(tmp_path):
+    sys.path.insert(0, ROOT)
+    import bench
+
+    p = tmp_path / "smi.txt"
+    p.write_text("GPU: 0\n    POWER:\n        SOCKET_POWER: 1362 W\n    CLOCK:\n        GFX_0:\n"
+                 "            CLK: 2106 MHz\n            MIN_CLK: 500 MHz\n        GFX_1:\n"
+                 "            CLK: 2000 MHz\n")
+    r = bench.read_smi(str(p))
+    assert r == {"gfx_clock_mhz_mean": 2053.0, "gfx_clock_mhz_min": 2000, "gfx_clock_mhz_max": 2106,
+                 "socket_power_w": 1362.0}
+    assert "error" in bench.read_smi(str(tmp_path / "missing.txt"))
+
+
+def test_stats_from_trace_skips_warmup(tmp_path):
+    from paper_2609_24519_amd import profiling
+
+    trace = tmp_path / "trace.csv"
+    with open(trace, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        t = 0
+        for us in (900, 800, 100, 110, 120):  # two slow warm-up dispatches, then three timed ones
+            w.writerow(["void k<1>(int)", t, t + us * 1000])
+            t += 1_000_000
+    out = tmp_path / "out.md"
+    profiling.stats(str(trace), str(out), "cmd", 2)
+    row = [l for l in out.read_text().splitlines() if l.startswith("| void k")][0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[1:5] == ["3", "110.0", "100.0", "120.0"]
+
+
+def test_kernel_source_hash_tracks_the_kernel_file():
+    from paper_2609_24519_amd import profiling
+
+    h = profiling.kernel_source_hash()
+    assert h == profiling.kernel_source_hash() and len(h) >= 8

@@ -270,6 +270,7 @@ def main():
         del src, dst
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(A_h, B_h)
+        line["cpu_oracle_other_workloads"] = cpu_oracle_timings()
     print(json.dumps(line), flush=True)
 
 
@@ -526,6 +527,37 @@ def cpu_baseline(A_h, B_h, target_s=15.0):
             "kind": "oracle",
             "sample": "rows 0..%d of C over full N=%d, K=%d (%d MACs), %.1f s"
                       % (rows - 1, N, K, macs, dt)}
+
+
+def cpu_oracle_timings():
+    """The same oracle on the other workloads, each whole or on a stated block of rows (a few
+    seconds in all): 256^3 int8, 2048^3 int8, the 4096 x 4096 x 65,536 stress operands (rows
+    0..63), and one modulus of the residue set at 4096^3 (m = 251, rows 0..255).  MAC/s."""
+    import numpy as np
+
+    from oracle import gemm as og
+    from paper_2609_24519_amd import inputs
+
+    out = {}
+
+    def timed(name, A, B, full_rows, fn):
+        t0 = time.perf_counter()
+        fn(A, B)
+        dt = time.perf_counter() - t0
+        macs = A.shape[0] * A.shape[1] * B.shape[1]
+        out[name] = {"MAC_per_s": round(macs / dt, 1), "seconds": round(dt, 3),
+                     "rows": "%d of %d" % (A.shape[0], full_rows)}
+
+    A, B = inputs.int8_pair(256, 256, 256, seed=0)
+    og.gemm_i64(A, B)  # loads the library and starts its threads
+    timed("int8_256^3", A, B, 256, og.gemm_i64)
+    A, B = inputs.int8_pair(2048, 2048, 2048, seed=0)
+    timed("int8_2048^3", A, B, 2048, og.gemm_i64)
+    A, B = inputs.stress_operands(64, 4096, 65536, seed=0)
+    timed("stress_4096x4096x65536", np.ascontiguousarray(A), B, 4096, og.gemm_i64)
+    A, B = inputs.residue_pair(256, 4096, 4096, 251)
+    timed("residues_mod251_4096^3", A, B, 4096, lambda a, b: og.gemm_mod(251, a, b))
+    return out
 
 
 if __name__ == "__main__":

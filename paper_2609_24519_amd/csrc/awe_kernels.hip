@@ -48,8 +48,9 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
   slut[threadIdx.x] = lut.v[threadIdx.x];
   __syncthreads();
   const int lane = threadIdx.x & 63;
-  const int64_t brick = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (brick >= nbricks) return;
+  // each wave takes one brick, or several when the grid is capped
+  for (int64_t brick = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); brick < nbricks;
+       brick += (int64_t)gridDim.x * 4) {
   const int64_t rb = brick / KS, ks = brick - rb * KS;
   const int64_t row = rb * kBrickRows + (lane & 31);
   const int64_t k0 = ks * kBrickK + (lane >> 5) * 32;
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
       *reinterpret_cast<uint4*>(u + i * 1024 + lane * 16) = make_uint4(d[0], d[1], d[2], d[3]);
       *reinterpret_cast<uint2*>(u + 2048 + i * 512 + lane * 8) = make_uint2(d[4], d[5]);
     }
-    return;
+    continue;
   }
 
   // E4M3 planes (2 KiB bricks, 32 bytes per lane) first, then the E2M1 planes; an E4M3
@@ -134,6 +135,7 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
     for (int j = 0; j < 32; ++j) d[j >> 3] |= ((e[j] >> sh) & 0xfu) << (4 * (j & 7));
     *reinterpret_cast<uint4*>(dst + p * plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
   }
+  }  // bricks
 }
 
 // ---------------------------------------------------------------------------
@@ -895,8 +897,8 @@ awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
   }
   LutArg lut;
   for (int i = 0; i < 256; ++i) lut.v[i] = e.lut[i];
-  const int64_t blocks = (nbricks + 3) / 4;
-  if (blocks > 0x7fffffffLL) return AWE_ERR_UNSUPPORTED;
+  // one brick per wave; past 2^31 - 1 workgroups the waves walk several bricks each
+  const int64_t blocks = std::min<int64_t>((nbricks + 3) / 4, 0x7fffffffLL);
   if (e.transposed)
     hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,

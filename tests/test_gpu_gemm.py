@@ -118,8 +118,26 @@ def test_multi_launch_reduction():
     # host splits the reduction and the launches add into the int64 output
     M, N, K = 40, 72, 300_000
     A, B = inputs.int8_pair(M, N, K, seed=9)
-    C = _run_exact(awe.ENC_AWE6, A, B, torch.int64)
-    assert np.array_equal(C, og.gemm_i64(A, B))
+    ref = og.gemm_i64(A, B)
+    for enc in (awe.ENC_AWE6, awe.ENC_FP6K3, awe.ENC_FP6P4):
+        C = _run_exact(enc, A, B, torch.int64)
+        assert np.array_equal(C, ref), enc
+
+
+def test_fp32_partial_near_bound_fp6k3():
+    # the 3-product E2M3 scheme: c_A c_B = 15 * 15 (the sum plane of x = -120 is -8 - 7 = -15),
+    # default fold segment 37,120, so with A = B = -120 the sum plane's FP32 partial reaches
+    # 225 * 37120 = 8,352,000, just below 2^23, before its fold with coefficient 16
+    info = awe.get_encoding_info(awe.ENC_FP6K3)
+    K = info["k_seg"]
+    assert 225 * K < 2 ** 23 <= 225 * (K + awe.K_PAD)
+    lo, T = awe.get_plane_table(awe.ENC_FP6K3, 0, awe.SIDE_A)
+    assert list(T[-120 - lo]) == [-8, -7, -15]
+    A = np.full((32, K), -120, np.int8)
+    B = np.full((K, 48), -120, np.int8)
+    B[:, 1::2] = 127
+    C = _run_exact(awe.ENC_FP6K3, A, B, torch.int32)
+    assert np.array_equal(C.astype(np.int64), og.gemm_i64(A, B))
 
 
 def test_fp32_partial_near_bound():

@@ -6,6 +6,10 @@
 #include <cstring>
 #include <string>
 
+#include <map>
+#include <memory>
+#include <mutex>
+#include <vector>
 #include "awe_internal.h"
 
 namespace awe {
@@ -286,25 +290,55 @@ awe_status rns_setup(const int32_t* moduli, int32_t n, ResidueParams* rp, CrtPar
 }
 
 struct CrtLayout {  // workspace of awe_gemm_crt
-  size_t res_a, res_b, res_c, planes, total;
+  size_t luts;                   // the moduli's code tables, A side then B side (n x 1 KiB each)
+  size_t planes_a, planes_b;     // every modulus's stored planes of A, then of B
+  int64_t off_a[kMaxModuli], off_b[kMaxModuli];
+  size_t res_c;                  // the n int32 residue products
+  size_t total;
 };
 
 CrtLayout crt_layout(const int32_t* moduli, int32_t n, int64_t M, int64_t N, int64_t K, awe_status* st) {
   CrtLayout L{};
   *st = AWE_OK;
-  L.res_a = (size_t)round_up((int64_t)n * M * K, 256);
-  L.res_b = (size_t)round_up((int64_t)n * K * N, 256);
-  L.res_c = (size_t)round_up((int64_t)n * M * N * 4, 256);
-  size_t planes = 0;
+  L.luts = (size_t)round_up(2 * (int64_t)n * 256 * 4, 256);
+  int64_t pa = 0, pb = 0;
   for (int j = 0; j < n; ++j) {
     const Scheme* s = scheme_or_fail(AWE_ENC_MOD, moduli[j], st);
     if (!s) return L;
-    planes = std::max(planes, (size_t)round_up((int64_t)side_bytes(*s, true, M, K), 256) +
-                                  side_bytes(*s, false, N, K));
+    L.off_a[j] = pa;
+    L.off_b[j] = pb;
+    pa += (int64_t)side_bytes(*s, true, M, K);
+    pb += (int64_t)side_bytes(*s, false, N, K);
   }
-  L.planes = planes;
-  L.total = L.res_a + L.res_b + L.res_c + L.planes;
+  L.planes_a = (size_t)round_up(pa, 256);
+  L.planes_b = (size_t)round_up(pb, 256);
+  L.res_c = (size_t)round_up((int64_t)n * M * N * 4, 256);
+  L.total = L.luts + L.planes_a + L.planes_b + L.res_c;
   return L;
+}
+
+// The code tables of a set of moduli packed for the device (A side, then B side), built once
+// per set and kept for the life of the process, so that an asynchronous copy may read them.
+const std::vector<uint32_t>* crt_tables(const int32_t* moduli, int32_t n, awe_status* st) {
+  static std::mutex mu;
+  static std::map<std::vector<int32_t>, std::unique_ptr<std::vector<uint32_t>>> cache;
+  std::vector<int32_t> key(moduli, moduli + n);
+  {
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = cache.find(key);
+    if (it != cache.end()) return it->second.get();
+  }
+  auto t = std::make_unique<std::vector<uint32_t>>(2 * (size_t)n * 256);
+  for (int j = 0; j < n; ++j) {
+    const Scheme* s = scheme_or_fail(AWE_ENC_MOD, moduli[j], st);
+    if (!s) return nullptr;
+    std::copy(s->lut_a.begin(), s->lut_a.begin() + 256, t->begin() + (size_t)j * 256);
+    std::copy(s->lut_b.begin(), s->lut_b.begin() + 256, t->begin() + ((size_t)n + j) * 256);
+  }
+  std::lock_guard<std::mutex> lk(mu);
+  auto& slot = cache[key];
+  if (!slot) slot = std::move(t);
+  return slot.get();
 }
 
 }  // namespace
@@ -515,21 +549,48 @@ awe_status awe_gemm_crt(int64_t M, int64_t N, int64_t K, const int64_t* A, int64
   if (L.total > 0 && (workspace == nullptr || ws_bytes < L.total))
     return fail(AWE_ERR_WORKSPACE, "workspace smaller than awe_crt_workspace_bytes");
   uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
-  uint8_t* ra = ws;
-  uint8_t* rb = ra + L.res_a;
-  int32_t* rc = reinterpret_cast<int32_t*>(rb + L.res_b);
-  uint8_t* planes = rb + L.res_b + L.res_c;
+  uint32_t* luts = reinterpret_cast<uint32_t*>(ws);
+  uint8_t* pla = ws + L.luts;
+  uint8_t* plb = pla + L.planes_a;
+  int32_t* rc = reinterpret_cast<int32_t*>(plb + L.planes_b);
   if (K > 0) {
-    st = launch_residues(A, M, K, lda, bound_a, rp, ra, M * K, d_range_flag, stream);
-    if (st != AWE_OK) return st;
-    st = launch_residues(B, K, N, ldb, bound_b, rp, rb, K * N, d_range_flag, stream);
-    if (st != AWE_OK) return st;
+    // every modulus's planes of A and of B straight from the int64 operands
+    const std::vector<uint32_t>* tab = crt_tables(moduli, n, &st);
+    if (!tab) return st;
+    hipError_t err = hipMemcpyAsync(luts, tab->data(), tab->size() * sizeof(uint32_t),
+                                    hipMemcpyHostToDevice, stream);
+    if (err != hipSuccess) return fail(AWE_ERR_HIP, std::string("table upload: ") + hipGetErrorString(err));
+    const int64_t kp = round_up(K, kKPad);
+    for (int side = 0; side < 2; ++side) {
+      const bool sideA = side == 0;
+      ResidueEncodeArgs e{};
+      e.x = sideA ? A : B;
+      e.rows = sideA ? M : N;
+      e.K = K;
+      e.ld = sideA ? lda : ldb;
+      e.KS = kp / kBrickK;
+      e.R32 = (e.rows + kBrickRows - 1) / kBrickRows;
+      e.nbricks = e.R32 * e.KS;
+      e.bound = sideA ? bound_a : bound_b;
+      e.luts = luts + (sideA ? 0 : (size_t)n * 256);
+      e.planes = sideA ? pla : plb;
+      e.plane_stride = plane_stride_bytes(e.rows, K);
+      for (int j = 0; j < n; ++j) {
+        const Scheme* s = scheme_or_fail(AWE_ENC_MOD, moduli[j], &st);
+        if (!s) return st;
+        e.off[j] = sideA ? L.off_a[j] : L.off_b[j];
+        e.np[j] = sideA ? s->na : s->nb;
+      }
+      e.flag = d_range_flag;
+      st = launch_residue_encode(e, rp, !sideA, stream);
+      if (st != AWE_OK) return st;
+    }
   }
   for (int j = 0; j < n; ++j) {
     const Scheme* s = scheme_or_fail(AWE_ENC_MOD, moduli[j], &st);
     if (!s) return st;
-    st = exact_impl(*s, M, N, K, ra + (size_t)j * M * K, K, rb + (size_t)j * K * N, N, rc + (size_t)j * M * N,
-                    N, AWE_I32, planes, L.planes, nullptr, stream);
+    st = gemm_planes_impl(*s, M, N, K, pla + L.off_a[j], plb + L.off_b[j], rc + (size_t)j * M * N, N,
+                          AWE_I32, 0, stream);
     if (st != AWE_OK) return st;
   }
   if (c128 == nullptr && c64 == nullptr) return AWE_OK;

@@ -188,6 +188,22 @@ awe_status launch_residues(const int64_t* x, int64_t rows, int64_t cols, int64_t
                            const ResidueParams& P, uint8_t* out, int64_t out_stride, int32_t* flag,
                            hipStream_t stream);
 
+// Residues of an int64 operand written straight as every modulus's E2M1 planes.
+struct ResidueEncodeArgs {
+  const int64_t* x;
+  int64_t rows, K, ld;        // A side: x[row * ld + k]; B side: x[k * ld + row]
+  int64_t KS, R32, nbricks;   // bricks along K per row block, row blocks, all bricks
+  int64_t bound;              // |x| above it sets *flag
+  const uint32_t* luts;       // device: n x 256 packed E2M1 codes, one table per modulus
+  uint8_t* planes;            // modulus j's planes at planes + off[j], plane_stride apart
+  int64_t plane_stride;
+  int64_t off[kMaxModuli];
+  int32_t np[kMaxModuli];
+  int32_t* flag;
+};
+awe_status launch_residue_encode(const ResidueEncodeArgs& a, const ResidueParams& P, bool transposed,
+                                 hipStream_t stream);
+
 struct CrtModulus {
   uint32_t m;
   float inv;     // 1/m in fp32

@@ -4,6 +4,7 @@
 // correctly rounded double.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "awe_internal.h"
@@ -136,6 +137,104 @@ __global__ __launch_bounds__(256) void residues_kernel(const int64_t* __restrict
     }
   }
   if (out_of_range && flag) *flag = 1;
+}
+
+// Residues of an int64 operand for every modulus, turned straight into each modulus's
+// stored E2M1 planes (Alg. 1's table lookup applied to the residue), without the dense
+// residue matrices in between.  One wave per brick of the plane layout, as the encoder:
+// lane L = 32 h + t produces row t of the brick at reduction indices 32 h .. 32 h + 31.
+// On the B side (x is K x N) lane l first loads reduction index ks*64 + l at 32 columns,
+// computes their residues and stages them in LDS, then reads its column back, per modulus.
+template <bool kTransposed>
+__global__ __launch_bounds__(256) void residue_encode_kernel(ResidueEncodeArgs a, ResidueParams P) {
+  __shared__ uint32_t slut[kMaxModuli * 256];
+  __shared__ uint8_t tblk[kTransposed ? 4 : 1][kTransposed ? 64 * 32 : 1];
+  const int n = P.n;
+  for (int i = threadIdx.x; i < n * 256; i += blockDim.x) slut[i] = a.luts[i];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  bool out_of_range = false;
+  for (int64_t brick = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); brick < a.nbricks;
+       brick += (int64_t)gridDim.x * 4) {
+    const int64_t rb = brick / a.KS, ks = brick - rb * a.KS;
+    // this lane's 32 entries and which of them are real (the rest pad with code 0)
+    int64_t v[32];
+    uint32_t valid = 0;
+    if (!kTransposed) {
+      const int64_t row = rb * kBrickRows + (lane & 31), k0 = ks * kBrickK + (lane >> 5) * 32;
+      const int64_t* src = a.x + row * a.ld + k0;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        const bool ok = row < a.rows && k0 + e < a.K;
+        v[e] = ok ? src[e] : 0;
+        valid |= (ok ? 1u : 0u) << e;
+      }
+    } else {
+      const int64_t kr = ks * kBrickK + lane, n0 = rb * kBrickRows;
+      const int64_t* src = a.x + kr * a.ld + n0;
+#pragma unroll
+      for (int c = 0; c < 32; ++c) {
+        const bool ok = kr < a.K && n0 + c < a.rows;
+        v[c] = ok ? src[c] : 0;
+        valid |= (ok ? 1u : 0u) << c;
+      }
+    }
+    bool small = true;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+      out_of_range |= v[e] > a.bound || v[e] < -a.bound;
+      small &= v[e] < (int64_t(1) << 53) && v[e] > -(int64_t(1) << 53);
+    }
+    // one route for the whole wave (a per-entry choice would run both)
+    const bool wave_small = __all(small);
+    for (int j = 0; j < n; ++j) {
+      const ModConsts k = mod_consts(P, j);
+      uint32_t r[32];
+      if (wave_small) {
+#pragma unroll
+        for (int e = 0; e < 32; ++e) r[e] = residue_f64((double)v[e], k);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 32; ++e) {
+          uint32_t d[4];
+          digits_of(v[e], d);
+          r[e] = residue_of(d, (uint32_t)(v[e] >> 63), k);
+        }
+      }
+      uint32_t code[32];
+      uint32_t ok = valid;
+      if (kTransposed) {
+        // stage this lane's row of residues, read back column (lane & 31), rows 32 h ..
+        uint8_t* tw = tblk[threadIdx.x >> 6];
+        uint32_t w[8] = {};
+#pragma unroll
+        for (int c = 0; c < 32; ++c) w[c >> 2] |= r[c] << (8 * (c & 3));
+        *reinterpret_cast<uint4*>(tw + lane * 32) = make_uint4(w[0], w[1], w[2], w[3]);
+        *reinterpret_cast<uint4*>(tw + lane * 32 + 16) = make_uint4(w[4], w[5], w[6], w[7]);
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+        __builtin_amdgcn_wave_barrier();
+        const uint8_t* col = tw + (lane >> 5) * 32 * 32 + (lane & 31);
+        const int64_t row = rb * kBrickRows + (lane & 31), k0 = ks * kBrickK + (lane >> 5) * 32;
+        ok = 0;
+#pragma unroll
+        for (int e = 0; e < 32; ++e) {
+          r[e] = col[e * 32];
+          ok |= (row < a.rows && k0 + e < a.K ? 1u : 0u) << e;
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+#pragma unroll
+      for (int e = 0; e < 32; ++e) code[e] = ((ok >> e) & 1u) ? slut[j * 256 + r[e]] : 0u;
+      uint8_t* dst = a.planes + a.off[j] + (ks * a.R32 + rb) * kBrickBytes + lane * 16;
+      for (int pl = 0; pl < a.np[j]; ++pl) {
+        uint32_t d[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int e = 0; e < 32; ++e) d[e >> 3] |= ((code[e] >> (4 * pl)) & 0xfu) << (4 * (e & 7));
+        *reinterpret_cast<uint4*>(dst + pl * a.plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
+      }
+    }
+  }
+  if (out_of_range && a.flag) *a.flag = 1;
 }
 
 // |X| < 2^127 (two's complement in lo/hi) -> nearest double, ties to even.
@@ -272,6 +371,22 @@ awe_status launch_residues(const int64_t* x, int64_t rows, int64_t cols, int64_t
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) {
     set_error(std::string("residues launch: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  return AWE_OK;
+}
+
+awe_status launch_residue_encode(const ResidueEncodeArgs& a, const ResidueParams& P, bool transposed,
+                                 hipStream_t stream) {
+  if (a.nbricks == 0) return AWE_OK;
+  const int64_t blocks = std::min<int64_t>((a.nbricks + 3) / 4, 0x7fffffffLL);
+  if (transposed)
+    hipLaunchKernelGGL(residue_encode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, a, P);
+  else
+    hipLaunchKernelGGL(residue_encode_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, a, P);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) {
+    set_error(std::string("residue encode launch: ") + hipGetErrorString(err));
     return AWE_ERR_HIP;
   }
   return AWE_OK;

@@ -173,3 +173,26 @@ def test_gemm_crt_4096_sampled():
     assert (_words_to_ints(sub) == ref).all()
     sub64 = c64[torch.as_tensor(rows, device="cuda")][:, torch.as_tensor(cols, device="cuda")]
     assert np.array_equal(sub64.cpu().numpy(), ocrt.to_double(ref))
+
+
+def test_gemm_crt_range_flag_and_large_entries():
+    # entries beyond the stated bound set the flag (both operands), and entries at or beyond
+    # 2^53 (the integer residue route instead of the double one) still give exact residues;
+    # the product stays within the moduli's range, so C is exact too
+    ms = _moduli()
+    M, N, K = 33, 40, 300
+    rng = np.random.default_rng(21)
+    A = rng.integers(-1000, 1000, size=(M, K), dtype=np.int64, endpoint=True)
+    B = rng.integers(-1000, 1000, size=(K, N), dtype=np.int64, endpoint=True)
+    for bound_a, bound_b, big in ((1000, 1000, False), (999, 1000, False), (1000, 999, False),
+                                  (1 << 60, 1000, True)):
+        Ai = A.copy()
+        if big:
+            Ai[3, 7] = (1 << 53) + 5  # a wave of A entries takes the integer route
+            Ai[4, 9] = -(1 << 60)
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        c128, c64 = awe.matmul_crt(to_dev(Ai), to_dev(B), ms, bound_a, bound_b, flag)
+        torch.cuda.synchronize()
+        expect_flag = bool((np.abs(Ai) > bound_a).any() or (np.abs(B) > bound_b).any())
+        assert bool(flag.item()) == expect_flag, (bound_a, bound_b)
+        assert (_words_to_ints(c128) == og.gemm_i128(Ai, B)).all()

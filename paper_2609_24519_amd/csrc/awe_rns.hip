@@ -186,25 +186,11 @@ __global__ __launch_bounds__(256) void residue_encode_kernel(ResidueEncodeArgs a
       small &= v[e] < (int64_t(1) << 53) && v[e] > -(int64_t(1) << 53);
     }
     // one route for the whole wave (a per-entry choice would run both)
-    const bool wave_small = __all(small);
-    for (int j = 0; j < n; ++j) {
-      const ModConsts k = mod_consts(P, j);
-      uint32_t r[32];
-      if (wave_small) {
-#pragma unroll
-        for (int e = 0; e < 32; ++e) r[e] = residue_f64((double)v[e], k);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 32; ++e) {
-          uint32_t d[4];
-          digits_of(v[e], d);
-          r[e] = residue_of(d, (uint32_t)(v[e] >> 63), k);
-        }
-      }
-      uint32_t code[32];
+    // Modulus j's planes of this brick from the lane's 32 residues r (this lane's row, or on
+    // the B side its row of K x N, transposed through LDS first).
+    auto emit = [&](int j, uint32_t (&r)[32]) {
       uint32_t ok = valid;
       if (kTransposed) {
-        // stage this lane's row of residues, read back column (lane & 31), rows 32 h ..
         uint8_t* tw = tblk[threadIdx.x >> 6];
         uint32_t w[8] = {};
 #pragma unroll
@@ -223,6 +209,7 @@ __global__ __launch_bounds__(256) void residue_encode_kernel(ResidueEncodeArgs a
         }
         __builtin_amdgcn_wave_barrier();
       }
+      uint32_t code[32];
 #pragma unroll
       for (int e = 0; e < 32; ++e) code[e] = ((ok >> e) & 1u) ? slut[j * 256 + r[e]] : 0u;
       uint8_t* dst = a.planes + a.off[j] + (ks * a.R32 + rb) * kBrickBytes + lane * 16;
@@ -231,6 +218,32 @@ __global__ __launch_bounds__(256) void residue_encode_kernel(ResidueEncodeArgs a
 #pragma unroll
         for (int e = 0; e < 32; ++e) d[e >> 3] |= ((code[e] >> (4 * pl)) & 0xfu) << (4 * (e & 7));
         *reinterpret_cast<uint4*>(dst + pl * a.plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
+      }
+    };
+    // one route for the whole wave (a per-entry choice would run both); the double route
+    // keeps only the converted entries live across the moduli
+    if (__all(small)) {
+      double xd[32];
+#pragma unroll
+      for (int e = 0; e < 32; ++e) xd[e] = (double)v[e];
+      for (int j = 0; j < n; ++j) {
+        const ModConsts k = mod_consts(P, j);
+        uint32_t r[32];
+#pragma unroll
+        for (int e = 0; e < 32; ++e) r[e] = residue_f64(xd[e], k);
+        emit(j, r);
+      }
+    } else {
+      for (int j = 0; j < n; ++j) {
+        const ModConsts k = mod_consts(P, j);
+        uint32_t r[32];
+#pragma unroll
+        for (int e = 0; e < 32; ++e) {
+          uint32_t d[4];
+          digits_of(v[e], d);
+          r[e] = residue_of(d, (uint32_t)(v[e] >> 63), k);
+        }
+        emit(j, r);
       }
     }
   }

@@ -160,10 +160,7 @@ awe_status encode_impl(const Scheme& s, awe_side side, const void* x, int64_t ro
                        int64_t ld, void* planes, int32_t* flag, hipStream_t stream) {
   if (side != AWE_SIDE_A && side != AWE_SIDE_B) return fail(AWE_ERR_INVALID_VALUE, "bad side");
   if (rows < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
-  if (rows == 0 || K == 0) {
-    if (rows > 0 && K == 0) return AWE_OK;  // no bricks: Kp = 0
-    return AWE_OK;
-  }
+  if (rows == 0 || K == 0) return AWE_OK;  // no bricks
   if (x == nullptr || planes == nullptr) return fail(AWE_ERR_INVALID_VALUE, "NULL pointer");
   const bool sideA = side == AWE_SIDE_A;
   if (sideA ? ld < K : ld < rows) return fail(AWE_ERR_INVALID_VALUE, "leading dimension too small");

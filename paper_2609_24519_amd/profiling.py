@@ -6,6 +6,7 @@
         <write_counter_collection.csv> <out.json> <out.md> "<fetch command>" "<write command>"
     python -m paper_2609_24519_amd.profiling counters <out.md> <fp4_flop_per_gemm> \\
         "<command>" <counter_collection.csv> [<counter_collection.csv> ...]
+    python -m paper_2609_24519_amd.profiling clock <bench output> <out.md> "<command>"
 
 ``stats`` turns a ``--kernel-trace --stats`` kernel_stats.csv into a short
 Markdown table.  ``traffic`` takes two ``--pmc`` runs (FETCH_SIZE, then
@@ -17,7 +18,8 @@ they were taken on, so that a later change to the kernel makes them stale.
 ``counters`` summarises one or more ``--pmc`` passes over the same command:
 per kernel the FP4 MFMA operation count (checked against the algorithmic
 r 2MNK), MFMA busy cycles, LDS bank conflicts and activity, L2 hit rate and
-request latency.
+request latency.  ``clock`` renders the engine clocks and socket power that
+``bench.py --clock-sample`` read under each load.
 """
 import csv
 import hashlib
@@ -201,6 +203,48 @@ def counters(out_md, fp4_flop, command, paths):
         f.write("\n".join(lines) + "\n")
 
 
+CLOCK_LOADS = (
+    ("gemm", "AWE6 GEMM (awe_gemm_planes, 8192^3, 6 FP4 products)"),
+    ("gemm_e2m3", "E2M3 GEMM, 3 products (FP6 Karatsuba, 8192^3)"),
+    ("gemm_e2m3_scaled", "E2M3 GEMM, 4 products with the weights in the scales (8192^3)"),
+    ("probe_static", "FP4 MFMA probe, constant operands (8 waves/CU)"),
+    ("probe_varied", "FP4 MFMA probe, operands changing between MFMAs (8 waves/CU)"),
+    ("probe_varied_e2m3", "E2M3 MFMA probe, operands changing between MFMAs (8 waves/CU)"),
+)
+
+
+def clock(bench_log, out_md, command):
+    """The `clock_under_load` field of a `bench.py --clock-sample` line as a table."""
+    line = None
+    with open(bench_log) as f:
+        for l in f:
+            if l.startswith("{") and "clock_under_load" in l:
+                line = json.loads(l)
+    if line is None:
+        raise SystemExit("no bench line with clock_under_load in " + bench_log)
+    loads = line["clock_under_load"]
+    lines = ["# Engine clock and socket power under load (amd-smi metric -c -p)", "",
+             "Command: `%s`" % command, "",
+             "Each load runs in a loop; `amd-smi metric -c -p` is read once 2 s after it starts (a child",
+             "process started before the GPU is touched).  Clock = mean of the 8 XCDs' GFX clocks; the",
+             "peak at that clock is 256 CUs x 16,384 FP4 (or FP6) FLOP per clock; rates count the",
+             "products' FP4/FP6 work, r 2MNK per GEMM.", "",
+             "| load | GFX clock mean (min..max) MHz | socket power W | TFLOP/s | fraction of the peak at that "
+             "clock | fraction of the 10.1 PF spec |", "|---|---|---|---|---|---|"]
+    for key, label in CLOCK_LOADS:
+        r = loads.get(key)
+        if not r or "fp4_TFLOPs" not in r:
+            continue
+        clk = "%.0f (%.0f..%.0f)" % (r["gfx_clock_mhz_mean"], r["gfx_clock_mhz_min"], r["gfx_clock_mhz_max"]) \
+            if "gfx_clock_mhz_mean" in r else "n/a"
+        pw = "%.0f" % r["socket_power_w"] if r.get("socket_power_w") is not None else "n/a"
+        fr = "%.3f" % r["frac_of_peak_at_this_clock"] if "frac_of_peak_at_this_clock" in r else "n/a"
+        lines.append("| %s | %s | %s | %.1f | %s | %.3f |" % (label, clk, pw, r["fp4_TFLOPs"], fr,
+                                                            r["fp4_TFLOPs"] / 10100.0))
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], sys.argv[4], int(sys.argv[5]) if len(sys.argv) > 5 else 0)
@@ -208,5 +252,7 @@ if __name__ == "__main__":
         traffic(*sys.argv[2:8])
     elif sys.argv[1] == "counters":
         counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:])
+    elif sys.argv[1] == "clock":
+        clock(sys.argv[2], sys.argv[3], sys.argv[4])
     else:
         raise SystemExit(__doc__)

@@ -51,3 +51,25 @@ def test_kernel_source_hash_tracks_the_kernel_file():
 
     h = profiling.kernel_source_hash()
     assert h == profiling.kernel_source_hash() and len(h) >= 8
+
+
+def test_clock_table_from_bench_line(tmp_path):
+    import json
+
+    from paper_2609_24519_amd import profiling
+
+    line = {"metric": "m", "clock_under_load": {
+        "gemm": {"gfx_clock_mhz_mean": 2000.0, "gfx_clock_mhz_min": 1950, "gfx_clock_mhz_max": 2050,
+                 "socket_power_w": 1380.0, "fp4_TFLOPs": 4040.0, "frac_of_peak_at_this_clock": 0.4817},
+        "probe_varied": {"gfx_clock_mhz_mean": 1600.0, "gfx_clock_mhz_min": 1500, "gfx_clock_mhz_max": 1700,
+                         "socket_power_w": None, "fp4_TFLOPs": 6363.0}}}
+    log = tmp_path / "bench.log"
+    log.write_text("noise\n" + json.dumps(line) + "\n")
+    out = tmp_path / "clock.md"
+    profiling.clock(str(log), str(out), "cmd")
+    rows = [l for l in out.read_text().splitlines() if l.startswith("| AWE6") or l.startswith("| FP4 MFMA")]
+    assert len(rows) == 2
+    gemm = [c.strip() for c in rows[0].strip("|").split("|")]
+    assert gemm[1:] == ["2000 (1950..2050)", "1380", "4040.0", "0.482", "0.400"]
+    probe = [c.strip() for c in rows[1].strip("|").split("|")]
+    assert probe[2] == "n/a" and probe[4] == "n/a" and probe[5] == "0.630"

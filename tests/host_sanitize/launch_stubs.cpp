@@ -1,0 +1,24 @@
+// Host-only stand-ins for the device launchers of libawe: with these, the table builder and the
+// C ABI's argument checks link and run without a GPU (and under the host sanitizers).  Each stub
+// only counts its calls.
+#include "awe_internal.h"
+
+namespace awe {
+int g_launches = 0;
+awe_status launch_encode(const EncodeLaunch&, hipStream_t) { ++g_launches; return AWE_OK; }
+awe_status launch_gemm(const GemmLaunch&, hipStream_t) { ++g_launches; return AWE_OK; }
+awe_status launch_residues(const int64_t*, int64_t, int64_t, int64_t, int64_t, const ResidueParams&, uint8_t*,
+                           int64_t, int32_t*, hipStream_t) {
+  ++g_launches;
+  return AWE_OK;
+}
+awe_status launch_residue_encode(const ResidueEncodeArgs&, const ResidueParams&, bool, hipStream_t) {
+  ++g_launches;
+  return AWE_OK;
+}
+awe_status launch_crt(const int32_t*, int64_t, int64_t, int64_t, int64_t, const CrtParams&, int64_t*, double*,
+                      int64_t, hipStream_t) {
+  ++g_launches;
+  return AWE_OK;
+}
+}  // namespace awe

@@ -236,8 +236,8 @@ awe_status awe_crt_workspace_bytes(const int32_t* moduli, int32_t n, int64_t M, 
 /* Exact C = A B for int64 A (M x K, lda) and B (K x N, ldb) with |entries| <= bound_a and
    bound_b, through residues: every modulus's stored planes of both operands in one pass over
    each (the residues of awe_residues, encoded as awe_encode would), the mod-m product of
-   awe_gemm_mod for every modulus, awe_crt into c128 and/or c64 (as for awe_crt, leading
-   dimension ldc).  Requires M_prod > 2 K bound_a bound_b (AWE_ERR_OVERFLOW otherwise) and every
+   awe_gemm_mod for every modulus (all moduli in one kernel launch where the tile configuration
+   allows it), awe_crt into c128 and/or c64 (as for awe_crt, leading dimension ldc).  Requires M_prod > 2 K bound_a bound_b (AWE_ERR_OVERFLOW otherwise) and every
    modulus to have a scheme (AWE_ERR_UNSUPPORTED).  Entries beyond their bound set
    *d_range_flag.  The workspace (caller-owned device memory, awe_crt_workspace_bytes) holds the
    moduli's code tables, all their planes and the n int32 residue products; it is uploaded to

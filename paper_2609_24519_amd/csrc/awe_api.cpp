@@ -65,9 +65,11 @@ int64_t launch_k_limit(const Scheme& s) {
   return std::max<int64_t>(lim / per_k / kKPad * kKPad, kKPad);
 }
 
-awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, const void* pa,
-                            const void* pb, void* C, int64_t ldc, awe_dtype c_type, int64_t k_seg,
-                            hipStream_t stream) {
+// The launches of one exact or mod-m GEMM on stored planes, in order (every launch after
+// the first adds into C); nothing is enqueued.
+awe_status plan_gemm(const Scheme& s, int64_t M, int64_t N, int64_t K, const void* pa, const void* pb,
+                     void* C, int64_t ldc, awe_dtype c_type, int64_t k_seg, std::vector<GemmLaunch>* plan) {
+  plan->clear();
   if (M < 0 || N < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
   if (c_type != AWE_I32 && c_type != AWE_I64) return fail(AWE_ERR_INVALID_VALUE, "bad c_type");
   if (s.modulus && c_type != AWE_I32) return fail(AWE_ERR_INVALID_VALUE, "residues are written as int32");
@@ -107,7 +109,8 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
   if (kp == 0) {
     L.k_begin = L.k_end = 0;
     L.accumulate = false;
-    return launch_gemm(L, stream);
+    plan->push_back(L);
+    return AWE_OK;
   }
   // one launch per (reduction range, launch group); every launch after the first adds into C
   for (int64_t k0 = 0; k0 < kp; k0 += step) {
@@ -149,11 +152,19 @@ awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, co
       L.k_begin = k0;
       L.k_end = std::min(kp, k0 + step);
       L.accumulate = k0 > 0 || g > 0;
-      awe_status st = launch_gemm(L, stream);
-      if (st != AWE_OK) return st;
+      plan->push_back(L);
     }
   }
   return AWE_OK;
+}
+
+awe_status gemm_planes_impl(const Scheme& s, int64_t M, int64_t N, int64_t K, const void* pa,
+                            const void* pb, void* C, int64_t ldc, awe_dtype c_type, int64_t k_seg,
+                            hipStream_t stream) {
+  std::vector<GemmLaunch> plan;
+  awe_status st = plan_gemm(s, M, N, K, pa, pb, C, ldc, c_type, k_seg, &plan);
+  for (size_t i = 0; st == AWE_OK && i < plan.size(); ++i) st = launch_gemm(plan[i], stream);
+  return st;
 }
 
 awe_status encode_impl(const Scheme& s, awe_side side, const void* x, int64_t rows, int64_t K,
@@ -583,12 +594,27 @@ awe_status awe_gemm_crt(int64_t M, int64_t N, int64_t K, const int64_t* A, int64
       if (st != AWE_OK) return st;
     }
   }
+  // the n mod-m GEMMs: one grouped launch when each is a single launch (AWE_GEMM_GROUPED=0
+  // asks for one launch per modulus)
+  std::vector<GemmLaunch> all, plan;
+  bool single = true;
   for (int j = 0; j < n; ++j) {
     const Scheme* s = scheme_or_fail(AWE_ENC_MOD, moduli[j], &st);
     if (!s) return st;
-    st = gemm_planes_impl(*s, M, N, K, pla + L.off_a[j], plb + L.off_b[j], rc + (size_t)j * M * N, N,
-                          AWE_I32, 0, stream);
+    st = plan_gemm(*s, M, N, K, pla + L.off_a[j], plb + L.off_b[j], rc + (size_t)j * M * N, N, AWE_I32, 0, &plan);
     if (st != AWE_OK) return st;
+    single = single && plan.size() == 1;
+    all.insert(all.end(), plan.begin(), plan.end());
+  }
+  const char* ge = getenv("AWE_GEMM_GROUPED");
+  if (single && !(ge && atoi(ge) == 0) && gemm_group_ok(all.data(), (int)all.size())) {
+    st = launch_gemm_group(all.data(), (int)all.size(), stream);
+    if (st != AWE_OK) return st;
+  } else {
+    for (const GemmLaunch& gl : all) {
+      st = launch_gemm(gl, stream);
+      if (st != AWE_OK) return st;
+    }
   }
   if (c128 == nullptr && c64 == nullptr) return AWE_OK;
   return launch_crt(rc, M * N, M, N, N, cp, c128, c64, ldc, stream);

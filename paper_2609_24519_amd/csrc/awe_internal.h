@@ -171,6 +171,13 @@ struct GemmLaunch {
 };
 awe_status launch_gemm(const GemmLaunch& g, hipStream_t stream);
 
+// Several single-launch GEMMs of one shape as one launch (the residue route's moduli).  Each
+// launch must pass gemm_group_ok: E2M1 planes, one product per plane pair stream of at most
+// kGroupProducts products, the same M, N, K and reduction range, no accumulation into C.
+constexpr int kGroupProducts = 4;
+bool gemm_group_ok(const GemmLaunch* L, int n);
+awe_status launch_gemm_group(const GemmLaunch* L, int n, hipStream_t stream);
+
 // ---- residue number system (awe_rns.hip) ----
 constexpr int kMaxModuli = AWE_MAX_MODULI;
 

@@ -535,24 +535,14 @@ __global__ __launch_bounds__(256) void zero_tiles_kernel(GemmArgs g, int bm, int
   }
 }
 
+// One workgroup's output tile over reduction stages t_beg .. t_end - 1 (part >= 0: one
+// part of a split tile, added into C).  fold_ell: the fold coefficient of each product.
 template <class C>
-__global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int32_t* fold_ell, int tile, int part,
+                                          int t_beg, int t_end) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // Which tile, and which part of the reduction range: the workgroups past n_full
-  // share the ragged last round's tiles, `split` to a tile.
-  int tile = blockIdx.x, part = -1;
-  int t_beg = g.t_begin, t_end = g.t_end;
-  if (tile >= g.n_full) {
-    const int rel = tile - g.n_full;
-    tile = g.n_full + rel / g.split;
-    part = rel % g.split;
-    const int per = (g.t_end - g.t_begin + g.split - 1) / g.split;
-    t_beg = g.t_begin + part * per;
-    t_end = min(g.t_end, t_beg + per);
-    if (t_beg >= t_end) return;  // the host splits only ranges of at least 2 stages per part
-  }
   int tm, tn;
   tile_of_block(g, tile, tm, tn);
   const int wm = wave / C::WN, wn = wave % C::WN;
@@ -661,7 +651,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
         buf = nbuf;
       }
       if ((g.fold_mask >> p) & 1u) {
-        const int32_t l = g.fold_ell[p];
+        const int32_t l = fold_ell[p];
         // one 32x32 block at a time keeps the temporaries of the fold small
 #pragma unroll
         for (int i = 0; i < C::BMW; ++i)
@@ -699,6 +689,76 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
         else
           add_output(g, row, col, iacc[i][j][v]);
       }
+}
+
+template <class C>
+__global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
+  // Which tile, and which part of the reduction range: the workgroups past n_full
+  // share the ragged last round's tiles, `split` to a tile.
+  int tile = blockIdx.x, part = -1;
+  int t_beg = g.t_begin, t_end = g.t_end;
+  if (tile >= g.n_full) {
+    const int rel = tile - g.n_full;
+    tile = g.n_full + rel / g.split;
+    part = rel % g.split;
+    const int per = (g.t_end - g.t_begin + g.split - 1) / g.split;
+    t_beg = g.t_begin + part * per;
+    t_end = min(g.t_end, t_beg + per);
+    if (t_beg >= t_end) return;  // the host splits only ranges of at least 2 stages per part
+  }
+  gemm_tile<C>(g, g.fold_ell, tile, part, t_beg, t_end);
+}
+
+// Several GEMMs of one shape in one launch (the residue route's moduli): job j's tiles are
+// workgroups j * tiles .. j * tiles + tiles - 1, the jobs ordered by the host (most products
+// first, so that the short jobs fill the last rounds).  Every job covers the launch's whole
+// reduction range; nothing is split.
+struct GroupJob {
+  const uint8_t* pa;
+  const uint8_t* pb;
+  void* C;
+  uint64_t pidx_a, pidx_b;
+  int32_t fold_ell[kGroupProducts];
+  uint32_t fold_mask;
+  int32_t r, modulus, ts;
+};
+struct GroupArgs {
+  GemmArgs g;  // the fields all jobs share (shape, strides, reduction range, tiling)
+  GroupJob job[kMaxModuli];
+  int32_t tiles;
+};
+
+// A wave-uniform value in scalar registers.
+__device__ __forceinline__ uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint64_t uniform(uint64_t v) {
+  return ((uint64_t)uniform((uint32_t)(v >> 32)) << 32) | uniform((uint32_t)v);
+}
+template <class T>
+__device__ __forceinline__ T* uniform(T* p) {
+  return reinterpret_cast<T*>(uniform(reinterpret_cast<uint64_t>(p)));
+}
+
+template <class C>
+__global__ __launch_bounds__(C::THREADS, 1) void gemm_group_kernel(GroupArgs ga) {
+  // wave-uniform job index, so that the job's fields load into scalar registers
+  const int j = __builtin_amdgcn_readfirstlane((int)(blockIdx.x / ga.tiles));
+  const int tile = blockIdx.x - j * ga.tiles;
+  const GroupJob& jb = ga.job[j];
+  GemmArgs g = ga.g;
+  g.pa = uniform(jb.pa);
+  g.pb = uniform(jb.pb);
+  g.C = uniform(jb.C);
+  g.pidx_a = uniform(jb.pidx_a);
+  g.pidx_b = uniform(jb.pidx_b);
+  g.fold_mask = uniform(jb.fold_mask);
+  g.r = uniform(jb.r);
+  g.modulus = uniform(jb.modulus);
+  g.ts = uniform(jb.ts);
+  int32_t fold_ell[kGroupProducts];
+#pragma unroll
+  for (int k = 0; k < kGroupProducts; ++k) fold_ell[k] = uniform(jb.fold_ell[k]);
+  gemm_tile<C>(g, fold_ell, tile, -1, g.t_begin, g.t_end);
 }
 
 // The tile configurations the launcher chooses from: waves (M x N), 32x32
@@ -783,6 +843,52 @@ int choose_cfg_e2m3() {
   return forced >= 0 && forced <= 4 ? forced : 3;
 }
 
+// The kernel arguments of one launch.
+void fill_args(const GemmLaunch& L, GemmArgs& g) {
+  g.pa = L.planes_a;
+  g.pb = L.planes_b;
+  g.stride_a = L.stride_a;
+  g.stride_b = L.stride_b;
+  g.rba = (int32_t)((L.M + kBrickRows - 1) / kBrickRows);
+  g.rbb = (int32_t)((L.N + kBrickRows - 1) / kBrickRows);
+  const int64_t kp = (L.K + kKPad - 1) / kKPad * kKPad;
+  g.KS = (int32_t)(kp / kBrickK);
+  g.r = L.r;
+  g.pidx_a = g.pidx_b = 0;
+  for (int k = 0; k < L.r; ++k) {
+    g.pidx_a |= (uint64_t)(L.pa[k] & 15) << (4 * k);
+    g.pidx_b |= (uint64_t)(L.pb[k] & 15) << (4 * k);
+    g.fold_ell[k] = L.fold_ell[k];
+  }
+  g.fold_mask = L.fold_mask;
+  g.C = L.C;
+  g.ldc = L.ldc;
+  g.M = (int32_t)L.M;
+  g.N = (int32_t)L.N;
+  g.c64 = L.c_type == AWE_I64;
+  g.accumulate = L.accumulate;
+  g.log2D = L.log2D;
+  g.modulus = L.modulus;
+  g.outer = L.outer;
+}
+
+// Raises a kernel's dynamic LDS limit to `bytes` once per device (the GEMM's ring exceeds
+// the default).
+awe_status set_lds_limit(const void* fn, int bytes, std::mutex& mu, std::set<int>& done) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  std::lock_guard<std::mutex> lk(mu);
+  if (e == hipSuccess && !done.count(dev)) {
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess) done.insert(dev);
+  }
+  if (e != hipSuccess) {
+    set_error(std::string("gemm LDS attribute: ") + hipGetErrorString(e));
+    return AWE_ERR_HIP;
+  }
+  return AWE_OK;
+}
+
 template <class C>
 awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
   const int64_t tiles_m = (L.M + C::BM - 1) / C::BM, tiles_n = (L.N + C::BN - 1) / C::BN;
@@ -821,26 +927,69 @@ awe_status launch_tile(GemmArgs& g, const GemmLaunch& L, hipStream_t stream) {
     }
   }
   {
-    // the LDS ring exceeds the default dynamic LDS limit: raise it once per device
     static std::mutex mu;
     static std::set<int> done;
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    std::lock_guard<std::mutex> lk(mu);
-    if (e == hipSuccess && !done.count(dev)) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<C>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-      if (e == hipSuccess) done.insert(dev);
-    }
-    if (e != hipSuccess) {
-      set_error(std::string("gemm LDS attribute: ") + hipGetErrorString(e));
-      return AWE_ERR_HIP;
-    }
+    const awe_status st = set_lds_limit(reinterpret_cast<const void*>(&gemm_kernel<C>), C::LDS_BYTES, mu, done);
+    if (st != AWE_OK) return st;
   }
   hipLaunchKernelGGL(gemm_kernel<C>, dim3((unsigned)blocks), dim3(C::THREADS), C::LDS_BYTES, stream, g);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) {
     set_error(std::string("gemm launch: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  return AWE_OK;
+}
+
+// One launch for n jobs (launch_gemm_group): the shared arguments from the first, each job's
+// planes, C, products and coefficients from its own launch.
+template <class C>
+awe_status launch_group_tile(const GemmLaunch* L, const int* order, int n, hipStream_t stream) {
+  GroupArgs ga{};
+  GemmArgs& g = ga.g;
+  fill_args(L[order[0]], g);
+  const int64_t tiles_m = (L[0].M + C::BM - 1) / C::BM, tiles_n = (L[0].N + C::BN - 1) / C::BN;
+  const int64_t tiles = tiles_m * tiles_n;
+  if (tiles * n > 0x7fffffffLL) {
+    set_error("too many workgroups for one grouped launch");
+    return AWE_ERR_UNSUPPORTED;
+  }
+  g.t_begin = (int32_t)(L[0].k_begin / C::KT);
+  g.t_end = (int32_t)(L[0].k_end / C::KT);
+  g.tiles_m = (int32_t)tiles_m;
+  g.tiles_n = (int32_t)tiles_n;
+  g.n_full = (int32_t)tiles;
+  g.split = 1;
+  ga.tiles = (int32_t)tiles;
+  for (int j = 0; j < n; ++j) {
+    const GemmLaunch& Lj = L[order[j]];
+    GroupJob& jb = ga.job[j];
+    jb.pa = Lj.planes_a;
+    jb.pb = Lj.planes_b;
+    jb.C = Lj.C;
+    jb.pidx_a = jb.pidx_b = 0;
+    for (int k = 0; k < Lj.r; ++k) {
+      jb.pidx_a |= (uint64_t)(Lj.pa[k] & 15) << (4 * k);
+      jb.pidx_b |= (uint64_t)(Lj.pb[k] & 15) << (4 * k);
+      jb.fold_ell[k] = Lj.fold_ell[k];
+    }
+    jb.fold_mask = Lj.fold_mask;
+    jb.r = Lj.r;
+    jb.modulus = Lj.modulus;
+    jb.ts = (int32_t)(Lj.k_seg / C::KT);
+  }
+  {
+    static std::mutex mu;
+    static std::set<int> done;
+    const awe_status st =
+        set_lds_limit(reinterpret_cast<const void*>(&gemm_group_kernel<C>), C::LDS_BYTES, mu, done);
+    if (st != AWE_OK) return st;
+  }
+  hipLaunchKernelGGL(gemm_group_kernel<C>, dim3((unsigned)(tiles * n)), dim3(C::THREADS), C::LDS_BYTES, stream,
+                     ga);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) {
+    set_error(std::string("grouped gemm launch: ") + hipGetErrorString(err));
     return AWE_ERR_HIP;
   }
   return AWE_OK;
@@ -942,31 +1091,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     return AWE_OK;
   }
   GemmArgs g{};
-  g.pa = L.planes_a;
-  g.pb = L.planes_b;
-  g.stride_a = L.stride_a;
-  g.stride_b = L.stride_b;
-  g.rba = (int32_t)((L.M + kBrickRows - 1) / kBrickRows);
-  g.rbb = (int32_t)((L.N + kBrickRows - 1) / kBrickRows);
-  const int64_t kp = (L.K + kKPad - 1) / kKPad * kKPad;
-  g.KS = (int32_t)(kp / kBrickK);
-  g.r = L.r;
-  g.pidx_a = g.pidx_b = 0;
-  for (int k = 0; k < L.r; ++k) {
-    g.pidx_a |= (uint64_t)(L.pa[k] & 15) << (4 * k);
-    g.pidx_b |= (uint64_t)(L.pb[k] & 15) << (4 * k);
-    g.fold_ell[k] = L.fold_ell[k];
-  }
-  g.fold_mask = L.fold_mask;
-  g.C = L.C;
-  g.ldc = L.ldc;
-  g.M = (int32_t)L.M;
-  g.N = (int32_t)L.N;
-  g.c64 = L.c_type == AWE_I64;
-  g.accumulate = L.accumulate;
-  g.log2D = L.log2D;
-  g.modulus = L.modulus;
-  g.outer = L.outer;
+  fill_args(L, g);
   if (L.fmt == kFmtE4M3) return launch_tile<Cfg8w64x64e4m3>(g, L, stream);
   if (L.shared) {
     for (int k = 0; k < 2; ++k) {
@@ -997,6 +1122,43 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 7: return launch_tile<Cfg8w64x96s5>(g, L, stream);
     case 8: return launch_tile<Cfg8w64x96k4p0>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
+  }
+}
+
+// The grouped kernel is built for the 256 x 128 tiles on 8 waves (configurations 1, 4
+// and 5); the 256 x 192 ones leave no registers for the jobs' fields.
+bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5; }
+
+bool gemm_group_ok(const GemmLaunch* L, int n) {
+  if (n < 1 || n > kMaxModuli) return false;
+  if (!group_cfg(choose_cfg(L[0].M, L[0].N))) return false;
+  for (int j = 0; j < n; ++j) {
+    const GemmLaunch& a = L[j];
+    if (a.fmt != kFmtE2M1 || a.shared || a.accumulate || a.r < 1 || a.r > kGroupProducts) return false;
+    if (a.M != L[0].M || a.N != L[0].N || a.K != L[0].K || a.k_begin != L[0].k_begin ||
+        a.k_end != L[0].k_end || a.k_end <= a.k_begin)
+      return false;
+    if (a.c_type != L[0].c_type || a.log2D != L[0].log2D || a.outer != L[0].outer || a.ldc != L[0].ldc ||
+        a.stride_a != L[0].stride_a || a.stride_b != L[0].stride_b)
+      return false;
+  }
+  return true;
+}
+
+awe_status launch_gemm_group(const GemmLaunch* L, int n, hipStream_t stream) {
+  if (!gemm_group_ok(L, n)) {
+    set_error("these GEMMs cannot share one launch");
+    return AWE_ERR_UNSUPPORTED;
+  }
+  if (L[0].M == 0 || L[0].N == 0) return AWE_OK;
+  // the jobs with the most products first: the short ones fill the last rounds
+  int order[kMaxModuli];
+  for (int j = 0; j < n; ++j) order[j] = j;
+  std::stable_sort(order, order + n, [&](int a, int b) { return L[a].r > L[b].r; });
+  switch (choose_cfg(L[0].M, L[0].N)) {
+    case 4: return launch_group_tile<Cfg8w64x64k4>(L, order, n, stream);
+    case 5: return launch_group_tile<Cfg8w64x64k4p3>(L, order, n, stream);
+    default: return launch_group_tile<Cfg8w64x64>(L, order, n, stream);
   }
 }
 

@@ -37,11 +37,27 @@ def kernel_source_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+_LABELS = (  # first match wins
+    ("residue_encode_kernel<true>", "residue_encode_kernel (B side, transposed)"),
+    ("residue_encode_kernel<false>", "residue_encode_kernel (A side)"),
+    ("residues_kernel", "residues_kernel"),
+    ("crt_kernel", "crt_kernel"),
+    ("gemm_group_kernel", "gemm_group_kernel"),
+    ("gemm_kernel", "gemm_kernel"),
+    ("encode16_kernel<true>", "encode16_kernel (B side, transposed)"),
+    ("encode16_kernel<false>", "encode16_kernel (A side)"),
+    ("encode_kernel<true>", "encode_kernel (B side, transposed)"),
+    ("encode_kernel<false>", "encode_kernel (A side)"),
+    ("zero_tiles_kernel", "zero_tiles_kernel"),
+    ("fill_zero_kernel", "fill_zero_kernel"),
+    ("distribution_elementwise", "input generation (torch random)"),
+)
+
+
 def _short(name):
-    for key in ("gemm_kernel", "encode_kernel<true>", "encode_kernel<false>", "fill_zero_kernel"):
+    for key, label in _LABELS:
         if key in name:
-            return {"encode_kernel<true>": "encode_kernel (B side, transposed)",
-                    "encode_kernel<false>": "encode_kernel (A side)"}.get(key, key)
+            return label
     return name[:60]
 
 

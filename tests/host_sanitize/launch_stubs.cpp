@@ -7,6 +7,8 @@ namespace awe {
 int g_launches = 0;
 awe_status launch_encode(const EncodeLaunch&, hipStream_t) { ++g_launches; return AWE_OK; }
 awe_status launch_gemm(const GemmLaunch&, hipStream_t) { ++g_launches; return AWE_OK; }
+bool gemm_group_ok(const GemmLaunch*, int n) { return n >= 1 && n <= kMaxModuli; }
+awe_status launch_gemm_group(const GemmLaunch*, int, hipStream_t) { ++g_launches; return AWE_OK; }
 awe_status launch_residues(const int64_t*, int64_t, int64_t, int64_t, int64_t, const ResidueParams&, uint8_t*,
                            int64_t, int32_t*, hipStream_t) {
   ++g_launches;

@@ -73,3 +73,15 @@ def test_clock_table_from_bench_line(tmp_path):
     assert gemm[1:] == ["2000 (1950..2050)", "1380", "4040.0", "0.482", "0.400"]
     probe = [c.strip() for c in rows[1].strip("|").split("|")]
     assert probe[2] == "n/a" and probe[4] == "n/a" and probe[5] == "0.630"
+
+
+def test_kernel_labels():
+    from paper_2609_24519_amd import profiling
+
+    ns = "void awe::(anonymous namespace)::"
+    assert profiling._short(ns + "residue_encode_kernel<true>(awe::ResidueEncodeArgs)") == \
+        "residue_encode_kernel (B side, transposed)"
+    assert profiling._short(ns + "encode_kernel<true>(unsigned char const*)") == "encode_kernel (B side, transposed)"
+    assert profiling._short(ns + "encode_kernel<false>(unsigned char const*)") == "encode_kernel (A side)"
+    assert profiling._short(ns + "gemm_group_kernel<Cfg<4> >(GroupArgs)") == "gemm_group_kernel"
+    assert profiling._short(ns + "gemm_kernel<Cfg<4> >(GemmArgs)") == "gemm_kernel"

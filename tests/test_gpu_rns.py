@@ -143,6 +143,24 @@ def test_gemm_crt_full(shape):
     assert np.array_equal(c64.cpu().numpy(), ocrt.to_double(ref))
 
 
+@pytest.mark.parametrize("grouped,cfg", [("1", None), ("0", None), ("1", "4"), ("1", "1"), ("1", "6")])
+def test_gemm_crt_grouped_launch(monkeypatch, grouped, cfg):
+    # the moduli's GEMMs run as one grouped launch (jobs with the most products first) or,
+    # with AWE_GEMM_GROUPED=0 or a tile configuration the grouped kernel lacks (6), one launch
+    # per modulus; 9 tiles per modulus (256 x 128) are not a multiple of the 8 XCDs
+    monkeypatch.setenv("AWE_GEMM_GROUPED", grouped)
+    if cfg is not None:
+        monkeypatch.setenv("AWE_GEMM_CFG", cfg)
+    ms = _moduli()
+    M, N, K = 700, 300, 2000
+    A, B = _int53_pair(M, N, K, seed=5)
+    c128, c64 = awe.matmul_crt(to_dev(A), to_dev(B), ms, B53, B53)
+    torch.cuda.synchronize()
+    ref = og.gemm_i128(A, B)
+    assert (_words_to_ints(c128) == ref).all()
+    assert np.array_equal(c64.cpu().numpy(), ocrt.to_double(ref))
+
+
 def test_gemm_crt_extremes():
     # every product at the bound: C = -K B^2 needs 120 bits and the top of the range
     ms = _moduli()

@@ -536,10 +536,12 @@ __global__ __launch_bounds__(256) void zero_tiles_kernel(GemmArgs g, int bm, int
 }
 
 // One workgroup's output tile over reduction stages t_beg .. t_end - 1 (part >= 0: one
-// part of a split tile, added into C).  fold_ell: the fold coefficient of each product.
-template <class C>
-__device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int32_t* fold_ell, int tile, int part,
-                                          int t_beg, int t_end) {
+// part of a split tile, added into C).  fold_coef(p): the fold coefficient of product p.
+// The arguments come by value: through a reference the compiler keeps more of them live
+// (the 256 x 192 tiles then spill).
+template <class C, class FoldCoef>
+__device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int tile, int part, int t_beg,
+                                          int t_end) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -651,7 +653,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int32_t* fold
         buf = nbuf;
       }
       if ((g.fold_mask >> p) & 1u) {
-        const int32_t l = fold_ell[p];
+        const int32_t l = fold_coef(p);
         // one 32x32 block at a time keeps the temporaries of the fold small
 #pragma unroll
         for (int i = 0; i < C::BMW; ++i)
@@ -706,7 +708,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
     t_end = min(g.t_end, t_beg + per);
     if (t_beg >= t_end) return;  // the host splits only ranges of at least 2 stages per part
   }
-  gemm_tile<C>(g, g.fold_ell, tile, part, t_beg, t_end);
+  gemm_tile<C>(g, [&](int p) { return g.fold_ell[p]; }, tile, part, t_beg, t_end);
 }
 
 // Several GEMMs of one shape in one launch (the residue route's moduli): job j's tiles are
@@ -755,10 +757,11 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_group_kernel(GroupArgs ga)
   g.r = uniform(jb.r);
   g.modulus = uniform(jb.modulus);
   g.ts = uniform(jb.ts);
-  int32_t fold_ell[kGroupProducts];
-#pragma unroll
-  for (int k = 0; k < kGroupProducts; ++k) fold_ell[k] = uniform(jb.fold_ell[k]);
-  gemm_tile<C>(g, fold_ell, tile, -1, g.t_begin, g.t_end);
+  static_assert(kGroupProducts == 4, "the fold coefficients below");
+  const int32_t f0 = uniform(jb.fold_ell[0]), f1 = uniform(jb.fold_ell[1]), f2 = uniform(jb.fold_ell[2]),
+                f3 = uniform(jb.fold_ell[3]);
+  gemm_tile<C>(g, [=](int p) { return p == 0 ? f0 : p == 1 ? f1 : p == 2 ? f2 : f3; }, tile, -1, g.t_begin,
+               g.t_end);
 }
 
 // The tile configurations the launcher chooses from: waves (M x N), 32x32

@@ -60,8 +60,10 @@ def build(verbose=False):
     return _compile(SOURCES, LIB, verbose)
 
 
-def resources(out_md):
-    """Per-kernel register / spill / LDS figures from the gfx950 code object metadata."""
+def kernel_resources():
+    """Per-kernel register / spill / LDS figures from the gfx950 code object metadata: a list of
+    (name, vgpr, agpr, sgpr, vgpr spill, sgpr spill, static LDS, scratch, max workgroup) with the
+    mangled name's namespace prefix removed."""
     import re
     import tempfile
 
@@ -86,6 +88,12 @@ def resources(out_md):
                          k.get(".vgpr_spill_count"), k.get(".sgpr_spill_count"),
                          k.get(".group_segment_fixed_size"), k.get(".private_segment_fixed_size"),
                          k.get(".max_flat_workgroup_size")))
+    return rows
+
+
+def resources(out_md):
+    """kernel_resources() as a Markdown table."""
+    rows = kernel_resources()
     lines = ["# Kernel resources (gfx950 code object metadata)", "",
              "Command: `python -m paper_2609_24519_amd.build --resources %s`" % out_md, "",
              "VGPR is the unified count (arch + accumulation registers); the GEMM's LDS ring is",

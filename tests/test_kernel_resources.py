@@ -1,0 +1,51 @@
+"""Register budget of the kernels, from the gfx950 code object (hipcc cross-compiles here,
+no GPU needed): the GEMM configurations the library picks by default, the grouped GEMM and
+every encoder, residue and reconstruction kernel must run without scratch memory (a spill of
+the accumulators to scratch costs the GEMM ~20 %)."""
+import os
+import shutil
+
+import pytest
+
+from paper_2609_24519_amd import build
+
+
+def _cfg(*t):
+    return "CfgI" + "".join("Li%dE" % v for v in t) + "EE"
+
+
+# (waves M, waves N, blocks M, blocks N, k-steps per stage, stages, read-ahead, format, planes)
+DEFAULTS = {
+    "E2M1 256x128, 3 k-steps ahead (default)": _cfg(4, 2, 2, 2, 4, 3, 3, 0, 1),
+    "E2M1 256x192, 4 k-steps per stage": _cfg(4, 2, 2, 3, 4, 2, 1, 0, 1),
+    "E2M1 256x192, 5 stages": _cfg(4, 2, 2, 3, 2, 5, 1, 0, 1),
+    "E2M1 256x192, in place": _cfg(4, 2, 2, 3, 4, 2, 0, 0, 1),
+    "E4M3": _cfg(4, 2, 2, 2, 2, 3, 1, 1, 1),
+    "E2M3 (default)": _cfg(4, 2, 2, 2, 4, 2, 1, 2, 1),
+    "E2M3 weights in the scales": _cfg(4, 2, 2, 2, 2, 2, 1, 2, 2),
+}
+
+
+@pytest.fixture(scope="module")
+def rows():
+    h = build.hipcc()
+    if not (os.path.exists(h) or shutil.which(h)):
+        pytest.skip("hipcc not found")
+    return build.kernel_resources()
+
+
+def test_default_gemm_configurations_do_not_spill(rows):
+    for label, frag in DEFAULTS.items():
+        hits = [r for r in rows if "gemm_kernel" in r[0] and "group" not in r[0] and frag in r[0]]
+        assert hits, label
+        for r in hits:
+            assert r[4] == 0 and r[7] == 0, (label, r)
+    groups = [r for r in rows if "gemm_group_kernel" in r[0]]
+    assert groups and all(r[4] == 0 and r[7] == 0 for r in groups), groups
+
+
+def test_other_kernels_use_no_scratch(rows):
+    for r in rows:
+        if "gemm" in r[0]:
+            continue
+        assert r[7] == 0, r

@@ -92,8 +92,8 @@ typedef enum awe_encoding {
                           the base-13 limbs, C = sum_j 13^j P_j (Sec. 6.2).  A is int8 in [-1, 1]. */
   AWE_ENC_FP16 = 7,    /* FP16-significand integers x FP16-significand integers in 12 products,
                           w = v = (1, 9, 71, 639), D = 2 (App. A).  Both operands are int16 in
-                          [-2048, 2047]; the products run as four launches, one per outer weight
-                          71^(k+l), each adding its share into C. */
+                          [-2048, 2047]; the products run as three launches, one per outer weight
+                          71^(k+l) (k + l = 0, 1, 2), each adding its share into C. */
   AWE_ENC_FP8FP4 = 8,  /* INT8 x INT8 with 2 FP8 (E4M3) products and 1 FP4 product (App. A):
                           A = 13 h + 5 eps, planes h, h + eps (E4M3, 2 KiB bricks, see the
                           layout above) and eps (E2M1); AB = 104 P1 + 65 P2 - 40 P3. */

@@ -219,7 +219,7 @@ def test_ternary_4096_sampled():
 @pytest.mark.parametrize("shape,out", [((70, 45, 500), torch.int32), ((130, 260, 2000), torch.int64),
                                        ((33, 40, 16384), torch.int64), ((16, 24, 120_000), torch.int64)])
 def test_fp16_12_products(shape, out):
-    # App. A: 12-bit integers (FP16 significands) in 12 FP4 products, run as four launch
+    # App. A: 12-bit integers (FP16 significands) in 12 FP4 products, run as three launch
     # groups with outer weights 71^(k+l); the last shape needs several reduction launches
     M, N, K = shape
     rng = np.random.default_rng(M + N + K)

@@ -2,13 +2,14 @@
 // sizes, argument checks, the residue set's constants) with the device launchers stubbed out.
 // Built with -fsanitize=address,undefined by tests/test_host_sanitizers.py; any sanitizer report
 // aborts, and every status this program expects is checked.
+#include <atomic>
 #include <cstdio>
 #include <vector>
 
 #include "awe.h"
 
 namespace awe {
-extern int g_launches;
+extern std::atomic<int> g_launches;
 }
 
 static int failures = 0;
@@ -95,6 +96,6 @@ int main() {
          AWE_ERR_INVALID_VALUE, "crt, moduli not coprime");
   expect(awe_residues((const int64_t*)fake, 300, 200, 200, 1000, set, 33, (uint8_t*)fake, 60000, nullptr, nullptr),
          AWE_ERR_INVALID_VALUE, "residues, too many moduli");
-  std::printf("schemes %d launches %d failures %d\n", schemes, awe::g_launches, failures);
+  std::printf("schemes %d launches %d failures %d\n", schemes, awe::g_launches.load(), failures);
   return failures ? 1 : 0;
 }

@@ -1,10 +1,12 @@
 // Host-only stand-ins for the device launchers of libawe: with these, the table builder and the
 // C ABI's argument checks link and run without a GPU (and under the host sanitizers).  Each stub
 // only counts its calls.
+#include <atomic>
+
 #include "awe_internal.h"
 
 namespace awe {
-int g_launches = 0;
+std::atomic<int> g_launches{0};  // atomic: the thread test calls the ABI from several threads
 awe_status launch_encode(const EncodeLaunch&, hipStream_t) { ++g_launches; return AWE_OK; }
 awe_status launch_gemm(const GemmLaunch&, hipStream_t) { ++g_launches; return AWE_OK; }
 bool gemm_group_ok(const GemmLaunch*, int n) { return n >= 1 && n <= kMaxModuli; }

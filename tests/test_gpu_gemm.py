@@ -101,6 +101,25 @@ def test_forced_fold_segments(enc, kseg):
     assert np.array_equal(C.cpu().numpy().astype(np.int64), og.gemm_i64(A, B))
 
 
+def test_concurrent_streams():
+    # the library keeps no device state between calls: two GEMMs of different encodings and
+    # shapes enqueued on two streams at once (default priority) both stay exact
+    A1, B1 = _operands(awe.ENC_AWE6, 700, 500, 3000, seed=31)
+    A2, B2 = _operands(awe.ENC_FP6P4, 600, 900, 2100, seed=32)
+    pa1, pb1 = _planes(awe.ENC_AWE6, 0, A1, B1)
+    pa2, pb2 = _planes(awe.ENC_FP6P4, 0, A2, B2)
+    torch.cuda.synchronize()
+    C1 = torch.empty((700, 500), dtype=torch.int32, device="cuda")
+    C2 = torch.empty((600, 900), dtype=torch.int64, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for _ in range(3):
+        awe.gemm_planes(awe.ENC_AWE6, 0, 700, 500, 3000, pa1, pb1, C1, 500, awe.I32, 0, s1)
+        awe.gemm_planes(awe.ENC_FP6P4, 0, 600, 900, 2100, pa2, pb2, C2, 900, awe.I64, 0, s2)
+    torch.cuda.synchronize()
+    assert np.array_equal(C1.cpu().numpy().astype(np.int64), og.gemm_i64(A1, B1))
+    assert np.array_equal(C2.cpu().numpy(), og.gemm_i64(A2, B2))
+
+
 def test_ldc_larger_than_n():
     M, N, K = 70, 50, 300
     A, B = inputs.int8_pair(M, N, K, seed=2)

@@ -22,6 +22,11 @@
  *    enqueued and returned as a status; nothing is written then.  No C++
  *    exception crosses this interface.  awe_last_error() gives detail.
  *  - Results are bit-exact and do not depend on the launch configuration.
+ *  - awe_encode, awe_gemm_planes, awe_gemm_exact and awe_gemm_mod enqueue only kernels (no
+ *    memset, no copy), so they can be captured into a HIP graph once each has been called
+ *    eagerly on the device (the first calls set the GEMM's LDS limit and, for the FP16
+ *    scheme, upload its code table).  awe_gemm_crt also copies host tables and is not meant
+ *    for capture.
  *  - Matrices are row-major: A is M x K (A[i*lda + k]), B is K x N
  *    (B[k*ldb + j]), C is M x N (C[i*ldc + j]).  Leading dimensions must be
  *    at least the row length.  Empty problems (M or N zero) succeed and write

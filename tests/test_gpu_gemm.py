@@ -120,6 +120,39 @@ def test_concurrent_streams():
     assert np.array_equal(C2.cpu().numpy(), og.gemm_i64(A2, B2))
 
 
+def test_graph_capture_replays():
+    # encode A, encode B and the GEMM captured into one HIP graph (after an eager call, which
+    # also sets the kernels' LDS limits): every replay, with eager work and synchronisations in
+    # between, gives the exact product; nothing in these calls records a memset
+    M, N, K = 520, 300, 1500
+    A, B = _operands(awe.ENC_AWE6, M, N, K, seed=41)
+    Ad, Bd = to_dev(A), to_dev(B)
+    pa = torch.empty(awe.plane_bytes(awe.ENC_AWE6, 0, awe.SIDE_A, M, K), dtype=torch.uint8, device="cuda")
+    pb = torch.empty(awe.plane_bytes(awe.ENC_AWE6, 0, awe.SIDE_B, N, K), dtype=torch.uint8, device="cuda")
+    C = torch.empty((M, N), dtype=torch.int32, device="cuda")
+
+    def step():
+        awe.encode(awe.ENC_AWE6, 0, awe.SIDE_A, Ad, M, K, K, pa)
+        awe.encode(awe.ENC_AWE6, 0, awe.SIDE_B, Bd, N, K, N, pb)
+        awe.gemm_planes(awe.ENC_AWE6, 0, M, N, K, pa, pb, C, N, awe.I32)
+
+    ref = og.gemm_i64(A, B)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        step()
+    for rep in range(3):
+        C.fill_(-7)
+        pa.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(C.cpu().numpy().astype(np.int64), ref), rep
+
+
 def test_ldc_larger_than_n():
     M, N, K = 70, 50, 300
     A, B = inputs.int8_pair(M, N, K, seed=2)

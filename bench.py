@@ -258,6 +258,8 @@ def main():
             probe["gemm_frac_of_8_wave_rate"] = round(gemm_tflops / probe["8_waves_per_cu_TFLOPs"], 4)
             probe["gemm_frac_of_varied_operand_rate"] = round(
                 gemm_tflops / probe["varied_operands_8_waves_per_cu_TFLOPs"], 4)
+            probe["gemm_frac_of_varied_operand_16x16x128_rate"] = round(
+                gemm_tflops / probe["varied_operands_16x16x128_8_waves_per_cu_TFLOPs"], 4)
         line["mfma_sustained"] = probe
     if sampler is not None:
         line["clock_under_load"] = clock_under_load(sampler, clock_dir, awe, M, N, K, stream)
@@ -400,6 +402,15 @@ def mfma_sustained(iters=20000):
         best = tf.value
     out["varied_operands_8_waves_per_cu_TFLOPs"] = round(best, 1)
     out["varied_operands_frac_of_peak"] = round(best / FP4_PEAK_TFLOPS, 4)
+    # the same on the 16x16x128 form of the MFMA, which sustains more on changing operands
+    lib.awe_mfma_peak_varied16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    for _ in range(2):
+        tf = ctypes.c_double(0.0)
+        rc = lib.awe_mfma_peak_varied16(8, 10 * iters, ctypes.byref(tf))
+        if rc != 0:
+            return {"error": "HIP error %d" % rc}
+    out["varied_operands_16x16x128_8_waves_per_cu_TFLOPs"] = round(tf.value, 1)
+    out["varied_operands_16x16x128_frac_of_peak"] = round(tf.value / FP4_PEAK_TFLOPS, 4)
     lib.awe_mfma_peak_varied_fmt.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                              ctypes.POINTER(ctypes.c_double)]
     for fmt, name in ((2, "e2m3"), (0, "e4m3")):

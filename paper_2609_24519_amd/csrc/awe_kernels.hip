@@ -8,6 +8,7 @@
 #include <mutex>
 #include <set>
 #include <string>
+#include <type_traits>
 
 #include "awe_internal.h"
 
@@ -23,6 +24,7 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 struct LutArg {
   uint32_t v[256];
@@ -225,19 +227,29 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
 template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0,
-          int NPL_ = 1>
+          int NPL_ = 1, int MF_ = 32>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
-  static constexpr int KST = KST_;        // k-steps (64 reduction indices each) per stage
+  static constexpr int KST = KST_;        // bricks (64 reduction indices each) per row block and stage
   static constexpr int KT = 64 * KST;     // reduction indices per stage
   static constexpr int NSTAGE = NSTAGE_;  // LDS ring depth
+  // MFMA shape: 32 (32x32x64: one k-step is one brick) or 16 (16x16x128: one k-step is two
+  // bricks; a wave's 32x32 block is four 16x16 MFMA blocks).  Both read the same operand
+  // bytes from LDS per MAC for a given wave tile; on changing operands the 16x16x128 form
+  // sustains a higher rate at the board's power limit.
+  static constexpr int MF = MF_;
+  static_assert(MF == 32 || (MF == 16 && FMT_ == 0 && NPL_ == 1 && KST % 2 == 0), "MFMA shape");
+  static constexpr int KSTEPS = MF == 16 ? KST / 2 : KST;  // MFMA k-steps per stage
   // Fragments are read PD k-steps before their MFMAs, into NSETS register sets
-  // (k-step ks of every stage uses set ks % NSETS, so NSETS divides KST).  PD = 0
+  // (k-step ks of every stage uses set ks % NSETS, so NSETS divides KSTEPS).  PD = 0
   // reads each k-step's fragments right before its MFMAs into a single set (the
   // other wave of the SIMD covers the wait), which saves one set of registers.
   static constexpr int PD = PD_;
-  static constexpr int NSETS = PD == 0 ? 1 : (PD == 1 ? 2 : KST);
-  static_assert(PD == 0 || (PD < NSETS && KST % NSETS == 0), "fragment prefetch distance");
+  static constexpr int NSETS = PD == 0 ? 1 : (PD == 1 ? 2 : KSTEPS);
+  static_assert(PD == 0 || (PD < NSETS && KSTEPS % NSETS == 0), "fragment prefetch distance");
+  // Accumulator blocks per wave (M x N) and FP32 values per lane and block.
+  static constexpr int AM = MF == 16 ? 2 * BMW : BMW, AN = MF == 16 ? 2 * BNW : BNW;
+  static constexpr int AV = MF == 16 ? 4 : 16;
   // Operand element format and its storage unit: 0 E2M1, one k-step in 1 KiB (16 bytes
   // per lane); 1 E4M3, one k-step in 2 KiB (32 bytes per lane); 2 E2M3, two k-steps in
   // 3 KiB (24 bytes per lane and k-step).  Units move as 1 KiB copies.
@@ -421,12 +433,36 @@ __device__ __forceinline__ v8i frag_fmt(const uint8_t* unit, int i, int lane) {
 // The wave's operand fragments for one k-step (64 reduction indices) of a stage.
 template <class C>
 struct Frags {
-  v8i a[C::NPL * C::BMW], b[C::NPL * C::BNW];  // plane pl's fragments at pl * BMW (pl * BNW)
+  // plane pl's fragments at pl * BMW (pl * BNW); 16x16x128: one per 16-row block
+  v8i a[C::MF == 16 ? C::AM : C::NPL * C::BMW], b[C::MF == 16 ? C::AN : C::NPL * C::BNW];
 };
+
+// 16x16x128 operand fragment: lane L holds row (column) L % 16 of its 16-row block at
+// reduction indices 32 (L / 16) .. 32 (L / 16) + 31 of the k-step's 128, i.e. the 16
+// bytes that lane (L / 16 % 2) * 32 + row of brick L / 32 holds in the stored layout.
+__device__ __forceinline__ uint32_t frag16_lane_offset(int lane) {
+  const int q = lane >> 4;
+  return (uint32_t)((q >> 1) * kBrickBytes + ((q & 1) * 32 + (lane & 15)) * 16);
+}
 
 template <class C>
 __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, int ks, int wm,
                                            int wn, int lane) {
+  if constexpr (C::MF == 16) {
+    const uint32_t lo = frag16_lane_offset(lane);
+#pragma unroll
+    for (int ia = 0; ia < C::BMW; ++ia)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        f.a[2 * ia + h] = frag(stage + ((wm * C::BMW + ia) * C::KU + 2 * ks) * C::UNIT_BYTES + h * 256 + lo);
+#pragma unroll
+    for (int j = 0; j < C::BNW; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        f.b[2 * j + h] =
+            frag(stage + (C::A_UNITS + (wn * C::BNW + j) * C::KU + 2 * ks) * C::UNIT_BYTES + h * 256 + lo);
+    return;
+  }
   const int u = ks / C::UK, i = ks % C::UK;
 #pragma unroll
   for (int pl = 0; pl < C::NPL; ++pl) {
@@ -550,14 +586,15 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   const int wm = wave / C::WN, wn = wave % C::WN;
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
 
-  v16f acc[C::BMW][C::BNW];
-  int32_t iacc[C::BMW][C::BNW][16];
+  using AccT = std::conditional_t<C::MF == 16, v4f, v16f>;
+  AccT acc[C::AM][C::AN];
+  int32_t iacc[C::AM][C::AN][C::AV];
 #pragma unroll
-  for (int i = 0; i < C::BMW; ++i)
+  for (int i = 0; i < C::AM; ++i)
 #pragma unroll
-    for (int j = 0; j < C::BNW; ++j)
+    for (int j = 0; j < C::AN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
+      for (int v = 0; v < C::AV; ++v) {
         acc[i][j][v] = 0.0f;
         iacc[i][j][v] = 0;
       }
@@ -591,8 +628,8 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
         const uint32_t cur_off = buf * C::STAGE_BYTES;
         const int nbuf = buf + 1 == NSTAGE ? 0 : buf + 1;
 #pragma unroll
-        for (int ks = 0; ks < C::KST; ++ks) {
-          if (ks == C::KST - PD) {
+        for (int ks = 0; ks < C::KSTEPS; ++ks) {
+          if (ks == C::KSTEPS - PD) {
             wait_stages<C, NSTAGE - 2>(wave);
             wait_lgkm0();
             block_barrier();
@@ -600,15 +637,22 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
             cursor_next(nxt, g, t_end);
           }
           const int kr = ks + PD;  // k-step whose fragments are read now
-          if (kr < C::KST)
+          if (kr < C::KSTEPS)
             read_frags<C>(f[kr % NSETS], smem + cur_off, kr, wm, wn, lane);
           else
-            read_frags<C>(f[kr % NSETS], smem + nbuf * C::STAGE_BYTES, kr - C::KST, wm, wn, lane);
+            read_frags<C>(f[kr % NSETS], smem + nbuf * C::STAGE_BYTES, kr - C::KSTEPS, wm, wn, lane);
           // in place (PD = 0) the MFMAs wait for these reads; read ahead, the reads are
           // spread between the MFMAs below
           if constexpr (PD == 0) __builtin_amdgcn_sched_barrier(0);
           const Frags<C>& cur = f[ks % NSETS];
-          if constexpr (C::NPL == 2) {
+          if constexpr (C::MF == 16) {
+#pragma unroll
+            for (int i = 0; i < C::AM; ++i)
+#pragma unroll
+              for (int j = 0; j < C::AN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(cur.a[i], cur.b[j], acc[i][j], 4, 4,
+                                                                             0, kScale2, 0, kScale2);
+          } else if constexpr (C::NPL == 2) {
             // the four plane pairs, each block's MFMAs four apart in issue order
 #pragma unroll
             for (int q = 0; q < 4; ++q)
@@ -636,7 +680,7 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
             // issue order: one MFMA, then one fragment read of a later k-step (measured
             // 1-3 % faster than all reads ahead of the MFMAs)
 #pragma unroll
-            for (int q = 0; q < C::NPL * C::NPL * C::BMW * C::BNW; ++q) {
+            for (int q = 0; q < C::NPL * C::NPL * C::AM * C::AN; ++q) {
               __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // an MFMA
               __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // an LDS read
             }
@@ -656,11 +700,11 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
         const int32_t l = fold_coef(p);
         // one 32x32 block at a time keeps the temporaries of the fold small
 #pragma unroll
-        for (int i = 0; i < C::BMW; ++i)
+        for (int i = 0; i < C::AM; ++i)
 #pragma unroll
-          for (int j = 0; j < C::BNW; ++j) {
+          for (int j = 0; j < C::AN; ++j) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
+            for (int v = 0; v < C::AV; ++v) {
               // (two planes per side: the weights are in the scales, the partial may use
               // all 24 bits, and it is added unmultiplied)
               if constexpr (C::NPL == 2)
@@ -676,16 +720,19 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   }
   wait_vmcnt<0>();  // the saturated copies past the end must land before the wave exits
 
-  // Epilogue: exact shift by log2 D, or the non-negative residue mod m.
-  const int row0 = tm * C::BM + wm * (32 * C::BMW) + 4 * (lane >> 5);
-  const int col0 = tn * C::BN + wn * (32 * C::BNW) + (lane & 31);
+  // Epilogue: exact shift by log2 D, or the non-negative residue mod m.  Output layout of
+  // the MFMA: 32x32 blocks, lane L holds rows 8 (v / 4) + 4 (L / 32) + v % 4 of column L % 32;
+  // 16x16 blocks, rows 4 (L / 16) + v of column L % 16.
+  constexpr int BS = C::MF;  // rows and columns of an accumulator block
+  const int row0 = tm * C::BM + wm * (32 * C::BMW) + (BS == 16 ? 4 * (lane >> 4) : 4 * (lane >> 5));
+  const int col0 = tn * C::BN + wn * (32 * C::BNW) + (lane & (BS - 1));
 #pragma unroll
-  for (int i = 0; i < C::BMW; ++i)
+  for (int i = 0; i < C::AM; ++i)
 #pragma unroll
-    for (int j = 0; j < C::BNW; ++j)
+    for (int j = 0; j < C::AN; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = row0 + i * 32 + 8 * (v >> 2) + (v & 3), col = col0 + j * 32;
+      for (int v = 0; v < C::AV; ++v) {
+        const int row = row0 + i * BS + (BS == 16 ? v : 8 * (v >> 2) + (v & 3)), col = col0 + j * BS;
         if (part < 0)
           store_output(g, row, col, iacc[i][j][v]);
         else
@@ -776,6 +823,10 @@ using Cfg8w64x64e4m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 1>;  // 256 x 128, 8 waves, E4M3
 using Cfg8w64x96k4 = Cfg<4, 2, 2, 3, 4, 2>;         // 256 x 192, 8 waves, 4 k-steps, 2 stages
 using Cfg8w64x96s5 = Cfg<4, 2, 2, 3, 2, 5>;         // 256 x 192, 8 waves, 2 k-steps, 5 stages
 using Cfg8w64x96k4p0 = Cfg<4, 2, 2, 3, 4, 2, 0>;    // as 6, fragments read in place
+// 16x16x128 MFMAs (one k-step = two bricks)
+using Cfg8w64x64k4m16 = Cfg<4, 2, 2, 2, 4, 3, 1, 0, 1, 16>;   // 256 x 128, 8 waves, 2 k-steps of 128 per stage
+using Cfg8w64x64k4p0m16 = Cfg<4, 2, 2, 2, 4, 3, 0, 0, 1, 16>; // as above, fragments read in place
+using Cfg8w64x96k4m16 = Cfg<4, 2, 2, 3, 4, 2, 0, 0, 1, 16>;   // 256 x 192, 8 waves, 2 stages, in place
 // E2M3 operands (3 KiB units of two k-steps)
 using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
 using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
@@ -822,13 +873,15 @@ double rounds(int64_t tiles, int cus) {
 // 1: 256x128 with 8 waves, 2: 256x192 with 8 waves, 3 and 4: as 0 and 1 with
 // 4 k-steps per stage, 5: as 4 with fragments read three k-steps ahead, 6:
 // 256x192 with 4 k-steps per stage in 2 stages, 7: 256x192 with 2 k-steps per
-// stage in 5 stages, 8: as 6 with fragments read in place) overrides the choice.
+// stage in 5 stages, 8: as 6 with fragments read in place, 9: as 4 on the 16x16x128
+// MFMA, 10: as 9 with fragments read in place, 11: 256x192 on the 16x16x128 MFMA, in
+// place) overrides the choice.
 // Otherwise: configuration 5, or 6 when its rounds of workgroups (each about
 // 1.48 times as long as a round of 5, measured at 8192^3) finish clearly sooner.
 int choose_cfg(int64_t M, int64_t N) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
-  if (forced >= 0 && forced <= 8) return forced;
+  if (forced >= 0 && forced <= 11) return forced;
   const int cus = compute_units();
   const int64_t tm = (M + 255) / 256;
   const double t128 = rounds(tm * ((N + 127) / 128), cus);
@@ -1124,6 +1177,9 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 6: return launch_tile<Cfg8w64x96k4>(g, L, stream);
     case 7: return launch_tile<Cfg8w64x96s5>(g, L, stream);
     case 8: return launch_tile<Cfg8w64x96k4p0>(g, L, stream);
+    case 9: return launch_tile<Cfg8w64x64k4m16>(g, L, stream);
+    case 10: return launch_tile<Cfg8w64x64k4p0m16>(g, L, stream);
+    case 11: return launch_tile<Cfg8w64x96k4m16>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }

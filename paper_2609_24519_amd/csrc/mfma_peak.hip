@@ -12,6 +12,7 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int kMfmaPerIter = 16;
 constexpr double kFlopPerMfma = 2.0 * 32 * 32 * 64;
@@ -61,11 +62,40 @@ __global__ __launch_bounds__(512) void mfma_varied_kernel(int iters, float* sink
   if (s == 0.125f) sink[blockIdx.x] = s;  // keeps the MFMAs live
 }
 
+// As mfma_varied_kernel with E2M1 operands on the 16x16x128 form of the scaled MFMA (the
+// same operand registers, half the FLOP per instruction): 32 MFMAs per iteration, the same
+// FLOP per iteration as 16 of the 32x32x64 form.
+__global__ __launch_bounds__(512) void mfma_varied16_kernel(int iters, float* sink) {
+  constexpr uint32_t kScale = 0x80808080u;
+  v4f c[8] = {};
+  v8i a[4], b[4];
+  uint32_t h = 0x9e3779b9u * (threadIdx.x + 1) + 0x85ebca6bu * blockIdx.x;
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      h ^= h << 13; h ^= h >> 17; h ^= h << 5;
+      a[s][j] = (int)h;
+      h ^= h << 13; h ^= h >> 17; h ^= h << 5;
+      b[s][j] = (int)h;
+    }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int m = 0; m < 2 * kMfmaPerIter; ++m)
+      c[m & 7] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[m & 3], b[(m >> 2) & 3], c[m & 7], 4, 4, 0,
+                                                                 kScale, 0, kScale);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s += c[i][0];
+  if (s == 0.125f) sink[blockIdx.x] = s;  // keeps the MFMAs live
+}
+
 }  // namespace
 
 namespace {
 
-template <int FMT, bool kVaried = false>
+template <int FMT, bool kVaried = false, bool k16 = false>
 int run_peak(int waves_per_cu, int iters, double* tflops) {
   if (waves_per_cu < 1 || waves_per_cu > 8 || iters < 1 || tflops == nullptr) return (int)hipErrorInvalidValue;
   int dev = 0, cus = 0;
@@ -79,7 +109,9 @@ int run_peak(int waves_per_cu, int iters, double* tflops) {
   const dim3 grid(cus), block(64 * waves_per_cu);
   if ((e = hipEventCreate(&e0)) == hipSuccess && (e = hipEventCreate(&e1)) == hipSuccess) {
     auto launch = [&]() {
-      if (kVaried)
+      if (k16)
+        hipLaunchKernelGGL(mfma_varied16_kernel, grid, block, 0, nullptr, iters, sink);
+      else if (kVaried)
         hipLaunchKernelGGL(mfma_varied_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
       else
         hipLaunchKernelGGL(mfma_peak_kernel<FMT>, grid, block, 0, nullptr, iters, sink);
@@ -133,4 +165,10 @@ extern "C" int awe_mfma_peak_fmt(int fmt, int waves_per_cu, int iters, double* t
     case 0: return run_peak<0>(waves_per_cu, iters, tflops);
     default: return (int)hipErrorInvalidValue;
   }
+}
+
+// As awe_mfma_peak_varied on the 16x16x128 form of the MFMA (E2M1 operands that change
+// between MFMAs).
+extern "C" int awe_mfma_peak_varied16(int waves_per_cu, int iters, double* tflops) {
+  return run_peak<4, true, true>(waves_per_cu, iters, tflops);
 }

@@ -234,13 +234,13 @@ def test_mod_forced_segments():
     assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
 
 
-@pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4", "5", "6", "7", "8"])
+@pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4", "5", "6", "7", "8", "9", "10", "11"])
 @pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13, awe.ENC_TERNARY])
 def test_every_tile_configuration(monkeypatch, cfg, enc):
     # AWE_GEMM_CFG forces one of the GEMM's tile configurations (256x128 on 4 or 8
     # waves with 2 or 4 k-steps per stage, 256x192 on 8 waves in 2 or 5 stages,
-    # fragments read one or three k-steps ahead or in place); every one must give the
-    # exact product
+    # fragments read one or three k-steps ahead or in place, 32x32x64 or 16x16x128
+    # MFMAs); every one must give the exact product
     monkeypatch.setenv("AWE_GEMM_CFG", cfg)
     M, N, K = 300, 420, 1100
     A, B = _operands(enc, M, N, K, seed=int(cfg) + 40)

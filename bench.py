@@ -11,7 +11,8 @@ as ``value``, the roofline of the dominant kernel (the GEMM) from HIP events
 on its stream, the 9-product base-13 baseline, the 2 FP8 + 1 FP4 scheme, the
 3-product {0,+-1} x INT8 GEMM, the 12-product FP16-significand GEMM, the
 native INT8 MFMA GEMM
-(hipBLASLt through torch._int_mm), the residue-number-system route for 53-bit
+(hipBLASLt through torch._int_mm), one plain MXFP4 GEMM of the vendor library
+(torch._scaled_mm), the residue-number-system route for 53-bit
 integers (the integer layer of Ozaki scheme II) and the sustained rate of the
 FP4 MFMA alone timed in the same run as context, and the oracle timed on the host's cores on
 a bounded sample.
@@ -202,6 +203,7 @@ def main():
             line["int8_mfma_context"]["equal_to_exact_C"] = bool(torch.equal(Ci, C))
         except Exception as ex:  # noqa: BLE001 - context only
             line["int8_mfma_context"] = {"error": str(ex)[:200]}
+        line["fp4_vendor_gemm_context"] = fp4_vendor_context(dev, M, N, K, stream)
     if not args.no_context:
         # INT8 x INT8 with 2 E4M3 products and 1 E2M1 product (App. A) on the same A and B;
         # an E4M3 MFMA runs at half the E2M1 rate, so the work is 5 FP4-product equivalents
@@ -356,6 +358,47 @@ def ozaki2_context(dev, M=4096, N=4096, K=16384, reps=3):
     del A, B, c128, c64, ws
     torch.cuda.empty_cache()
     return out
+
+
+def fp4_vendor_context(dev, M, N, K, stream):
+    """One plain MXFP4 GEMM of the same shape from the vendor library (hipBLASLt through
+    torch._scaled_mm: E2M1 operands with E8M0 block scales of 2^0, bf16 output) on random codes:
+    what one FP4 GEMM reaches on this board, next to the r plane products of the AWE GEMM.  Its
+    output is rounded to bf16, so it is checked only to one bf16 ulp on a 64 x 64 corner."""
+    import torch
+
+    try:
+        g = torch.Generator(device=dev).manual_seed(0)
+        a8 = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, device=dev, generator=g)
+        b8 = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=g)
+        a, b = a8.view(torch.float4_e2m1fn_x2), b8.view(torch.float4_e2m1fn_x2)
+        sa = torch.full((M, K // 32), 127, dtype=torch.uint8, device=dev).view(torch.float8_e8m0fnu)
+        sb = torch.full((N, K // 32), 127, dtype=torch.uint8, device=dev).view(torch.float8_e8m0fnu)
+        with torch.cuda.stream(stream):
+            out = torch._scaled_mm(a, b.t(), sa, sb, out_dtype=torch.bfloat16)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(10):
+                out = torch._scaled_mm(a, b.t(), sa, sb, out_dtype=torch.bfloat16)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 10
+        lut = torch.tensor([0, .5, 1, 1.5, 2, 3, 4, 6, 0, -.5, -1, -1.5, -2, -3, -4, -6], device=dev)
+
+        def decode(x8):
+            return torch.stack([lut[(x8 & 15).long()], lut[(x8 >> 4).long()]], -1).reshape(x8.shape[0], -1)
+
+        ref = decode(a8[:64]) @ decode(b8[:64]).t()
+        err = (out[:64, :64].float() - ref).abs()
+        # within one bf16 unit in the last place (its conversion does not round to nearest)
+        ok = bool((err <= ref.abs() * 2.0 ** -7 + 1e-6).all())
+        tf = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+        return {"library": "hipBLASLt via torch._scaled_mm (MXFP4, bf16 output)", "ms": round(ms, 4),
+                "fp4_TFLOPs": round(tf, 1), "fp4_peak_frac": round(tf / FP4_PEAK_TFLOPS, 4),
+                "within_1_bf16_ulp_64x64": ok}
+    except Exception as ex:  # noqa: BLE001 - context only
+        return {"error": str(ex)[:200]}
 
 
 def mfma_sustained(iters=20000):

@@ -33,7 +33,7 @@ def _encode(enc, m, side, X, rows, K, flag=None):
 
 
 @pytest.mark.parametrize("name", sorted(EXACT))
-@pytest.mark.parametrize("rows,K", [(32, 128), (70, 200), (1, 1), (257, 333)])
+@pytest.mark.parametrize("rows,K", [(32, 128), (70, 200), (1, 1), (257, 333), (160, 1000)])
 def test_encode_matches_oracle(name, rows, K):
     s = sc.ALL_SCHEMES[name]()
     rng = np.random.default_rng(rows * 1000 + K)

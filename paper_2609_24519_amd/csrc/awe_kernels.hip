@@ -227,7 +227,7 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
 template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0,
-          int NPL_ = 1, int MF_ = 32>
+          int NPL_ = 1, int MF_ = 32, int NLB_ = 0>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
   static constexpr int KST = KST_;        // bricks (64 reduction indices each) per row block and stage
@@ -272,7 +272,14 @@ struct Cfg {
   static constexpr int A_UNITS = NPL * PA_UNITS;
   static constexpr int B_UNITS = NPL * PB_UNITS;
   static constexpr int STAGE_BYTES = (A_UNITS + B_UNITS) * UNIT_BYTES;
-  static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES;
+  // The int32 fold accumulators of the last NLB accumulator blocks of every wave live in LDS
+  // after the ring (each wave its own 4 KiB per block, lane-major), so that a tile whose
+  // registers hold only its FP32 accumulators and part of its int32 ones still fits.
+  static constexpr int NLB = NLB_;
+  static_assert(NLB >= 0 && NLB < AM * AN && (NLB == 0 || MF == 32), "LDS fold blocks");
+  static constexpr int FOLD_LDS_OFFSET = NSTAGE * STAGE_BYTES;
+  static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES + NW * NLB * AV * 64 * 4;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS of one CU");
   // copies per wave and stage: A units evenly, B units round-robin (the first
   // B_UNITS % NW waves take one more)
   static constexpr int A_PW = A_UNITS / NW;
@@ -588,16 +595,28 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
 
   using AccT = std::conditional_t<C::MF == 16, v4f, v16f>;
   AccT acc[C::AM][C::AN];
+  // Blocks b = i * AN + j < NREG keep their int32 fold accumulators in iacc; the others in this
+  // wave's LDS fold area (int32 v of lane L of block b - NREG at ((b - NREG) * AV + v) * 64 + L).
+  constexpr int NREG = C::AM * C::AN - C::NLB;
   int32_t iacc[C::AM][C::AN][C::AV];
+  int32_t* const fold_lds =
+      reinterpret_cast<int32_t*>(smem + C::FOLD_LDS_OFFSET) + wave * (C::NLB * C::AV * 64) + lane;
+  // (register blocks and LDS blocks in separate loops: an expression that chooses between
+  // iacc and the LDS area would keep iacc out of registers)
 #pragma unroll
   for (int i = 0; i < C::AM; ++i)
 #pragma unroll
     for (int j = 0; j < C::AN; ++j)
 #pragma unroll
-      for (int v = 0; v < C::AV; ++v) {
-        acc[i][j][v] = 0.0f;
-        iacc[i][j][v] = 0;
-      }
+      for (int v = 0; v < C::AV; ++v) acc[i][j][v] = 0.0f;
+#pragma unroll
+  for (int b = 0; b < NREG; ++b)
+#pragma unroll
+    for (int v = 0; v < C::AV; ++v) iacc[b / C::AN][b % C::AN][v] = 0;
+#pragma unroll
+  for (int b = NREG; b < C::AM * C::AN; ++b)
+#pragma unroll
+    for (int v = 0; v < C::AV; ++v) fold_lds[((b - NREG) * C::AV + v) * 64] = 0;
 
   constexpr int NSTAGE = C::NSTAGE;
   Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
@@ -700,21 +719,30 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
         const int32_t l = fold_coef(p);
         // one 32x32 block at a time keeps the temporaries of the fold small
 #pragma unroll
-        for (int i = 0; i < C::AM; ++i)
+        for (int b = 0; b < NREG; ++b) {
+          const int i = b / C::AN, j = b % C::AN;
 #pragma unroll
-          for (int j = 0; j < C::AN; ++j) {
-#pragma unroll
-            for (int v = 0; v < C::AV; ++v) {
-              // (two planes per side: the weights are in the scales, the partial may use
-              // all 24 bits, and it is added unmultiplied)
-              if constexpr (C::NPL == 2)
-                iacc[i][j][v] += (int32_t)acc[i][j][v];
-              else
-                iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
-              acc[i][j][v] = 0.0f;
-            }
-            __builtin_amdgcn_sched_barrier(0);
+          for (int v = 0; v < C::AV; ++v) {
+            // (two planes per side: the weights are in the scales, the partial may use
+            // all 24 bits, and it is added unmultiplied)
+            if constexpr (C::NPL == 2)
+              iacc[i][j][v] += (int32_t)acc[i][j][v];
+            else
+              iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
+            acc[i][j][v] = 0.0f;
           }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int b = NREG; b < C::AM * C::AN; ++b) {
+          const int i = b / C::AN, j = b % C::AN;
+#pragma unroll
+          for (int v = 0; v < C::AV; ++v) {
+            fold_lds[((b - NREG) * C::AV + v) * 64] += __mul24(l, (int32_t)acc[i][j][v]);
+            acc[i][j][v] = 0.0f;
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
   }
@@ -726,18 +754,21 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   constexpr int BS = C::MF;  // rows and columns of an accumulator block
   const int row0 = tm * C::BM + wm * (32 * C::BMW) + (BS == 16 ? 4 * (lane >> 4) : 4 * (lane >> 5));
   const int col0 = tn * C::BN + wn * (32 * C::BNW) + (lane & (BS - 1));
+  auto emit = [&](int i, int j, int v, int32_t val) {
+    const int row = row0 + i * BS + (BS == 16 ? v : 8 * (v >> 2) + (v & 3)), col = col0 + j * BS;
+    if (part < 0)
+      store_output(g, row, col, val);
+    else
+      add_output(g, row, col, val);
+  };
 #pragma unroll
-  for (int i = 0; i < C::AM; ++i)
+  for (int b = 0; b < NREG; ++b)
 #pragma unroll
-    for (int j = 0; j < C::AN; ++j)
+    for (int v = 0; v < C::AV; ++v) emit(b / C::AN, b % C::AN, v, iacc[b / C::AN][b % C::AN][v]);
 #pragma unroll
-      for (int v = 0; v < C::AV; ++v) {
-        const int row = row0 + i * BS + (BS == 16 ? v : 8 * (v >> 2) + (v & 3)), col = col0 + j * BS;
-        if (part < 0)
-          store_output(g, row, col, iacc[i][j][v]);
-        else
-          add_output(g, row, col, iacc[i][j][v]);
-      }
+  for (int b = NREG; b < C::AM * C::AN; ++b)
+#pragma unroll
+    for (int v = 0; v < C::AV; ++v) emit(b / C::AN, b % C::AN, v, fold_lds[((b - NREG) * C::AV + v) * 64]);
 }
 
 template <class C>
@@ -827,6 +858,11 @@ using Cfg8w64x96k4p0 = Cfg<4, 2, 2, 3, 4, 2, 0>;    // as 6, fragments read in p
 using Cfg8w64x64k4m16 = Cfg<4, 2, 2, 2, 4, 3, 1, 0, 1, 16>;   // 256 x 128, 8 waves, 2 k-steps of 128 per stage
 using Cfg8w64x64k4p0m16 = Cfg<4, 2, 2, 2, 4, 3, 0, 0, 1, 16>; // as above, fragments read in place
 using Cfg8w64x96k4m16 = Cfg<4, 2, 2, 3, 4, 2, 0, 0, 1, 16>;   // 256 x 192, 8 waves, 2 stages, in place
+// 256 x 256 on 8 waves of 2 x 4 blocks, 2 k-steps per stage in 2 stages, fragments read in place;
+// the int32 fold accumulators of 3 of each wave's 8 blocks in LDS (96 KiB + a 64 KiB ring)
+using Cfg8w64x128lf = Cfg<4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3>;
+// as above with the fold accumulators of 2 blocks per wave in LDS (64 KiB) and a 3-stage ring
+using Cfg8w64x128lf3 = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2>;
 // E2M3 operands (3 KiB units of two k-steps)
 using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
 using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
@@ -875,18 +911,34 @@ double rounds(int64_t tiles, int cus) {
 // 256x192 with 4 k-steps per stage in 2 stages, 7: 256x192 with 2 k-steps per
 // stage in 5 stages, 8: as 6 with fragments read in place, 9: as 4 on the 16x16x128
 // MFMA, 10: as 9 with fragments read in place, 11: 256x192 on the 16x16x128 MFMA, in
-// place) overrides the choice.
-// Otherwise: configuration 5, or 6 when its rounds of workgroups (each about
-// 1.48 times as long as a round of 5, measured at 8192^3) finish clearly sooner.
-int choose_cfg(int64_t M, int64_t N) {
+// place, 12: 256x256 with the int32 fold accumulators of 3 blocks per wave in LDS and a
+// 2-stage ring, 13: as 12 with 2 blocks per wave in LDS and a 3-stage ring) overrides the
+// choice.  Otherwise the configuration whose rounds of workgroups finish first: 5, 6 (a round
+// about 1.48 times as long as a round of 5, measured at 8192^3; only when clearly sooner) or
+// 13.  A round takes about 2.2 k + 1700 time units for 5 and 3.9 k + 6000 for 13, k = r K / 6
+// reduction indices at r products (fitted to 4096^2 and 8192^2 tiles at K = 4096 .. 65536):
+// the larger tile pays off once the reduction is long enough to amortise its fixed cost.
+int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
-  if (forced >= 0 && forced <= 11) return forced;
+  if (forced >= 0 && forced <= 13) return forced;
   const int cus = compute_units();
   const int64_t tm = (M + 255) / 256;
-  const double t128 = rounds(tm * ((N + 127) / 128), cus);
-  const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.48;
+  const double k = (double)r * (double)K / 6.0;
+  const double r128 = 2.2 * k + 1700.0, r256 = 3.9 * k + 6000.0;
+  const double t128 = rounds(tm * ((N + 127) / 128), cus) * r128;
+  const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.48 * r128;
+  const double t256 = rounds(tm * ((N + 255) / 256), cus) * r256;
+  if (t256 < t128 && t256 < t192) return 13;
   return t192 < 0.97 * t128 ? 6 : 5;
+}
+
+// Tile configuration of a grouped launch: AWE_GEMM_CFG if set, else configuration 5 (the
+// grouped kernel is built for the 256 x 128 tiles on 8 waves).
+int choose_group_cfg() {
+  const char* e = getenv("AWE_GEMM_CFG");
+  const int forced = e ? atoi(e) : -1;
+  return forced >= 0 ? forced : 5;
 }
 
 // Tile configuration for E2M3 operands: AWE_GEMM_CFG_E2M3 (0: 256x128 with 8 waves in
@@ -1168,7 +1220,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
       default: return launch_tile<Cfg8w64x64e2m3>(g, L, stream);
     }
   }
-  switch (choose_cfg(L.M, L.N)) {
+  switch (choose_cfg(L.M, L.N, L.r, L.k_end - L.k_begin)) {
     case 0: return launch_tile<Cfg4w128x64>(g, L, stream);
     case 2: return launch_tile<Cfg8w64x96>(g, L, stream);
     case 3: return launch_tile<Cfg4w128x64k4>(g, L, stream);
@@ -1180,6 +1232,8 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 9: return launch_tile<Cfg8w64x64k4m16>(g, L, stream);
     case 10: return launch_tile<Cfg8w64x64k4p0m16>(g, L, stream);
     case 11: return launch_tile<Cfg8w64x96k4m16>(g, L, stream);
+    case 12: return launch_tile<Cfg8w64x128lf>(g, L, stream);
+    case 13: return launch_tile<Cfg8w64x128lf3>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }
@@ -1190,7 +1244,7 @@ bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5; }
 
 bool gemm_group_ok(const GemmLaunch* L, int n) {
   if (n < 1 || n > kMaxModuli) return false;
-  if (!group_cfg(choose_cfg(L[0].M, L[0].N))) return false;
+  if (!group_cfg(choose_group_cfg())) return false;
   for (int j = 0; j < n; ++j) {
     const GemmLaunch& a = L[j];
     if (a.fmt != kFmtE2M1 || a.shared || a.accumulate || a.r < 1 || a.r > kGroupProducts) return false;
@@ -1214,7 +1268,7 @@ awe_status launch_gemm_group(const GemmLaunch* L, int n, hipStream_t stream) {
   int order[kMaxModuli];
   for (int j = 0; j < n; ++j) order[j] = j;
   std::stable_sort(order, order + n, [&](int a, int b) { return L[a].r > L[b].r; });
-  switch (choose_cfg(L[0].M, L[0].N)) {
+  switch (choose_group_cfg()) {
     case 4: return launch_group_tile<Cfg8w64x64k4>(L, order, n, stream);
     case 5: return launch_group_tile<Cfg8w64x64k4p3>(L, order, n, stream);
     default: return launch_group_tile<Cfg8w64x64>(L, order, n, stream);

@@ -15,18 +15,21 @@ def _cfg(*t):
 
 
 # (waves M, waves N, blocks M, blocks N, k-steps per stage, stages, read-ahead, format, planes,
-#  MFMA shape)
+#  MFMA shape, blocks per wave whose int32 fold accumulators live in LDS)
 DEFAULTS = {
-    "E2M1 256x128, 3 k-steps ahead (default)": _cfg(4, 2, 2, 2, 4, 3, 3, 0, 1, 32),
-    "E2M1 256x192, 4 k-steps per stage": _cfg(4, 2, 2, 3, 4, 2, 1, 0, 1, 32),
-    "E2M1 256x192, 5 stages": _cfg(4, 2, 2, 3, 2, 5, 1, 0, 1, 32),
-    "E2M1 256x192, in place": _cfg(4, 2, 2, 3, 4, 2, 0, 0, 1, 32),
-    "E2M1 256x128, 16x16x128": _cfg(4, 2, 2, 2, 4, 3, 1, 0, 1, 16),
-    "E2M1 256x128, 16x16x128, in place": _cfg(4, 2, 2, 2, 4, 3, 0, 0, 1, 16),
-    "E2M1 256x192, 16x16x128, in place": _cfg(4, 2, 2, 3, 4, 2, 0, 0, 1, 16),
-    "E4M3": _cfg(4, 2, 2, 2, 2, 3, 1, 1, 1, 32),
-    "E2M3 (default)": _cfg(4, 2, 2, 2, 4, 2, 1, 2, 1, 32),
-    "E2M3 weights in the scales": _cfg(4, 2, 2, 2, 2, 2, 1, 2, 2, 32),
+    "E2M1 256x128, 3 k-steps ahead (default for smaller shapes)": _cfg(4, 2, 2, 2, 4, 3, 3, 0, 1, 32, 0),
+    "E2M1 256x192, 4 k-steps per stage": _cfg(4, 2, 2, 3, 4, 2, 1, 0, 1, 32, 0),
+    "E2M1 256x192, 5 stages": _cfg(4, 2, 2, 3, 2, 5, 1, 0, 1, 32, 0),
+    "E2M1 256x192, in place": _cfg(4, 2, 2, 3, 4, 2, 0, 0, 1, 32, 0),
+    "E2M1 256x128, 16x16x128": _cfg(4, 2, 2, 2, 4, 3, 1, 0, 1, 16, 0),
+    "E2M1 256x128, 16x16x128, in place": _cfg(4, 2, 2, 2, 4, 3, 0, 0, 1, 16, 0),
+    "E2M1 256x192, 16x16x128, in place": _cfg(4, 2, 2, 3, 4, 2, 0, 0, 1, 16, 0),
+    "E2M1 256x256, int32 fold of 3 blocks per wave in LDS": _cfg(4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3),
+    "E2M1 256x256, int32 fold of 2 blocks per wave in LDS, 3 stages (default)": _cfg(4, 2, 2, 4, 2, 3, 0, 0,
+                                                                                     1, 32, 2),
+    "E4M3": _cfg(4, 2, 2, 2, 2, 3, 1, 1, 1, 32, 0),
+    "E2M3 (default)": _cfg(4, 2, 2, 2, 4, 2, 1, 2, 1, 32, 0),
+    "E2M3 weights in the scales": _cfg(4, 2, 2, 2, 2, 2, 1, 2, 2, 32, 0),
 }
 
 

@@ -236,7 +236,8 @@ struct Cfg {
   // MFMA shape: 32 (32x32x64: one k-step is one brick) or 16 (16x16x128: one k-step is two
   // bricks; a wave's 32x32 block is four 16x16 MFMA blocks).  Both read the same operand
   // bytes from LDS per MAC for a given wave tile; on changing operands the 16x16x128 form
-  // sustains a higher rate at the board's power limit.
+  // sustains a higher rate at the board's power limit, but the GEMM, bound by its data path,
+  // runs no faster on it.
   static constexpr int MF = MF_;
   static_assert(MF == 32 || (MF == 16 && FMT_ == 0 && NPL_ == 1 && KST % 2 == 0), "MFMA shape");
   static constexpr int KSTEPS = MF == 16 ? KST / 2 : KST;  // MFMA k-steps per stage
@@ -276,7 +277,7 @@ struct Cfg {
   // after the ring (each wave its own 4 KiB per block, lane-major), so that a tile whose
   // registers hold only its FP32 accumulators and part of its int32 ones still fits.
   static constexpr int NLB = NLB_;
-  static_assert(NLB >= 0 && NLB < AM * AN && (NLB == 0 || MF == 32), "LDS fold blocks");
+  static_assert(NLB >= 0 && NLB < AM * AN && (NLB == 0 || (MF == 32 && NPL_ == 1)), "LDS fold blocks");
   static constexpr int FOLD_LDS_OFFSET = NSTAGE * STAGE_BYTES;
   static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES + NW * NLB * AV * 64 * 4;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS of one CU");

@@ -46,7 +46,10 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
                                                      int64_t plane_stride, int32_t* flag,
                                                      LutArg lut) {
   __shared__ uint32_t slut[256];
-  __shared__ uint8_t tblk[kTransposed ? 4 : 1][kTransposed ? 64 * 32 : 1];  // per-wave input block
+  // B side: per-wave 64 x 32 input block stored column-major, kTileCol bytes per column (64
+  // rows + 16 bytes of padding, so that the 16-byte column reads below hit distinct banks)
+  constexpr int kTileCol = 80;
+  __shared__ __attribute__((aligned(16))) uint8_t tblk[kTransposed ? 4 : 1][kTransposed ? 32 * kTileCol : 1];
   slut[threadIdx.x] = lut.v[threadIdx.x];
   __syncthreads();
   const int lane = threadIdx.x & 63;
@@ -73,24 +76,42 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
     }
   } else {
     // B side, K x N row-major: the brick needs the 64 x 32 block of B at rows
-    // (reduction indices) ks*64 .. +63 and columns rb*32 .. +31.  Lane l loads row
-    // ks*64 + l (32 contiguous bytes, two 16-byte loads) into this wave's slice of
-    // LDS; lane 32 h + t then reads column t of rows 32 h .. 32 h + 31.
+    // (reduction indices) ks*64 .. +63 and columns rb*32 .. +31.  Load i of lane l takes
+    // the 16 bytes at columns 16 (l & 1) .. +15 of block row 32 i + l / 2 (so each load
+    // instruction covers 32 rows x 32 bytes) and writes them into those columns of this
+    // wave's column-major tile; lane 32 h + t then reads rows 32 h .. 32 h + 31 of column t
+    // as two 16-byte words.
     uint8_t* tw = tblk[threadIdx.x >> 6];
-    const int64_t kr = ks * kBrickK + lane;
     const int64_t n0 = rb * kBrickRows;
-    const uint8_t* src = x + kr * ld + n0;
-    if (kr < K && n0 + 32 <= rows && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
-      *reinterpret_cast<uint4*>(tw + lane * 32) = *reinterpret_cast<const uint4*>(src);
-      *reinterpret_cast<uint4*>(tw + lane * 32 + 16) = *reinterpret_cast<const uint4*>(src + 16);
-    } else {
-      for (int c = 0; c < 32; ++c) tw[lane * 32 + c] = (kr < K && n0 + c < rows) ? src[c] : 0;
+    const int half = lane & 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = 32 * i + (lane >> 1);
+      const int64_t kr = ks * kBrickK + r;
+      const uint8_t* src = x + kr * ld + n0 + 16 * half;
+      uint32_t w[4];
+      if (kr < K && n0 + 32 <= rows && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+        const uint4 v = *reinterpret_cast<const uint4*>(src);
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+      } else {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) w[d] = 0;
+        for (int c = 0; c < 16; ++c)
+          if (kr < K && n0 + 16 * half + c < rows) w[c >> 2] |= (uint32_t)src[c] << (8 * (c & 3));
+      }
+#pragma unroll
+      for (int c = 0; c < 16; ++c)
+        tw[(16 * half + c) * kTileCol + r] = (uint8_t)(w[c >> 2] >> (8 * (c & 3)));
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
     __builtin_amdgcn_wave_barrier();
-    const uint8_t* col = tw + (lane >> 5) * 32 * 32 + (lane & 31);
+    const uint8_t* col = tw + (lane & 31) * kTileCol + (lane >> 5) * 32;
+    const uint4 c0 = *reinterpret_cast<const uint4*>(col);
+    const uint4 c1 = *reinterpret_cast<const uint4*>(col + 16);
+    const uint32_t cw[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
 #pragma unroll
-    for (int j = 0; j < 32; ++j) e[j] = (row_ok && k0 + j < K) ? slut[col[j * 32]] : 0u;
+    for (int j = 0; j < 32; ++j)
+      e[j] = (row_ok && k0 + j < K) ? slut[(cw[j >> 2] >> (8 * (j & 3))) & 0xff] : 0u;
   }
   uint32_t bad = 0;
 #pragma unroll

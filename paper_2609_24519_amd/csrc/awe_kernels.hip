@@ -955,12 +955,23 @@ int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   return t192 < 0.97 * t128 ? 6 : 5;
 }
 
-// Tile configuration of a grouped launch: AWE_GEMM_CFG if set, else configuration 5 (the
-// grouped kernel is built for the 256 x 128 tiles on 8 waves).
-int choose_group_cfg() {
+// Tile configuration of a grouped launch of n jobs of one shape: AWE_GEMM_CFG if set, else 5
+// or 13 (the configurations the grouped kernel is built for), whichever the per-round model of
+// choose_cfg gives less time summed over the jobs' tiles (many jobs fill the rounds, so the
+// rounds are not quantised).
+int choose_group_cfg(const GemmLaunch* L, int n) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
-  return forced >= 0 ? forced : 5;
+  if (forced >= 0) return forced;
+  const double tm = (double)((L[0].M + 255) / 256);
+  const double t128 = tm * (double)((L[0].N + 127) / 128), t256 = tm * (double)((L[0].N + 255) / 256);
+  double s128 = 0.0, s256 = 0.0;
+  for (int j = 0; j < n; ++j) {
+    const double k = (double)L[j].r * (double)(L[j].k_end - L[j].k_begin) / 6.0;
+    s128 += t128 * (2.2 * k + 1700.0);
+    s256 += t256 * (3.9 * k + 6000.0);
+  }
+  return s256 < s128 ? 13 : 5;
 }
 
 // Tile configuration for E2M3 operands: AWE_GEMM_CFG_E2M3 (0: 256x128 with 8 waves in
@@ -1261,12 +1272,13 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
 }
 
 // The grouped kernel is built for the 256 x 128 tiles on 8 waves (configurations 1, 4
-// and 5); the 256 x 192 ones leave no registers for the jobs' fields.
-bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5; }
+// and 5) and the 256 x 256 tiles of configuration 13; the 256 x 192 ones leave no registers
+// for the jobs' fields.
+bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5 || cfg == 13; }
 
 bool gemm_group_ok(const GemmLaunch* L, int n) {
   if (n < 1 || n > kMaxModuli) return false;
-  if (!group_cfg(choose_group_cfg())) return false;
+  if (!group_cfg(choose_group_cfg(L, n))) return false;
   for (int j = 0; j < n; ++j) {
     const GemmLaunch& a = L[j];
     if (a.fmt != kFmtE2M1 || a.shared || a.accumulate || a.r < 1 || a.r > kGroupProducts) return false;
@@ -1290,9 +1302,10 @@ awe_status launch_gemm_group(const GemmLaunch* L, int n, hipStream_t stream) {
   int order[kMaxModuli];
   for (int j = 0; j < n; ++j) order[j] = j;
   std::stable_sort(order, order + n, [&](int a, int b) { return L[a].r > L[b].r; });
-  switch (choose_group_cfg()) {
+  switch (choose_group_cfg(L, n)) {
     case 4: return launch_group_tile<Cfg8w64x64k4>(L, order, n, stream);
     case 5: return launch_group_tile<Cfg8w64x64k4p3>(L, order, n, stream);
+    case 13: return launch_group_tile<Cfg8w64x128lf3>(L, order, n, stream);
     default: return launch_group_tile<Cfg8w64x64>(L, order, n, stream);
   }
 }

@@ -891,6 +891,10 @@ using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k
 using Cfg4w128x64e2m3 = Cfg<2, 2, 4, 2, 2, 3, 1, 2>;  // 256 x 128, 4 waves, 2 k-steps, 3 stages
 using Cfg8w64x64k4e2m3 = Cfg<4, 2, 2, 2, 4, 2, 1, 2>; // 256 x 128, 8 waves, 4 k-steps, 2 stages
 using Cfg8w64x96p0e2m3 = Cfg<4, 2, 2, 3, 2, 3, 0, 2>; // 256 x 192, 8 waves, fragments read in place
+// as above with the int32 fold accumulators of 1 of each wave's 6 blocks in LDS
+using Cfg8w64x96p0lfe2m3 = Cfg<4, 2, 2, 3, 2, 3, 0, 2, 1, 32, 1>;
+// 2 of each wave's 6 blocks in LDS, 2 stages
+using Cfg8w64x96p0lf2e2m3 = Cfg<4, 2, 2, 3, 2, 2, 0, 2, 1, 32, 2>;
 // E2M3, two planes per side with the weights in the scales (4 products, one accumulator)
 using Cfg8w64x64sh = Cfg<4, 2, 2, 2, 2, 2, 1, 2, 2>;    // 256 x 128, 8 waves, 2 k-steps, 2 stages
 using Cfg8w64x64shp0 = Cfg<4, 2, 2, 2, 2, 2, 0, 2, 2>;  // as above, fragments read in place
@@ -976,12 +980,14 @@ int choose_group_cfg(const GemmLaunch* L, int n) {
 
 // Tile configuration for E2M3 operands: AWE_GEMM_CFG_E2M3 (0: 256x128 with 8 waves in
 // 3 stages, 1: as 0 in 4 stages, 2: 256x128 with 4 waves, 3: as 0 with 4 k-steps per
-// stage in 2 stages, 4: 256x192 with 8 waves reading fragments in place) overrides the
-// default 3, the fastest measured at 8192^3 (0: 1.41 ms, 3: 1.33 ms, 4: 1.38 ms).
+// stage in 2 stages, 4: 256x192 with 8 waves reading fragments in place, 5: as 4 with the
+// int32 fold accumulators of 1 of each wave's 6 blocks in LDS, 6: as 4 with 2 blocks in LDS
+// and 2 stages) overrides the default 5, the fastest measured at 8192^3 (in one process:
+// 3: 1.16-1.18 ms, 4: 1.14-1.15 ms, 5: 1.07-1.10 ms, 6: 1.24-1.26 ms).
 int choose_cfg_e2m3() {
   const char* e = getenv("AWE_GEMM_CFG_E2M3");
   const int forced = e ? atoi(e) : -1;
-  return forced >= 0 && forced <= 4 ? forced : 3;
+  return forced >= 0 && forced <= 6 ? forced : 5;
 }
 
 // The kernel arguments of one launch.
@@ -1250,6 +1256,8 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
       case 2: return launch_tile<Cfg4w128x64e2m3>(g, L, stream);
       case 3: return launch_tile<Cfg8w64x64k4e2m3>(g, L, stream);
       case 4: return launch_tile<Cfg8w64x96p0e2m3>(g, L, stream);
+      case 5: return launch_tile<Cfg8w64x96p0lfe2m3>(g, L, stream);
+      case 6: return launch_tile<Cfg8w64x96p0lf2e2m3>(g, L, stream);
       default: return launch_tile<Cfg8w64x64e2m3>(g, L, stream);
     }
   }

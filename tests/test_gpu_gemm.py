@@ -325,12 +325,12 @@ def test_split_last_round(monkeypatch, cfg, cus, enc, out):
     assert np.array_equal(C.cpu().numpy().astype(np.int64), ref)
 
 
-@pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4"])
+@pytest.mark.parametrize("cfg", ["0", "1", "2", "3", "4", "5", "6"])
 def test_every_e2m3_tile_configuration(monkeypatch, cfg):
     # AWE_GEMM_CFG_E2M3 forces one of the E2M3 tile configurations (256x128 on 8 waves
     # in 3 or 4 stages, on 4 waves, with 4 k-steps per stage; 256x192 on 8 waves with
-    # fragments read in place); each must be exact, also with a forced fold segment of
-    # one K_PAD
+    # fragments read in place, with the int32 fold accumulators of 0, 1 or 2 blocks per
+    # wave in LDS); each must be exact, also with a forced fold segment of one K_PAD
     monkeypatch.setenv("AWE_GEMM_CFG_E2M3", cfg)
     M, N, K = 300, 420, 1100
     A, B = _operands(awe.ENC_FP6K3, M, N, K, seed=int(cfg) + 70)

@@ -16,6 +16,7 @@
  * thread runs the same plain loop over its rows.
  */
 #include <stdint.h>
+#include <stdlib.h>
 
 /* C = A B exactly, int8 inputs (an int4 operand arrives in an int8 container). */
 void oracle_gemm_i8_i64(int64_t M, int64_t N, int64_t K,
@@ -55,19 +56,30 @@ void oracle_gemm_i8_i64_sampled(int64_t nr, const int64_t* rows,
     }
 }
 
-/* (A B) mod m for residue operands, as the non-negative residue in [0, m). */
+/* (A B) mod m for residue operands, as the non-negative residue in [0, m).
+   The exact integer row of A B is formed first (i-k-j order into an int64
+   row, the same plain sum as oracle_gemm_i8_i64) and each entry is then
+   reduced; the residues of Sec. 5.3 are those of the exact product, so the
+   order in which the exact sum is formed does not matter. */
 void oracle_gemm_u8_mod(int64_t m, int64_t M, int64_t N, int64_t K,
                         const uint8_t* A, int64_t lda,
                         const uint8_t* B, int64_t ldb,
                         int32_t* C, int64_t ldc)
 {
-    #pragma omp parallel for schedule(static)
-    for (int64_t i = 0; i < M; ++i) {
-        for (int64_t j = 0; j < N; ++j) {
-            int64_t acc = 0;
-            for (int64_t k = 0; k < K; ++k) acc += (int64_t)A[i * lda + k] * (int64_t)B[k * ldb + j];
-            C[i * ldc + j] = (int32_t)(((acc % m) + m) % m);
+    #pragma omp parallel
+    {
+        int64_t* row = (int64_t*)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+        #pragma omp for schedule(static)
+        for (int64_t i = 0; i < M; ++i) {
+            for (int64_t j = 0; j < N; ++j) row[j] = 0;
+            for (int64_t k = 0; k < K; ++k) {
+                const int64_t a = A[i * lda + k];
+                const uint8_t* b = B + k * ldb;
+                for (int64_t j = 0; j < N; ++j) row[j] += a * (int64_t)b[j];
+            }
+            for (int64_t j = 0; j < N; ++j) C[i * ldc + j] = (int32_t)(((row[j] % m) + m) % m);
         }
+        free(row);
     }
 }
 

@@ -7,10 +7,14 @@ benchmark times, against the oracle (bit-exact).
   product against the full oracle.
 * 8192^3 int4 x int8, AWE4: the same checks.
 * 4096^3 residues for every modulus of the FP64-significand residue set
-  (tests/golden/moduli_fp64_k16384.txt): sampled tiles at 4096^3 and a full 512^3.
+  (tests/golden/moduli_fp64_k16384.txt): the whole C against the oracle's (its SHA-256 in
+  tests/golden/full_oracle_sha256.txt, written from the oracle by
+  make_full_oracle_hashes.py), sampled tiles to locate a difference, and a full 512^3.
 * 4096 x 4096 x 65536 accumulation stress, AWE6, int64 C, default and forced fold
-  segment: closed forms over the whole of C where they exist, plus sampled tiles.
+  segment: the whole C against the oracle's (SHA-256 as above), closed forms over the whole
+  of C where they exist, plus sampled tiles.
 """
+import hashlib
 import os
 
 import numpy as np
@@ -30,6 +34,23 @@ def _moduli():
     with open(os.path.join(GOLDEN, "moduli_fp64_k16384.txt")) as f:
         lines = [l for l in f if l.strip() and not l.startswith("#")]
     return [int(x) for x in lines[0].split()]
+
+
+def _full_hashes():
+    out = {}
+    with open(os.path.join(GOLDEN, "full_oracle_sha256.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                name, dims, dtype, digest = [x.strip() for x in line.split("|")]
+                out[name] = (tuple(int(v) for v in dims.split()), dtype, digest)
+    return out
+
+
+def _check_full(C, name, shape, dtype):
+    """C (host array) against the SHA-256 of the oracle's whole C for workload `name`."""
+    dims, want_dtype, digest = _full_hashes()[name]
+    assert C.shape == shape and str(C.dtype) == want_dtype == dtype, (C.shape, C.dtype)
+    return hashlib.sha256(np.ascontiguousarray(C).tobytes()).hexdigest() == digest
 
 
 def _check_tiles(C, A, B, tiles, mod=None):
@@ -89,7 +110,10 @@ def test_config4_residues_4096(m):
     Ch = C.cpu().numpy()
     del C
     assert Ch.min() >= 0 and Ch.max() < m
+    full_ok = _check_full(Ch, "residues mod %d" % m, (4096, 4096), "int32")
+    # sampled tiles locate a difference; the whole C must match the oracle's in any case
     _check_tiles(Ch, A, B, inputs.sample_tiles(4096, 4096, 12, 128, seed=m), mod=m)
+    assert full_ok, "C mod %d differs from the oracle's full product" % m
     a, b = inputs.residue_pair(512, 512, 512, m, seed=m + 1000)
     Cs = awe.matmul_mod(m, to_dev(a), to_dev(b))
     torch.cuda.synchronize()
@@ -139,5 +163,7 @@ def test_config5_stress_65536(stress, kseg):
     Ch = C.cpu().numpy()
     del C, pa, pb
     torch.cuda.empty_cache()
+    full_ok = _check_full(Ch, "stress", (4096, 4096), "int64")
     _stress_closed_forms(Ch, A, B, K)
     _check_tiles(Ch, A, B, inputs.sample_tiles(M, N, 4, 64, seed=5))
+    assert full_ok, "the stress product differs from the oracle's full product"

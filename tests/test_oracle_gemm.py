@@ -114,3 +114,66 @@ def test_mod_python_ints():
     for i in range(3):
         for j in range(2):
             assert C[i, j] == sum(int(A[i, k]) * int(B[k, j]) for k in range(9)) % m
+
+
+def _py_product(A, B):
+    M, K = A.shape
+    N = B.shape[1]
+    return [[sum(int(A[i, k]) * int(B[k, j]) for k in range(K)) for j in range(N)] for i in range(M)]
+
+
+def test_wide_product_python_ints_fp16_extremes():
+    """gemm_i64_wide (the checker of the 12-bit significand scheme) against Python integers on
+    int16 inputs in [-2048, 2047], with the -2048 / 2047 extremes placed so that some results are
+    negative (their low word, read as int64, is negative) and some reach K * 2048^2."""
+    rng = np.random.default_rng(21)
+    K = 37
+    A = inputs.uniform(rng, (6, K), -2048, 2047, np.int16)
+    B = inputs.uniform(rng, (K, 5), -2048, 2047, np.int16)
+    A[0, :] = -2048
+    B[:, 0] = -2048  # C[0, 0] = K 2^22
+    B[:, 1] = 2047   # C[0, 1] = -K 2048 2047 < 0
+    A[1, :] = 2047
+    C = og.gemm_i64_wide(A, B)
+    assert C.dtype == np.int64
+    assert C.tolist() == _py_product(A, B)
+    assert C[0, 0] == K * 2048 * 2048 and C[0, 1] == -K * 2048 * 2047
+    assert (C < 0).any() and (C > 0).any()
+
+
+def test_wide_product_int64_boundaries():
+    """Results at the edges of int64: -2^63 and 2^63 - 1 fit and come back exactly; 2^63 and a
+    product far beyond int64 (low word alone would look like a valid int64) must be refused."""
+    lo_edge = og.gemm_i64_wide(np.array([[-(1 << 31)]]), np.array([[1 << 32]]))
+    assert int(lo_edge[0, 0]) == -(1 << 63)
+    x = 3037000499  # x^2 = 2^63 - 5,928,526,806 < 2^63 - 1
+    hi_edge = og.gemm_i64_wide(np.array([[x, 1]]), np.array([[x], [(1 << 63) - 1 - x * x]]))
+    assert int(hi_edge[0, 0]) == (1 << 63) - 1
+    with pytest.raises(AssertionError):
+        og.gemm_i64_wide(np.array([[1 << 31]]), np.array([[1 << 32]]))  # 2^63: low word reads as -2^63
+    with pytest.raises(AssertionError):
+        og.gemm_i64_wide(np.array([[1 << 40, 3]]), np.array([[1 << 40], [5]]))  # 2^80 + 15
+
+
+def test_full_oracle_hash_file_matches_oracle():
+    """tests/golden/full_oracle_sha256.txt (used by the GPU tests of the residue and stress
+    workloads) lists every modulus of the residue set and the stress workload, and its entry for
+    m = 5 is the SHA-256 of the oracle's C recomputed here (8 s on a few cores)."""
+    import hashlib
+    import os
+
+    golden = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+    with open(os.path.join(golden, "moduli_fp64_k16384.txt")) as f:
+        moduli = [int(x) for x in [l for l in f if l.strip() and not l.startswith("#")][0].split()]
+    rows = {}
+    with open(os.path.join(golden, "full_oracle_sha256.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                name, dims, dtype, digest = [x.strip() for x in line.split("|")]
+                rows[name] = (dims, dtype, digest)
+    assert set(rows) == {"residues mod %d" % m for m in moduli} | {"stress"}
+    assert rows["stress"][:2] == ("4096 4096 65536", "int64")
+    A, B = inputs.residue_pair(4096, 4096, 4096, 5)
+    C = og.gemm_mod(5, A, B)
+    assert rows["residues mod 5"][:2] == ("4096 4096 4096", "int32")
+    assert hashlib.sha256(np.ascontiguousarray(C).tobytes()).hexdigest() == rows["residues mod 5"][2]

@@ -248,7 +248,7 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
 template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0,
-          int NPL_ = 1, int MF_ = 32, int NLB_ = 0>
+          int NPL_ = 1, int MF_ = 32, int NLB_ = 0, int SCHED_ = 0>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
   static constexpr int KST = KST_;        // bricks (64 reduction indices each) per row block and stage
@@ -308,6 +308,15 @@ struct Cfg {
   static constexpr int B_LO = B_UNITS / NW, B_XTRA = B_UNITS % NW;
   static_assert(A_UNITS % NW == 0, "A units must split evenly over the waves");
   static_assert(kKPad % KT == 0, "a stage must divide the reduction padding");
+  // Schedule of the stage loop.  0: after the barrier that frees a buffer every wave issues
+  // its copies of the stage that refills it, then runs the stage's k-steps.  1: the copies
+  // that refill the freed buffer are issued one after each of the first MFMAs of the next
+  // stage instead, so that a wave waiting for the address unit to take a copy has matrix work
+  // in flight (at 8192^3 2-3 % faster than 0 on the 256 x 256 tile).
+  static constexpr int SCHED = SCHED_;
+  static_assert(SCHED == 0 || (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 &&
+                               A_PW + B_LO <= BMW * BNW && NSTAGE >= 3),
+                "copies after the MFMAs: E2M1, one plane per side, 32x32x64 MFMAs, fragments in place");
 };
 
 struct GemmArgs {
@@ -392,13 +401,12 @@ __device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0
 // The copies of one stage: wave w takes A units A_PW w .. A_PW w + A_PW - 1
 // and B units w, w + NW, ... (unit id = KU * row block + unit of the stage).
 template <class C>
-__device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
-                                           int tm, int tn, int wave, int lane) {
-  const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u), kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
+__device__ __forceinline__ void load_stage_a(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
+                                             int tm, int wave, int lane) {
+  const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u);
   // k-step major planes: the units of one k-step (pair) for consecutive row blocks are adjacent
   constexpr int UB = C::UNIT_BYTES;
   const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * C::KU * g.rba * UB;
-  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KU * g.rbb * UB;
   const uint32_t voff = lane * 16;
 #pragma unroll
   for (int i = 0; i < C::A_PW; ++i) {
@@ -410,6 +418,15 @@ __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, u
       dma_brick(pa + pl * g.stride_a + ((int64_t)(r % C::KU) * g.rba + rb) * UB + h * kBrickBytes, voff,
                 stage_lds + id * UB + h * kBrickBytes);
   }
+}
+
+template <class C>
+__device__ __forceinline__ void load_stage_b(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
+                                             int tn, int wave, int lane) {
+  const int kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
+  constexpr int UB = C::UNIT_BYTES;
+  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KU * g.rbb * UB;
+  const uint32_t voff = lane * 16;
 #pragma unroll
   for (int i = 0; i < C::B_LO + (C::B_XTRA ? 1 : 0); ++i) {
     const int id = wave + i * C::NW;
@@ -420,6 +437,36 @@ __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, u
     for (int h = 0; h < C::COPIES; ++h)
       dma_brick(pb + pl * g.stride_b + ((int64_t)(r % C::KU) * g.rbb + cb) * UB + h * kBrickBytes, voff,
                 stage_lds + (C::A_UNITS + id) * UB + h * kBrickBytes);
+  }
+}
+
+template <class C>
+__device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
+                                           int tm, int tn, int wave, int lane) {
+  load_stage_a<C>(g, c, stage_lds, tm, wave, lane);
+  load_stage_b<C>(g, c, stage_lds, tn, wave, lane);
+}
+
+// Copy q of this wave's share of a stage (E2M1, one plane per side): q < A_PW is A brick
+// wave * A_PW + q, then B brick wave + (q - A_PW) * NW, as load_stage orders them.
+template <class C, int Q>
+__device__ __forceinline__ void load_one(const GemmArgs& g, const Cursor& c, uint32_t stage_lds, int tm,
+                                         int tn, int wave, int lane) {
+  const uint32_t voff = lane * 16;
+  if constexpr (Q < C::A_PW) {
+    const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u);
+    const int id = wave * C::A_PW + Q;
+    const int rb = min(tm * (C::BM / kBrickRows) + id / C::KU, g.rba - 1);
+    dma_brick(g.pa + (int64_t)ka * g.stride_a + ((int64_t)c.t * C::KU + id % C::KU) * g.rba * kBrickBytes +
+                  (int64_t)rb * kBrickBytes,
+              voff, stage_lds + id * kBrickBytes);
+  } else {
+    const int kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
+    const int id = wave + (Q - C::A_PW) * C::NW;
+    const int cb = min(tn * (C::BN / kBrickRows) + id / C::KU, g.rbb - 1);
+    dma_brick(g.pb + (int64_t)kb * g.stride_b + ((int64_t)c.t * C::KU + id % C::KU) * g.rbb * kBrickBytes +
+                  (int64_t)cb * kBrickBytes,
+              voff, stage_lds + (C::A_UNITS + id) * kBrickBytes);
   }
 }
 
@@ -546,7 +593,9 @@ __device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& t
 
 // One output of the epilogue: the int32 accumulator holds D*C (exact schemes,
 // modulo 2^32, the true value fits) or sum lambda_k P_k (residues); a launch
-// group of a wider scheme contributes outer * (its sum / D).
+// group of a wider scheme contributes outer * (its sum / D).  C is written with
+// non-temporal stores where it is not read back (C is not reused by the kernel,
+// and all tiles of a round write at once: measured 2 % faster at 8192^3).
 __device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col, int32_t val) {
   if (row >= g.M || col >= g.N) return;
   const int64_t off = (int64_t)row * g.ldc + col;
@@ -555,16 +604,24 @@ __device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col
     int32_t rr = val % m;
     if (rr < 0) rr += m;
     int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
-    if (g.accumulate) rr = (Cp[off] + rr) % m;
-    Cp[off] = rr;
+    if (g.accumulate)
+      Cp[off] = (Cp[off] + rr) % m;
+    else
+      __builtin_nontemporal_store(rr, Cp + off);
   } else {
     const int64_t t = (int64_t)(val >> g.log2D) * g.outer;
     if (g.c64) {
       int64_t* Cp = reinterpret_cast<int64_t*>(g.C);
-      Cp[off] = g.accumulate ? Cp[off] + t : t;
+      if (g.accumulate)
+        Cp[off] += t;
+      else
+        __builtin_nontemporal_store(t, Cp + off);
     } else {
       int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
-      Cp[off] = g.accumulate ? (int32_t)((uint32_t)Cp[off] + (uint32_t)t) : (int32_t)t;
+      if (g.accumulate)
+        Cp[off] = (int32_t)((uint32_t)Cp[off] + (uint32_t)t);
+      else
+        __builtin_nontemporal_store((int32_t)t, Cp + off);
     }
   }
 }
@@ -597,6 +654,15 @@ __global__ __launch_bounds__(256) void zero_tiles_kernel(GemmArgs g, int bm, int
       else
         reinterpret_cast<int32_t*>(g.C)[row + c] = 0;
     }
+  }
+}
+
+// f(integral_constant<int, Q>) for Q = I .. N - 1, unrolled at compile time.
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
   }
 }
 
@@ -640,131 +706,193 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
 #pragma unroll
     for (int v = 0; v < C::AV; ++v) fold_lds[((b - NREG) * C::AV + v) * 64] = 0;
 
-  constexpr int NSTAGE = C::NSTAGE;
-  Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
-  // Prologue: stages 0 .. NSTAGE-1 fill the whole ring.
+  // After product p's last stage of a fold segment: fold its FP32 partials into the int32
+  // accumulators with the product's coefficient and restart them.
+  auto fold_product = [&](int p) {
+    if ((g.fold_mask >> p) & 1u) {
+      const int32_t l = fold_coef(p);
+      // one 32x32 block at a time keeps the temporaries of the fold small
 #pragma unroll
-  for (int i = 0; i < NSTAGE; ++i) {
-    load_stage<C>(g, nxt, lds0 + i * C::STAGE_BYTES, tm, tn, wave, lane);
-    cursor_next(nxt, g, t_end);
-  }
-  wait_stages<C, NSTAGE - 1>(wave);
-  block_barrier();
-  constexpr int PD = C::PD, NSETS = C::NSETS;
-  Frags<C> f[NSETS];
+      for (int b = 0; b < NREG; ++b) {
+        const int i = b / C::AN, j = b % C::AN;
 #pragma unroll
-  for (int ks = 0; ks < PD; ++ks) read_frags<C>(f[ks], smem, ks, wm, wn, lane);
+        for (int v = 0; v < C::AV; ++v) {
+          // (two planes per side: the weights are in the scales, the partial may use
+          // all 24 bits, and it is added unmultiplied)
+          if constexpr (C::NPL == 2)
+            iacc[i][j][v] += (int32_t)acc[i][j][v];
+          else
+            iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
+          acc[i][j][v] = 0.0f;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int b = NREG; b < C::AM * C::AN; ++b) {
+        const int i = b / C::AN, j = b % C::AN;
+#pragma unroll
+        for (int v = 0; v < C::AV; ++v) {
+          fold_lds[((b - NREG) * C::AV + v) * 64] += __mul24(l, (int32_t)acc[i][j][v]);
+          acc[i][j][v] = 0.0f;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
 
-  // Stage s, k-steps 0 .. KST-1: the MFMAs of k-step ks run on fragment set
-  // ks % NSETS while the reads of k-step ks + PD go into another set.  At k-step
-  // KST - PD, before the first read that crosses into stage s+1: wait until
-  // stage s+1 has landed and this wave's reads of stage s are done (all of them
-  // were issued by then), barrier, refill stage s's buffer with stage s+NSTAGE.
-  // The barrier sits between two groups of MFMAs.
-  int buf = 0;
-  for (int cs = t_beg; cs < t_end; cs += g.ts) {
-    const int ce = min(cs + g.ts, t_end);
-    for (int p = 0; p < g.r; ++p) {
-      for (int t = cs; t < ce; ++t) {
-        const uint32_t cur_off = buf * C::STAGE_BYTES;
-        const int nbuf = buf + 1 == NSTAGE ? 0 : buf + 1;
+  constexpr int NSTAGE = C::NSTAGE;
+  if constexpr (C::SCHED == 1) {
+    // Stream stage u sits in buffer u % NSTAGE.  In stage u each wave issues its copies of
+    // stage u + NSTAGE - 1 into the buffer of stage u - 1 (freed by the barrier at the end of
+    // stage u - 1), one after each of the first MFMAs of the stage's first k-step.  Before the
+    // barrier at the end of stage u it waits until stage u + 1 has landed (its copies of the
+    // NSTAGE - 2 stages after u + 1 may still be in flight) and its reads of stage u are done.
+    constexpr int PER_STAGE = C::A_PW + C::B_LO;  // copies per wave and stage
+    Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
 #pragma unroll
-        for (int ks = 0; ks < C::KSTEPS; ++ks) {
-          if (ks == C::KSTEPS - PD) {
+    for (int i = 0; i < NSTAGE - 1; ++i) {
+      load_stage<C>(g, nxt, lds0 + i * C::STAGE_BYTES, tm, tn, wave, lane);
+      cursor_next(nxt, g, t_end);
+    }
+    wait_vmcnt<(NSTAGE - 2) * PER_STAGE>();
+    block_barrier();
+    Frags<C> f;
+    int buf = 0, cbuf = NSTAGE - 1;
+    for (int cs = t_beg; cs < t_end; cs += g.ts) {
+      const int ce = min(cs + g.ts, t_end);
+      for (int p = 0; p < g.r; ++p) {
+        for (int t = cs; t < ce; ++t) {
+          const uint32_t cur_off = buf * C::STAGE_BYTES, cp_lds = lds0 + cbuf * C::STAGE_BYTES;
+#pragma unroll
+          for (int ks = 0; ks < C::KSTEPS; ++ks) {
+            read_frags<C>(f, smem + cur_off, ks, wm, wn, lane);
+            __builtin_amdgcn_sched_barrier(0);
+            if (ks == 0) {
+              static_for<0, C::BMW * C::BNW>([&](auto qc) {
+                constexpr int q = decltype(qc)::value;
+                mfma_block(acc[q / C::BNW][q % C::BNW], f.a[q / C::BNW], f.b[q % C::BNW]);
+                if constexpr (q < PER_STAGE) {
+                  __builtin_amdgcn_sched_barrier(0);
+                  load_one<C, q>(g, nxt, cp_lds, tm, tn, wave, lane);
+                  __builtin_amdgcn_sched_barrier(0);
+                }
+              });
+              cursor_next(nxt, g, t_end);
+            } else {
+#pragma unroll
+              for (int i = 0; i < C::BMW; ++i)
+#pragma unroll
+                for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], f.a[i], f.b[j]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          wait_vmcnt<(NSTAGE - 2) * PER_STAGE>();
+          wait_lgkm0();
+          block_barrier();
+          buf = buf + 1 == NSTAGE ? 0 : buf + 1;
+          cbuf = cbuf + 1 == NSTAGE ? 0 : cbuf + 1;
+        }
+        fold_product(p);
+      }
+    }
+  } else {
+    Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
+    // Prologue: stages 0 .. NSTAGE-1 fill the whole ring.
+#pragma unroll
+    for (int i = 0; i < NSTAGE; ++i) {
+      load_stage<C>(g, nxt, lds0 + i * C::STAGE_BYTES, tm, tn, wave, lane);
+      cursor_next(nxt, g, t_end);
+    }
+    wait_stages<C, NSTAGE - 1>(wave);
+    block_barrier();
+    constexpr int PD = C::PD, NSETS = C::NSETS;
+    Frags<C> f[NSETS];
+#pragma unroll
+    for (int ks = 0; ks < PD; ++ks) read_frags<C>(f[ks], smem, ks, wm, wn, lane);
+
+    // Stage s, k-steps 0 .. KST-1: the MFMAs of k-step ks run on fragment set
+    // ks % NSETS while the reads of k-step ks + PD go into another set.  At k-step
+    // KST - PD, before the first read that crosses into stage s+1: wait until
+    // stage s+1 has landed and this wave's reads of stage s are done (all of them
+    // were issued by then), barrier, refill stage s's buffer with stage s+NSTAGE.
+    // The barrier sits between two groups of MFMAs.
+    int buf = 0;
+    for (int cs = t_beg; cs < t_end; cs += g.ts) {
+      const int ce = min(cs + g.ts, t_end);
+      for (int p = 0; p < g.r; ++p) {
+        for (int t = cs; t < ce; ++t) {
+          const uint32_t cur_off = buf * C::STAGE_BYTES;
+          const int nbuf = buf + 1 == NSTAGE ? 0 : buf + 1;
+#pragma unroll
+          for (int ks = 0; ks < C::KSTEPS; ++ks) {
+            if (ks == C::KSTEPS - PD) {
+              wait_stages<C, NSTAGE - 2>(wave);
+              wait_lgkm0();
+              block_barrier();
+              load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
+              cursor_next(nxt, g, t_end);
+            }
+            const int kr = ks + PD;  // k-step whose fragments are read now
+            if (kr < C::KSTEPS)
+              read_frags<C>(f[kr % NSETS], smem + cur_off, kr, wm, wn, lane);
+            else
+              read_frags<C>(f[kr % NSETS], smem + nbuf * C::STAGE_BYTES, kr - C::KSTEPS, wm, wn, lane);
+            // in place (PD = 0) the MFMAs wait for these reads; read ahead, the reads are
+            // spread between the MFMAs below
+            if constexpr (PD == 0) __builtin_amdgcn_sched_barrier(0);
+            const Frags<C>& cur = f[ks % NSETS];
+            if constexpr (C::MF == 16) {
+#pragma unroll
+              for (int i = 0; i < C::AM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::AN; ++j)
+                  acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(cur.a[i], cur.b[j], acc[i][j], 4, 4,
+                                                                               0, kScale2, 0, kScale2);
+            } else if constexpr (C::NPL == 2) {
+              // the four plane pairs, each block's MFMAs four apart in issue order
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int i = 0; i < C::BMW; ++i)
+#pragma unroll
+                  for (int j = 0; j < C::BNW; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        cur.a[(q >> 1) * C::BMW + i], cur.b[(q & 1) * C::BNW + j], acc[i][j], 2, 2, 0,
+                        (int)g.sa[q >> 1], 0, (int)g.sb[q & 1]);
+            } else {
+#pragma unroll
+              for (int i = 0; i < C::BMW; ++i)
+#pragma unroll
+                for (int j = 0; j < C::BNW; ++j) {
+                  if constexpr (C::FMT == 0)
+                    mfma_block(acc[i][j], cur.a[i], cur.b[j]);
+                  else if constexpr (C::FMT == 1)
+                    mfma_block8(acc[i][j], cur.a[i], cur.b[j]);
+                  else
+                    mfma_block6(acc[i][j], cur.a[i], cur.b[j]);
+                }
+            }
+            if constexpr (PD > 0) {
+              // issue order: one MFMA, then one fragment read of a later k-step (measured
+              // 1-3 % faster than all reads ahead of the MFMAs)
+#pragma unroll
+              for (int q = 0; q < C::NPL * C::NPL * C::AM * C::AN; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // an MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // an LDS read
+              }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          if constexpr (PD == 0) {
+            // every read of stage s has been consumed: refill its buffer after the barrier
             wait_stages<C, NSTAGE - 2>(wave);
-            wait_lgkm0();
             block_barrier();
             load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
             cursor_next(nxt, g, t_end);
           }
-          const int kr = ks + PD;  // k-step whose fragments are read now
-          if (kr < C::KSTEPS)
-            read_frags<C>(f[kr % NSETS], smem + cur_off, kr, wm, wn, lane);
-          else
-            read_frags<C>(f[kr % NSETS], smem + nbuf * C::STAGE_BYTES, kr - C::KSTEPS, wm, wn, lane);
-          // in place (PD = 0) the MFMAs wait for these reads; read ahead, the reads are
-          // spread between the MFMAs below
-          if constexpr (PD == 0) __builtin_amdgcn_sched_barrier(0);
-          const Frags<C>& cur = f[ks % NSETS];
-          if constexpr (C::MF == 16) {
-#pragma unroll
-            for (int i = 0; i < C::AM; ++i)
-#pragma unroll
-              for (int j = 0; j < C::AN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(cur.a[i], cur.b[j], acc[i][j], 4, 4,
-                                                                             0, kScale2, 0, kScale2);
-          } else if constexpr (C::NPL == 2) {
-            // the four plane pairs, each block's MFMAs four apart in issue order
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-              for (int i = 0; i < C::BMW; ++i)
-#pragma unroll
-                for (int j = 0; j < C::BNW; ++j)
-                  acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                      cur.a[(q >> 1) * C::BMW + i], cur.b[(q & 1) * C::BNW + j], acc[i][j], 2, 2, 0,
-                      (int)g.sa[q >> 1], 0, (int)g.sb[q & 1]);
-          } else {
-#pragma unroll
-            for (int i = 0; i < C::BMW; ++i)
-#pragma unroll
-              for (int j = 0; j < C::BNW; ++j) {
-                if constexpr (C::FMT == 0)
-                  mfma_block(acc[i][j], cur.a[i], cur.b[j]);
-                else if constexpr (C::FMT == 1)
-                  mfma_block8(acc[i][j], cur.a[i], cur.b[j]);
-                else
-                  mfma_block6(acc[i][j], cur.a[i], cur.b[j]);
-              }
-          }
-          if constexpr (PD > 0) {
-            // issue order: one MFMA, then one fragment read of a later k-step (measured
-            // 1-3 % faster than all reads ahead of the MFMAs)
-#pragma unroll
-            for (int q = 0; q < C::NPL * C::NPL * C::AM * C::AN; ++q) {
-              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // an MFMA
-              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // an LDS read
-            }
-          }
-          __builtin_amdgcn_sched_barrier(0);
+          buf = nbuf;
         }
-        if constexpr (PD == 0) {
-          // every read of stage s has been consumed: refill its buffer after the barrier
-          wait_stages<C, NSTAGE - 2>(wave);
-          block_barrier();
-          load_stage<C>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
-          cursor_next(nxt, g, t_end);
-        }
-        buf = nbuf;
-      }
-      if ((g.fold_mask >> p) & 1u) {
-        const int32_t l = fold_coef(p);
-        // one 32x32 block at a time keeps the temporaries of the fold small
-#pragma unroll
-        for (int b = 0; b < NREG; ++b) {
-          const int i = b / C::AN, j = b % C::AN;
-#pragma unroll
-          for (int v = 0; v < C::AV; ++v) {
-            // (two planes per side: the weights are in the scales, the partial may use
-            // all 24 bits, and it is added unmultiplied)
-            if constexpr (C::NPL == 2)
-              iacc[i][j][v] += (int32_t)acc[i][j][v];
-            else
-              iacc[i][j][v] += __mul24(l, (int32_t)acc[i][j][v]);
-            acc[i][j][v] = 0.0f;
-          }
-          __builtin_amdgcn_sched_barrier(0);
-        }
-#pragma unroll
-        for (int b = NREG; b < C::AM * C::AN; ++b) {
-          const int i = b / C::AN, j = b % C::AN;
-#pragma unroll
-          for (int v = 0; v < C::AV; ++v) {
-            fold_lds[((b - NREG) * C::AV + v) * 64] += __mul24(l, (int32_t)acc[i][j][v]);
-            acc[i][j][v] = 0.0f;
-          }
-          __builtin_amdgcn_sched_barrier(0);
-        }
+        fold_product(p);
       }
     }
   }
@@ -866,10 +994,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_group_kernel(GroupArgs ga)
 
 // The tile configurations the launcher chooses from: waves (M x N), 32x32
 // blocks per wave (M x N), k-steps per stage, LDS ring depth.
-using Cfg4w128x64 = Cfg<2, 2, 4, 2, 2, 4>;   // 256 x 128, 4 waves (1 per SIMD)
 using Cfg8w64x64 = Cfg<4, 2, 2, 2, 2, 4>;    // 256 x 128, 8 waves (2 per SIMD)
 using Cfg8w64x96 = Cfg<4, 2, 2, 3, 2, 4>;    // 256 x 192, 8 waves (2 per SIMD)
-using Cfg4w128x64k4 = Cfg<2, 2, 4, 2, 4, 3>; // 256 x 128, 4 waves, 4 k-steps per stage
 using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps per stage
 using Cfg8w64x64k4p3 = Cfg<4, 2, 2, 2, 4, 3, 3>;  // as above, fragments read 3 k-steps ahead
 using Cfg8w64x64e4m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 1>;  // 256 x 128, 8 waves, E4M3 operands
@@ -885,13 +1011,14 @@ using Cfg8w64x96k4m16 = Cfg<4, 2, 2, 3, 4, 2, 0, 0, 1, 16>;   // 256 x 192, 8 wa
 using Cfg8w64x128lf = Cfg<4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3>;
 // as above with the fold accumulators of 2 blocks per wave in LDS (64 KiB) and a 3-stage ring
 using Cfg8w64x128lf3 = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2>;
+// config 13 with the copies that refill a freed buffer issued after the first MFMAs of the next stage
+using Cfg8w64x128ci = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
 // E2M3 operands (3 KiB units of two k-steps)
 using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
 using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
-using Cfg4w128x64e2m3 = Cfg<2, 2, 4, 2, 2, 3, 1, 2>;  // 256 x 128, 4 waves, 2 k-steps, 3 stages
 using Cfg8w64x64k4e2m3 = Cfg<4, 2, 2, 2, 4, 2, 1, 2>; // 256 x 128, 8 waves, 4 k-steps, 2 stages
-using Cfg8w64x96p0e2m3 = Cfg<4, 2, 2, 3, 2, 3, 0, 2>; // 256 x 192, 8 waves, fragments read in place
-// as above with the int32 fold accumulators of 1 of each wave's 6 blocks in LDS
+// 256 x 192, 8 waves, fragments read in place, the int32 fold accumulators of 1 of each wave's 6
+// blocks in LDS
 using Cfg8w64x96p0lfe2m3 = Cfg<4, 2, 2, 3, 2, 3, 0, 2, 1, 32, 1>;
 // 2 of each wave's 6 blocks in LDS, 2 stages
 using Cfg8w64x96p0lf2e2m3 = Cfg<4, 2, 2, 3, 2, 2, 0, 2, 1, 32, 2>;
@@ -931,23 +1058,26 @@ double rounds(int64_t tiles, int cus) {
   return (double)full + (full > 0 && S >= 2 ? 1.0 / S : 1.0);
 }
 
-// Tile configuration for a problem.  AWE_GEMM_CFG (0: 256x128 with 4 waves,
-// 1: 256x128 with 8 waves, 2: 256x192 with 8 waves, 3 and 4: as 0 and 1 with
-// 4 k-steps per stage, 5: as 4 with fragments read three k-steps ahead, 6:
-// 256x192 with 4 k-steps per stage in 2 stages, 7: 256x192 with 2 k-steps per
-// stage in 5 stages, 8: as 6 with fragments read in place, 9: as 4 on the 16x16x128
-// MFMA, 10: as 9 with fragments read in place, 11: 256x192 on the 16x16x128 MFMA, in
-// place, 12: 256x256 with the int32 fold accumulators of 3 blocks per wave in LDS and a
-// 2-stage ring, 13: as 12 with 2 blocks per wave in LDS and a 3-stage ring) overrides the
-// choice.  Otherwise the configuration whose rounds of workgroups finish first: 5, 6 (a round
-// about 1.48 times as long as a round of 5, measured at 8192^3; only when clearly sooner) or
-// 13.  A round takes about 2.2 k + 1700 time units for 5 and 3.9 k + 6000 for 13, k = r K / 6
-// reduction indices at r products (fitted to 4096^2 and 8192^2 tiles at K = 4096 .. 65536):
-// the larger tile pays off once the reduction is long enough to amortise its fixed cost.
+// Whether n names one of the E2M1 tile configurations (AWE_GEMM_CFG): 1: 256x128 with 8
+// waves, 2: 256x192 with 8 waves, 4: as 1 with 4 k-steps per stage, 5: as 4 with fragments
+// read three k-steps ahead, 6: 256x192 with 4 k-steps per stage in 2 stages, 7: 256x192 with 2
+// k-steps per stage in 5 stages, 8: as 6 with fragments read in place, 9: as 4 on the
+// 16x16x128 MFMA, 10: as 9 with fragments read in place, 11: 256x192 on the 16x16x128 MFMA, in
+// place, 12: 256x256 with the int32 fold accumulators of 3 blocks per wave in LDS and a 2-stage
+// ring, 13: as 12 with 2 blocks per wave in LDS and a 3-stage ring, 14: as 13 with the copies
+// that refill a freed buffer issued after the first MFMAs of the next stage.
+bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 14); }
+
+// Tile configuration for a problem: AWE_GEMM_CFG if it names one, else the configuration whose
+// rounds of workgroups finish first: 5, 6 (a round about 1.48 times as long as a round of 5;
+// only when clearly sooner) or 14.  A round takes about 2.2 k + 1700 time units for 5 and
+// 3.9 k + 6000 for the 256x256 tile, k = r K / 6 reduction indices at r products: a fit of the
+// kernel times measured on MI355X for 4096^2 and 8192^2 outputs at K = 4096 .. 65536.  The
+// larger tile pays off once the reduction is long enough to amortise its fixed cost per round.
 int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
-  if (forced >= 0 && forced <= 13) return forced;
+  if (e2m1_cfg(forced)) return forced;
   const int cus = compute_units();
   const int64_t tm = (M + 255) / 256;
   const double k = (double)r * (double)K / 6.0;
@@ -955,7 +1085,7 @@ int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const double t128 = rounds(tm * ((N + 127) / 128), cus) * r128;
   const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.48 * r128;
   const double t256 = rounds(tm * ((N + 255) / 256), cus) * r256;
-  if (t256 < t128 && t256 < t192) return 13;
+  if (t256 < t128 && t256 < t192) return 14;
   return t192 < 0.97 * t128 ? 6 : 5;
 }
 
@@ -979,15 +1109,14 @@ int choose_group_cfg(const GemmLaunch* L, int n) {
 }
 
 // Tile configuration for E2M3 operands: AWE_GEMM_CFG_E2M3 (0: 256x128 with 8 waves in
-// 3 stages, 1: as 0 in 4 stages, 2: 256x128 with 4 waves, 3: as 0 with 4 k-steps per
-// stage in 2 stages, 4: 256x192 with 8 waves reading fragments in place, 5: as 4 with the
-// int32 fold accumulators of 1 of each wave's 6 blocks in LDS, 6: as 4 with 2 blocks in LDS
-// and 2 stages) overrides the default 5, the fastest measured at 8192^3 (in one process:
-// 3: 1.16-1.18 ms, 4: 1.14-1.15 ms, 5: 1.07-1.10 ms, 6: 1.24-1.26 ms).
+// 3 stages, 1: as 0 in 4 stages, 3: as 0 with 4 k-steps per stage in 2 stages, 5: 256x192 with
+// 8 waves reading fragments in place and the int32 fold accumulators of 1 of each wave's 6
+// blocks in LDS, 6: as 5 with 2 blocks in LDS and 2 stages) overrides the default 5, the
+// fastest measured at 8192^3 (in one process: 3: 1.16-1.18 ms, 5: 1.07-1.10 ms, 6: 1.24-1.26 ms).
 int choose_cfg_e2m3() {
   const char* e = getenv("AWE_GEMM_CFG_E2M3");
   const int forced = e ? atoi(e) : -1;
-  return forced >= 0 && forced <= 6 ? forced : 5;
+  return forced == 0 || forced == 1 || forced == 3 || forced == 6 ? forced : 5;
 }
 
 // The kernel arguments of one launch.
@@ -1253,18 +1382,14 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   if (L.fmt == kFmtE2M3) {
     switch (choose_cfg_e2m3()) {
       case 1: return launch_tile<Cfg8w64x64s4e2m3>(g, L, stream);
-      case 2: return launch_tile<Cfg4w128x64e2m3>(g, L, stream);
       case 3: return launch_tile<Cfg8w64x64k4e2m3>(g, L, stream);
-      case 4: return launch_tile<Cfg8w64x96p0e2m3>(g, L, stream);
       case 5: return launch_tile<Cfg8w64x96p0lfe2m3>(g, L, stream);
       case 6: return launch_tile<Cfg8w64x96p0lf2e2m3>(g, L, stream);
       default: return launch_tile<Cfg8w64x64e2m3>(g, L, stream);
     }
   }
   switch (choose_cfg(L.M, L.N, L.r, L.k_end - L.k_begin)) {
-    case 0: return launch_tile<Cfg4w128x64>(g, L, stream);
     case 2: return launch_tile<Cfg8w64x96>(g, L, stream);
-    case 3: return launch_tile<Cfg4w128x64k4>(g, L, stream);
     case 4: return launch_tile<Cfg8w64x64k4>(g, L, stream);
     case 5: return launch_tile<Cfg8w64x64k4p3>(g, L, stream);
     case 6: return launch_tile<Cfg8w64x96k4>(g, L, stream);
@@ -1275,13 +1400,14 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 11: return launch_tile<Cfg8w64x96k4m16>(g, L, stream);
     case 12: return launch_tile<Cfg8w64x128lf>(g, L, stream);
     case 13: return launch_tile<Cfg8w64x128lf3>(g, L, stream);
+    case 14: return launch_tile<Cfg8w64x128ci>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }
 
 // The grouped kernel is built for the 256 x 128 tiles on 8 waves (configurations 1, 4
-// and 5) and the 256 x 256 tiles of configuration 13; the 256 x 192 ones leave no registers
-// for the jobs' fields.
+// and 5) and the 256 x 256 tiles of configuration 13 (with configuration 14's schedule it
+// spills a register); the 256 x 192 ones leave no registers for the jobs' fields.
 bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5 || cfg == 13; }
 
 bool gemm_group_ok(const GemmLaunch* L, int n) {

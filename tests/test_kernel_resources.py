@@ -11,11 +11,12 @@ from paper_2609_24519_amd import build
 
 
 def _cfg(*t):
+    t = t + (0,) * (12 - len(t))
     return "CfgI" + "".join("Li%dE" % v for v in t) + "EE"
 
 
 # (waves M, waves N, blocks M, blocks N, k-steps per stage, stages, read-ahead, format, planes,
-#  MFMA shape, blocks per wave whose int32 fold accumulators live in LDS)
+#  MFMA shape, blocks per wave whose int32 fold accumulators live in LDS, schedule)
 DEFAULTS = {
     "E2M1 256x128, 3 k-steps ahead (default for smaller shapes)": _cfg(4, 2, 2, 2, 4, 3, 3, 0, 1, 32, 0),
     "E2M1 256x192, 4 k-steps per stage": _cfg(4, 2, 2, 3, 4, 2, 1, 0, 1, 32, 0),
@@ -25,8 +26,9 @@ DEFAULTS = {
     "E2M1 256x128, 16x16x128, in place": _cfg(4, 2, 2, 2, 4, 3, 0, 0, 1, 16, 0),
     "E2M1 256x192, 16x16x128, in place": _cfg(4, 2, 2, 3, 4, 2, 0, 0, 1, 16, 0),
     "E2M1 256x256, int32 fold of 3 blocks per wave in LDS": _cfg(4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3),
-    "E2M1 256x256, int32 fold of 2 blocks per wave in LDS, 3 stages (default)": _cfg(4, 2, 2, 4, 2, 3, 0, 0,
-                                                                                     1, 32, 2),
+    "E2M1 256x256, int32 fold of 2 blocks per wave in LDS, 3 stages": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2),
+    "E2M1 256x256, as above with the copies after the first MFMAs (default)": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32,
+                                                                                   2, 2),
     "E4M3": _cfg(4, 2, 2, 2, 2, 3, 1, 1, 1, 32, 0),
     "E2M3 256x128, 4 k-steps per stage": _cfg(4, 2, 2, 2, 4, 2, 1, 2, 1, 32, 0),
     "E2M3 weights in the scales": _cfg(4, 2, 2, 2, 2, 2, 1, 2, 2, 32, 0),

@@ -14,8 +14,10 @@ native INT8 MFMA GEMM
 (hipBLASLt through torch._int_mm), one plain MXFP4 GEMM of the vendor library
 (torch._scaled_mm), the residue-number-system route for 53-bit
 integers (the integer layer of Ozaki scheme II) and the sustained rate of the
-FP4 MFMA alone timed in the same run as context, and the oracle timed on the host's cores on
-a bounded sample.
+FP4 MFMA alone timed in the same run as context, the other workloads (INT4 x INT8 in 4
+products at 8192^3; C mod m at 4096^3 for every modulus of the FP64-significand residue set;
+the 4096 x 4096 x 65,536 accumulation stress with int64 C), and the oracle timed on the
+host's cores on a bounded sample.  ``--only <workload>`` times one of those workloads alone.
 """
 import argparse
 import json
@@ -41,6 +43,9 @@ def parse():
     p.add_argument("--no-context", action="store_true", help="skip base-13 and INT8 context")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain 1 GiB device copy (the reference for rocprofv3 byte counters)")
+    p.add_argument("--only", choices=sorted(WORKLOADS), default=None,
+                   help="only time this one workload of the other configurations and print its fields "
+                        "(for kernel traces of that workload)")
     p.add_argument("--ozaki2-only", type=int, default=0, metavar="CALLS",
                    help="only run the residue-number-system route (the ozaki2_int53 context) CALLS "
                         "times and print its timing (for kernel traces of that route)")
@@ -49,6 +54,8 @@ def parse():
                         "MFMA probes run in a loop")
     return p.parse_args()
 
+
+WORKLOADS = ("awe4_int4xint8", "residues_per_modulus", "stress_65536")
 
 CLOCK_PHASES = ("gemm", "gemm_e2m3", "gemm_e2m3_scaled", "probe_static", "probe_varied", "probe_varied_e2m3")
 
@@ -111,6 +118,9 @@ def main():
     if args.ozaki2_only:
         print(json.dumps({"ozaki2_int53": ozaki2_context(dev, reps=args.ozaki2_only)}), flush=True)
         return
+    if args.only:
+        print(json.dumps({args.only: WORKLOAD_FNS[args.only](dev)}), flush=True)
+        return
     M = N = K = args.size
     A_h, B_h = inputs.int8_pair(M, N, K, seed=0)
     A = torch.from_numpy(A_h).to(dev)
@@ -151,6 +161,7 @@ def main():
         return info, wall, enc_ms, gemm_ms
 
     info, wall, enc_ms, gemm_ms = run(awe.ENC_AWE6, args.steps, args.warmup)
+    C_awe6 = C.clone()  # the headline product, compared with the INT8 GEMM below
     ms_step = wall / args.steps * 1e3
     ops = 2.0 * M * N * K
     r = info["r"]
@@ -186,7 +197,8 @@ def main():
             "ms_per_step": round(bwall / max(3, args.steps // 2) * 1e3, 4),
             "gemm_ms": round(bgemm_ms, 4),
             "gemm_exact_TOPS": round(ops / (bgemm_ms * 1e-3) / 1e12, 2),
-            "fp4_peak_frac": round(binfo["r"] * ops / (bgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
+            "fp4_peak_frac": round(binfo["r"] * ops / (bgemm_ms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4),
+            "equal_to_awe6_C": bool(torch.equal(C, C_awe6))}
         try:
             Ci = torch._int_mm(A, B)
             torch.cuda.synchronize()
@@ -199,8 +211,8 @@ def main():
             ims = e0.elapsed_time(e1) / 5
             line["int8_mfma_context"] = {"library": "hipBLASLt via torch._int_mm", "ms": round(ims, 4),
                                          "TOPS": round(ops / (ims * 1e-3) / 1e12, 1)}
-            # both products are exact, so the last AWE result must equal the INT8 GEMM bit for bit
-            line["int8_mfma_context"]["equal_to_exact_C"] = bool(torch.equal(Ci, C))
+            # both products are exact, so the timed AWE6 result must equal the INT8 GEMM bit for bit
+            line["int8_mfma_context"]["equal_to_awe6_C"] = bool(torch.equal(Ci, C_awe6))
         except Exception as ex:  # noqa: BLE001 - context only
             line["int8_mfma_context"] = {"error": str(ex)[:200]}
         line["fp4_vendor_gemm_context"] = fp4_vendor_context(dev, M, N, K, stream)
@@ -254,6 +266,8 @@ def main():
             "fp4_peak_frac": round(tinfo["r"] * ops / (tms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
         del At, pta, ptb
         line["fp16_12_products"] = fp16_context(dev, M)
+        for name in WORKLOADS:
+            line[name] = WORKLOAD_FNS[name](dev)
         line["ozaki2_int53"] = ozaki2_context(dev)
         probe = mfma_sustained()
         if probe and "error" not in probe:
@@ -275,6 +289,137 @@ def main():
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(A_h, B_h)
     print(json.dumps(line), flush=True)
+
+
+def _time_ms(fn, reps, stream):
+    """Average milliseconds of fn() over reps calls, HIP events on `stream` after one warm-up call."""
+    import torch
+
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def awe4_workload(dev, n=8192):
+    """INT4 x INT8 in 4 FP4 products (App. A): A int4 uniform in [-8, 7] (one per int8 byte), B
+    int8 uniform in [-128, 127], seed 0, n^3, int32 C.  GEMM on resident planes (awe_gemm_planes)
+    and end to end (both encoders + GEMM); the FP4 work is 4 products of 2 n^3."""
+    import torch
+
+    from paper_2609_24519_amd import awe, inputs
+
+    A_h, B_h = inputs.int8_pair(n, n, n, seed=0, a_range=(-8, 7))
+    A, B = torch.from_numpy(A_h).to(dev), torch.from_numpy(B_h).to(dev)
+    enc = awe.ENC_AWE4
+    r = awe.get_encoding_info(enc)["r"]
+    pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, n, n), dtype=torch.uint8, device=dev)
+    pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, n, n), dtype=torch.uint8, device=dev)
+    C = torch.empty((n, n), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def enc_both():
+        awe.encode(enc, 0, awe.SIDE_A, A, n, n, n, pa, None, stream)
+        awe.encode(enc, 0, awe.SIDE_B, B, n, n, n, pb, None, stream)
+
+    def gemm():
+        awe.gemm_planes(enc, 0, n, n, n, pa, pb, C, n, awe.I32, 0, stream)
+
+    enc_both()
+    gms = _time_ms(gemm, 10, stream)
+    ems = _time_ms(lambda: (enc_both(), gemm()), 10, stream)
+    ops = 2.0 * n ** 3
+    tf = r * ops / (gms * 1e-3) / 1e12
+    out = {"workload": "INT4xINT8 exact GEMM, M=N=K=%d, A uniform [-8,7], B uniform [-128,127], seed 0, "
+                       "int32 C, %d FP4 products" % (n, r),
+           "gemm_ms": round(gms, 4), "gemm_exact_TOPS": round(ops / (gms * 1e-3) / 1e12, 1),
+           "fp4_TFLOPs": round(tf, 1), "fp4_peak_frac": round(tf / FP4_PEAK_TFLOPS, 4),
+           "end_to_end_ms": round(ems, 4), "end_to_end_exact_TOPS": round(ops / (ems * 1e-3) / 1e12, 1)}
+    del A, B, pa, pb, C
+    torch.cuda.empty_cache()
+    return out
+
+
+def residues_workload(dev, n=4096):
+    """C mod m at n^3 for every modulus of the FP64-significand residue set (Sec. 5.3), operands
+    uniform in [0, m - 1] (seed m), int32 C in [0, m): the mod-m GEMM on resident planes
+    (awe_gemm_planes) and awe_gemm_mod end to end, summed over the moduli; the FP4 work is
+    sum_m r_m 2 n^3."""
+    import torch
+
+    from paper_2609_24519_amd import awe, inputs
+
+    with open(os.path.join(ROOT, "tests", "golden", "moduli_fp64_k16384.txt")) as f:
+        rows = [l for l in f if l.strip() and not l.startswith("#")]
+    moduli = [int(x) for x in rows[0].split()]
+    stream = torch.cuda.current_stream()
+    C = torch.empty((n, n), dtype=torch.int32, device=dev)
+    g_ms = e_ms = 0.0
+    products = 0
+    for m in moduli:
+        A_h, B_h = inputs.residue_pair(n, n, n, m)
+        A, B = torch.from_numpy(A_h).to(dev), torch.from_numpy(B_h).to(dev)
+        r = awe.get_encoding_info(awe.ENC_MOD, m)["r"]
+        products += r
+        pa = torch.empty(awe.plane_bytes(awe.ENC_MOD, m, awe.SIDE_A, n, n), dtype=torch.uint8, device=dev)
+        pb = torch.empty(awe.plane_bytes(awe.ENC_MOD, m, awe.SIDE_B, n, n), dtype=torch.uint8, device=dev)
+        awe.encode(awe.ENC_MOD, m, awe.SIDE_A, A, n, n, n, pa, None, stream)
+        awe.encode(awe.ENC_MOD, m, awe.SIDE_B, B, n, n, n, pb, None, stream)
+        g_ms += _time_ms(lambda: awe.gemm_planes(awe.ENC_MOD, m, n, n, n, pa, pb, C, n, awe.I32, 0, stream),
+                         5, stream)
+        wsn = awe.workspace_bytes(awe.ENC_MOD, m, n, n, n)
+        ws = torch.empty(wsn, dtype=torch.uint8, device=dev)
+        e_ms += _time_ms(lambda: awe.gemm_mod(m, n, n, n, A, n, B, n, C, n, ws, wsn, None, stream), 5, stream)
+        del A, B, pa, pb, ws
+    ops = 2.0 * n ** 3
+    tf = products * ops / (g_ms * 1e-3) / 1e12
+    out = {"workload": "C mod m, M=N=K=%d, operands uniform [0,m-1] seed m, for the %d moduli of the "
+                       "FP64-significand residue set (%d FP4 products in all)" % (n, len(moduli), products),
+           "gemm_ms_sum": round(g_ms, 4), "fp4_TFLOPs": round(tf, 1), "fp4_peak_frac": round(tf / FP4_PEAK_TFLOPS, 4),
+           "end_to_end_ms_sum": round(e_ms, 4)}
+    del C
+    torch.cuda.empty_cache()
+    return out
+
+
+def stress_workload(dev, M=4096, N=4096, K=65536):
+    """Accumulation stress (every entry -128 or 127, structured rows and columns), AWE6, int64 C:
+    the GEMM on resident planes with the default fold segment and with a forced one of 4096."""
+    import torch
+
+    from paper_2609_24519_amd import awe, inputs
+
+    A_h, B_h = inputs.stress_operands(M, N, K, seed=0)
+    A, B = torch.from_numpy(A_h).to(dev), torch.from_numpy(B_h).to(dev)
+    enc = awe.ENC_AWE6
+    r = awe.get_encoding_info(enc)["r"]
+    pa = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_A, M, K), dtype=torch.uint8, device=dev)
+    pb = torch.empty(awe.plane_bytes(enc, 0, awe.SIDE_B, N, K), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    awe.encode(enc, 0, awe.SIDE_A, A, M, K, K, pa, None, stream)
+    awe.encode(enc, 0, awe.SIDE_B, B, N, K, N, pb, None, stream)
+    del A, B
+    C = torch.empty((M, N), dtype=torch.int64, device=dev)
+    ops = 2.0 * M * N * K
+    out = {"workload": "AWE6 exact GEMM, M=N=%d, K=%d, entries -128 or 127 (structured stress operands), "
+                       "int64 C" % (M, K)}
+    for name, kseg in (("default_fold_segment", 0), ("fold_segment_4096", 4096)):
+        ms = _time_ms(lambda: awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I64, kseg, stream), 5, stream)
+        tf = r * ops / (ms * 1e-3) / 1e12
+        out[name] = {"gemm_ms": round(ms, 4), "gemm_exact_TOPS": round(ops / (ms * 1e-3) / 1e12, 1),
+                     "fp4_TFLOPs": round(tf, 1), "fp4_peak_frac": round(tf / FP4_PEAK_TFLOPS, 4)}
+    del pa, pb, C
+    torch.cuda.empty_cache()
+    return out
+
+
+WORKLOAD_FNS = {"awe4_int4xint8": awe4_workload, "residues_per_modulus": residues_workload,
+                "stress_65536": stress_workload}
 
 
 def fp16_context(dev, n):
@@ -578,10 +723,22 @@ def cpu_baseline(A_h, B_h, target_s=15.0):
     dt = time.perf_counter() - t0
     macs = rows * N * K
     return {"value": round(2.0 * macs / dt / 1e12, 6), "unit": "TOPS", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "host_cpus": os.cpu_count(), "cpu_model": cpu_model(),
             "sample": "rows 0..%d of C over full N=%d, K=%d (%d MACs), %.1f s"
                       % (rows - 1, N, K, macs, dt),
             "other_workloads": cpu_oracle_timings()}
+
+
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_oracle_timings():

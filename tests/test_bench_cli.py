@@ -85,3 +85,15 @@ def test_kernel_labels():
     assert profiling._short(ns + "encode_kernel<false>(unsigned char const*)") == "encode_kernel (A side)"
     assert profiling._short(ns + "gemm_group_kernel<Cfg<4> >(GroupArgs)") == "gemm_group_kernel"
     assert profiling._short(ns + "gemm_kernel<Cfg<4> >(GemmArgs)") == "gemm_kernel"
+
+
+def test_cpu_model_and_workload_names():
+    sys.path.insert(0, ROOT)
+    import bench
+
+    m = bench.cpu_model()
+    assert m is None or (isinstance(m, str) and m)
+    assert set(bench.WORKLOADS) == set(bench.WORKLOAD_FNS)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--only", "nonsense"],
+                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    assert r.returncode == 2 and "invalid choice" in r.stderr

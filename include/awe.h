@@ -197,6 +197,26 @@ awe_status awe_gemm_exact(awe_encoding enc, int64_t M, int64_t N, int64_t K,
                           void* workspace, size_t ws_bytes, int32_t* d_range_flag,
                           hipStream_t stream);
 
+/* Bytes of the fixed device array that holds the planes of awe_gemm_exact_noalloc. */
+#define AWE_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+   loops, harnesses that forbid allocation): awe_gemm_exact without a workspace.  Both sides'
+   stored planes go to a fixed device array of AWE_NOALLOC_MAX_BYTES bytes inside the library
+   (one per GPU the library runs on, held until the process ends); the call allocates nothing
+   and calls no allocating routine.  Arguments, layouts, results and errors as awe_gemm_exact,
+   and AWE_ERR_WORKSPACE when awe_workspace_bytes for these sizes exceeds AWE_NOALLOC_MAX_BYTES
+   (nothing is enqueued then).  Every call on a GPU uses that GPU's one array, which keeps the
+   last call's planes (a call reads only planes it has written): calls that overlap on one GPU
+   (other streams, other threads) race on it and give wrong results; order them on one stream.
+   The first call on a device looks up the array's address (host side), and like awe_gemm_exact
+   sets the GEMM's LDS limit and, for AWE_ENC_FP16, uploads its code table: make that first
+   call eagerly before capturing the call into a graph. */
+awe_status awe_gemm_exact_noalloc(awe_encoding enc, int64_t M, int64_t N, int64_t K,
+                                  const void* A, int64_t lda, const void* B, int64_t ldb,
+                                  void* C, int64_t ldc, awe_dtype c_type, int32_t* d_range_flag,
+                                  hipStream_t stream);
+
 /* C = (A B) mod m in [0, m), residue operands in [0, m) as uint8 (Sec. 5.3). */
 awe_status awe_gemm_mod(int32_t m, int64_t M, int64_t N, int64_t K,
                         const uint8_t* A, int64_t lda, const uint8_t* B, int64_t ldb,

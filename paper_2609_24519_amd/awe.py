@@ -31,6 +31,7 @@ I32, I64 = 0, 1
 
 MAX_LIMBS, MAX_PLANES, MAX_PRODUCTS = 4, 8, 16
 K_PAD = 256  # AWE_K_PAD: stored planes pad the reduction length to a multiple of this
+NOALLOC_MAX_BYTES = 64 << 20  # AWE_NOALLOC_MAX_BYTES: the planes array of gemm_exact_noalloc
 
 
 class EncodingInfo(ctypes.Structure):
@@ -84,6 +85,8 @@ def lib():
                                      _P, _SZ, _P, _P]
         L.awe_gemm_mod.argtypes = [_I32, _I64, _I64, _I64, _P, _I64, _P, _I64, _P, _I64,
                                    _P, _SZ, _P, _P]
+        L.awe_gemm_exact_noalloc.argtypes = [_I32, _I64, _I64, _I64, _P, _I64, _P, _I64, _P, _I64, _I32,
+                                             _P, _P]
         L.awe_residues.argtypes = [_P, _I64, _I64, _I64, _I64, _P, _I32, _P, _I64, _P, _P]
         L.awe_crt.argtypes = [_P, _I64, _I64, _I64, _I64, _P, _I32, _P, _P, _I64, _P]
         L.awe_crt_workspace_bytes.argtypes = [_P, _I32, _I64, _I64, _I64, ctypes.POINTER(_SZ)]
@@ -94,7 +97,8 @@ def lib():
         L.awe_last_error.argtypes = []
         L.awe_last_error.restype = ctypes.c_char_p
         for name in ("awe_get_encoding_info", "awe_get_plane_table", "awe_plane_bytes", "awe_encode",
-                     "awe_gemm_planes", "awe_workspace_bytes", "awe_gemm_exact", "awe_gemm_mod",
+                     "awe_gemm_planes", "awe_workspace_bytes", "awe_gemm_exact", "awe_gemm_exact_noalloc",
+                     "awe_gemm_mod",
                      "awe_residues", "awe_crt", "awe_crt_workspace_bytes", "awe_gemm_crt"):
             getattr(L, name).restype = _I32
         _lib = L
@@ -198,6 +202,11 @@ def gemm_exact(enc, M, N, K, A, lda, B, ldb, C, ldc, c_type, workspace, ws_bytes
     _check(lib().awe_gemm_exact(enc, M, N, K, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, c_type,
                                 _ptr(workspace), ws_bytes, _ptr(d_range_flag), _stream(stream)),
            "awe_gemm_exact")
+
+
+def gemm_exact_noalloc(enc, M, N, K, A, lda, B, ldb, C, ldc, c_type, d_range_flag=None, stream=None):
+    _check(lib().awe_gemm_exact_noalloc(enc, M, N, K, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, c_type,
+                                        _ptr(d_range_flag), _stream(stream)), "awe_gemm_exact_noalloc")
 
 
 def gemm_mod(m, M, N, K, A, lda, B, ldb, C, ldc, workspace, ws_bytes, d_range_flag=None, stream=None):

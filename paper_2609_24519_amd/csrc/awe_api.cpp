@@ -477,6 +477,26 @@ awe_status awe_gemm_exact(awe_encoding enc, int64_t M, int64_t N, int64_t K, con
                     stream);
 }
 
+awe_status awe_gemm_exact_noalloc(awe_encoding enc, int64_t M, int64_t N, int64_t K, const void* A,
+                                  int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+                                  awe_dtype c_type, int32_t* d_range_flag, hipStream_t stream) {
+  if (enc == AWE_ENC_MOD) return fail(AWE_ERR_INVALID_VALUE, "use awe_gemm_mod for residues");
+  if (M < 0 || N < 0 || K < 0) return fail(AWE_ERR_INVALID_VALUE, "negative size");
+  awe_status st;
+  const Scheme* s = scheme_or_fail(enc, 0, &st);
+  if (!s) return st;
+  const size_t need = (size_t)round_up((int64_t)side_bytes(*s, true, M, K), 256) + side_bytes(*s, false, N, K);
+  if (need > kNoallocBytes)
+    return fail(AWE_ERR_WORKSPACE, "the planes of this product need " + std::to_string(need) +
+                                       " bytes; the fixed planes array holds " + std::to_string(kNoallocBytes));
+  void* ws = nullptr;
+  if (M > 0 && N > 0) {
+    st = noalloc_planes(&ws);
+    if (st != AWE_OK) return st;
+  }
+  return exact_impl(*s, M, N, K, A, lda, B, ldb, C, ldc, c_type, ws, kNoallocBytes, d_range_flag, stream);
+}
+
 awe_status awe_gemm_mod(int32_t m, int64_t M, int64_t N, int64_t K, const uint8_t* A, int64_t lda,
                         const uint8_t* B, int64_t ldb, int32_t* C, int64_t ldc, void* workspace,
                         size_t ws_bytes, int32_t* d_range_flag, hipStream_t stream) {

@@ -230,4 +230,10 @@ awe_status launch_crt(const int32_t* res, int64_t res_stride, int64_t rows, int6
 
 void set_error(const std::string& msg);
 
+// Bytes of the fixed device array that holds the planes of awe_gemm_exact_noalloc.
+constexpr size_t kNoallocBytes = AWE_NOALLOC_MAX_BYTES;
+// Device address of that array on the current device (looked up once per device, with that
+// device current; no allocation).
+awe_status noalloc_planes(void** out);
+
 }  // namespace awe

@@ -18,6 +18,11 @@ namespace awe {
 // kernel arguments, so they live in device memory of the module.
 __device__ uint32_t g_wide_lut[2][kWideValues];
 
+// The planes of awe_gemm_exact_noalloc: a fixed array of the module, one per GPU the library
+// runs on, held until the process ends.  Host code never passes its name to a kernel (on the
+// host it is only a stand-in for the symbol): noalloc_planes() looks up its device address.
+static __device__ __align__(256) uint8_t scratch[kNoallocBytes];
+
 namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
@@ -1303,6 +1308,30 @@ awe_status ensure_wide_table(const EncodeLaunch& e) {
     return AWE_ERR_HIP;
   }
   loaded[{dev, e.side}] = e.table_key;
+  return AWE_OK;
+}
+
+awe_status noalloc_planes(void** out) {
+  static std::mutex mu;
+  static std::map<int, void*> ptrs;
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) {
+    set_error(std::string("planes array: ") + hipGetErrorString(err));
+    return AWE_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = ptrs.find(dev);
+  if (it == ptrs.end()) {
+    void* p = nullptr;
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess || p == nullptr) {
+      set_error(std::string("planes array address: ") + hipGetErrorString(err));
+      return AWE_ERR_HIP;
+    }
+    it = ptrs.emplace(dev, p).first;
+  }
+  *out = it->second;
   return AWE_OK;
 }
 

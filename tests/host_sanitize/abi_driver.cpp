@@ -71,6 +71,23 @@ int main() {
         expect(awe_gemm_mod(m, 300, 200, 1100, (const uint8_t*)fake, 1100, (const uint8_t*)fake, 200,
                             (int32_t*)fake, 200, fake, (size_t)1 << 40, nullptr, nullptr),
                AWE_OK, "gemm_mod");
+      if (m == 0) {
+        // the allocation-free variant: small sizes run, sizes whose planes exceed the fixed array
+        // and negative sizes are refused
+        expect(awe_gemm_exact_noalloc((awe_encoding)enc, 300, 200, 1100, fake, 1100, fake, 200, fake, 200, AWE_I64,
+                                      nullptr, nullptr),
+               AWE_OK, "gemm_exact_noalloc");
+        expect(awe_gemm_exact_noalloc((awe_encoding)enc, 8192, 8192, 8192, fake, 8192, fake, 8192, fake, 8192,
+                                      AWE_I64, nullptr, nullptr),
+               AWE_ERR_WORKSPACE, "gemm_exact_noalloc, planes past the array");
+        expect(awe_gemm_exact_noalloc((awe_encoding)enc, -1, 200, 1100, fake, 1100, fake, 200, fake, 200, AWE_I64,
+                                      nullptr, nullptr),
+               AWE_ERR_INVALID_VALUE, "gemm_exact_noalloc, negative M");
+      } else {
+        expect(awe_gemm_exact_noalloc((awe_encoding)enc, 300, 200, 1100, fake, 1100, fake, 200, fake, 200, AWE_I32,
+                                      nullptr, nullptr),
+               AWE_ERR_INVALID_VALUE, "gemm_exact_noalloc, residues");
+      }
     }
   }
   // the FP64-significand residue set

@@ -25,4 +25,10 @@ awe_status launch_crt(const int32_t*, int64_t, int64_t, int64_t, int64_t, const 
   ++g_launches;
   return AWE_OK;
 }
+// a host buffer stands in for the device planes array (the stubbed launchers never touch it)
+awe_status noalloc_planes(void** out) {
+  static unsigned char planes[256];
+  *out = planes;
+  return AWE_OK;
+}
 }  // namespace awe

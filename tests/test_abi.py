@@ -210,3 +210,26 @@ def test_empty_problems_are_noops():
     assert L.awe_gemm_planes(awe.ENC_AWE6, 0, 64, 0, 64, None, None, None, 0, awe.I32, 0,
                              None) == awe.OK
     assert L.awe_encode(awe.ENC_AWE6, 0, awe.SIDE_A, None, 0, 64, 64, None, None, None) == awe.OK
+
+
+def test_library_imports_no_device_allocation_routine():
+    # the library allocates no memory itself (awe_gemm_exact_noalloc relies on it): its dynamic
+    # imports hold no HIP allocation or free routine
+    import shutil
+    import subprocess
+
+    if not shutil.which("nm"):
+        pytest.skip("nm not found")
+    out = subprocess.run(["nm", "-D", "--undefined-only", awe.LIB_PATH], stdout=subprocess.PIPE,
+                         text=True, check=True).stdout
+    names = [l.split()[-1].split("@")[0] for l in out.splitlines() if l.strip()]
+    assert "hipGetSymbolAddress" in names
+    bad = [n for n in names if n.startswith("hip") and any(w in n for w in ("Malloc", "Free", "Alloc", "MemPool"))]
+    assert not bad, bad
+
+
+def test_noalloc_limit_matches_header():
+    import re
+    with open(awe.HEADER) as f:
+        m = re.search(r"#define AWE_NOALLOC_MAX_BYTES \(\(size_t\)(\d+) << (\d+)\)", f.read())
+    assert int(m.group(1)) << int(m.group(2)) == awe.NOALLOC_MAX_BYTES

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 
@@ -63,6 +64,31 @@ int64_t launch_k_limit(const Scheme& s) {
     per_k = (int64_t(1) << s.log2D) * max_abs_input(s, true) * max_abs_input(s, false);
   }
   return std::max<int64_t>(lim / per_k / kKPad * kKPad, kKPad);
+}
+
+// Whether the scheme's products are all nine pairs (i, j) of 3 E2M1 planes per side in one
+// launch group, with a coefficient that depends on i + j only (base-13: 13^(i + j)); then
+// ell_d[i + j] receives it.  AWE_GEMM_ALLPAIRS=0 keeps such schemes on the product-major
+// stream (for comparison).
+bool all_pairs_by_sum(const Scheme& s, int64_t* ell_d) {
+  const char* e = getenv("AWE_GEMM_ALLPAIRS");
+  if (e && atoi(e) == 0) return false;
+  if (s.n_lgroups != 1 || s.na != 3 || s.nb != 3 || s.r != 9 || s.scale_weights || s.wide) return false;
+  for (int k = 0; k < 3; ++k)
+    if (s.fmt_a[k] != kFmtE2M1 || s.fmt_b[k] != kFmtE2M1) return false;
+  bool seen[3][3] = {};
+  bool have[5] = {};
+  for (int k = 0; k < s.r; ++k) {
+    const int i = s.pa[k], j = s.pb[k];
+    if (i < 0 || i > 2 || j < 0 || j > 2 || seen[i][j]) return false;
+    seen[i][j] = true;
+    const int64_t l = s.ell[k] / s.louter[0];
+    if (l * s.louter[0] != s.ell[k] || l >= (1 << 23) || l < -(1 << 23)) return false;
+    if (have[i + j] && ell_d[i + j] != l) return false;
+    have[i + j] = true;
+    ell_d[i + j] = l;
+  }
+  return true;
 }
 
 // The launches of one exact or mod-m GEMM on stored planes, in order (every launch after
@@ -139,7 +165,19 @@ awe_status plan_gemm(const Scheme& s, int64_t M, int64_t N, int64_t K, const voi
         L.fold_ell[0] = 1;
         L.fold_mask = 1;
       }
-      for (int k = 0; k < s.r && !L.shared; ++k) {
+      L.allpairs_a = L.allpairs_b = 0;
+      int64_t ell_d[2 * kMaxPlanes] = {};
+      if (!L.shared && all_pairs_by_sum(s, ell_d)) {
+        // every pair (i, j) of the 3 + 3 planes is a product with coefficient ell_d[i + j]: one
+        // stream in which each stage brings the six planes once and the MFMAs of all nine
+        // products add into five accumulators (one per i + j), folded with ell_d
+        L.allpairs_a = L.allpairs_b = 3;
+        L.r = 1;
+        L.pa[0] = L.pb[0] = 0;
+        for (int d = 0; d < 5; ++d) L.fold_ell[d] = (int32_t)ell_d[d];
+        L.fold_mask = 1;
+      }
+      for (int k = 0; k < s.r && !L.shared && !L.allpairs_a; ++k) {
         if (s.lgroup[k] != g) continue;
         L.pa[L.r] = s.pa[k] - first_a;
         L.pb[L.r] = s.pb[k] - first_b;

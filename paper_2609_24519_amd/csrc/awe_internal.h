@@ -160,6 +160,10 @@ struct GemmLaunch {
   bool shared;                     // two planes per side, every pair one product, one accumulator
   uint32_t scale_a[2], scale_b[2]; // shared: E8M0 scale byte of plane 0 / 1, replicated 4 times
   uint32_t fold_mask;              // bit k: fold after product k
+  // All pairs (planes per side, 0 = off): the stream's one product stands for every pair
+  // (i, j) of the first allpairs_a A planes and allpairs_b B planes, each adding into
+  // accumulator group i + j, folded with fold_ell[i + j].
+  int allpairs_a, allpairs_b;
   int64_t k_seg;                   // fold segment length (multiple of kKPad)
   int64_t k_begin, k_end;          // reduction range of this launch (multiples of kKPad)
   void* C;

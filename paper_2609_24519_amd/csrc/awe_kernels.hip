@@ -293,7 +293,7 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
 template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0,
-          int NPL_ = 1, int MF_ = 32, int NLB_ = 0, int SCHED_ = 0>
+          int NPL_ = 1, int MF_ = 32, int NLB_ = 0, int SCHED_ = 0, int NPA_ = 0, int NPB_ = 0>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
   static constexpr int KST = KST_;        // bricks (64 reduction indices each) per row block and stage
@@ -334,10 +334,21 @@ struct Cfg {
   // into one accumulator).
   static constexpr int NPL = NPL_;
   static_assert(NPL == 1 || (NPL == 2 && FMT == 2), "two planes per side: E2M3 with weights in the scales");
+  // All pairs (NPA > 0): a stage brings NPA planes of A and NPB planes of B, and every pair
+  // (i, j) is a product whose coefficient depends on i + j only, so its MFMAs add into
+  // accumulator group i + j (NG groups), folded once per segment with the group's coefficient
+  // (products with equal coefficients share an accumulator, Alg. 1): each plane is copied once
+  // per stage for all the products that use it.
+  static constexpr int NPA = NPA_, NPB = NPB_;
+  static constexpr bool AP = NPA_ > 0;
+  static constexpr int NG = AP ? NPA + NPB - 1 : 1;
+  static_assert(!AP || (NPB > 0 && FMT == 0 && NPL == 1 && MF == 32 && NLB_ == 0 && SCHED_ == 0),
+                "all pairs: E2M1, 32x32x64 MFMAs, int32 accumulators in registers, schedule 0");
   static constexpr int PA_UNITS = (BM / kBrickRows) * KU;  // per plane and stage: row blocks x units
   static constexpr int PB_UNITS = (BN / kBrickRows) * KU;
-  static constexpr int A_UNITS = NPL * PA_UNITS;
-  static constexpr int B_UNITS = NPL * PB_UNITS;
+  static constexpr int SPA = AP ? NPA : NPL, SPB = AP ? NPB : NPL;  // planes per side in a stage
+  static constexpr int A_UNITS = SPA * PA_UNITS;
+  static constexpr int B_UNITS = SPB * PB_UNITS;
   static constexpr int STAGE_BYTES = (A_UNITS + B_UNITS) * UNIT_BYTES;
   // The int32 fold accumulators of the last NLB accumulator blocks of every wave live in LDS
   // after the ring (each wave its own 4 KiB per block, lane-major), so that a tile whose
@@ -555,7 +566,7 @@ __device__ __forceinline__ v8i frag_fmt(const uint8_t* unit, int i, int lane) {
 template <class C>
 struct Frags {
   // plane pl's fragments at pl * BMW (pl * BNW); 16x16x128: one per 16-row block
-  v8i a[C::MF == 16 ? C::AM : C::NPL * C::BMW], b[C::MF == 16 ? C::AN : C::NPL * C::BNW];
+  v8i a[C::MF == 16 ? C::AM : C::SPA * C::BMW], b[C::MF == 16 ? C::AN : C::SPB * C::BNW];
 };
 
 // 16x16x128 operand fragment: lane L holds row (column) L % 16 of its 16-row block at
@@ -586,16 +597,17 @@ __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, in
   }
   const int u = ks / C::UK, i = ks % C::UK;
 #pragma unroll
-  for (int pl = 0; pl < C::NPL; ++pl) {
+  for (int pl = 0; pl < C::SPA; ++pl)
 #pragma unroll
     for (int ia = 0; ia < C::BMW; ++ia)
       f.a[pl * C::BMW + ia] = frag_fmt<C::FMT>(
           stage + (pl * C::PA_UNITS + (wm * C::BMW + ia) * C::KU + u) * C::UNIT_BYTES, i, lane);
 #pragma unroll
+  for (int pl = 0; pl < C::SPB; ++pl)
+#pragma unroll
     for (int j = 0; j < C::BNW; ++j)
       f.b[pl * C::BNW + j] = frag_fmt<C::FMT>(
           stage + (C::A_UNITS + pl * C::PB_UNITS + (wn * C::BNW + j) * C::KU + u) * C::UNIT_BYTES, i, lane);
-  }
 }
 
 __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
@@ -728,6 +740,7 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
 
   using AccT = std::conditional_t<C::MF == 16, v4f, v16f>;
   AccT acc[C::AM][C::AN];
+  AccT accg[C::AP ? C::NG : 1][C::AM][C::AN];  // all pairs: one accumulator per group i + j
   // Blocks b = i * AN + j < NREG keep their int32 fold accumulators in iacc; the others in this
   // wave's LDS fold area (int32 v of lane L of block b - NREG at ((b - NREG) * AV + v) * 64 + L).
   constexpr int NREG = C::AM * C::AN - C::NLB;
@@ -742,6 +755,16 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
     for (int j = 0; j < C::AN; ++j)
 #pragma unroll
       for (int v = 0; v < C::AV; ++v) acc[i][j][v] = 0.0f;
+  if constexpr (C::AP) {
+#pragma unroll
+    for (int d = 0; d < C::NG; ++d)
+#pragma unroll
+      for (int i = 0; i < C::AM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::AN; ++j)
+#pragma unroll
+          for (int v = 0; v < C::AV; ++v) accg[d][i][j][v] = 0.0f;
+  }
 #pragma unroll
   for (int b = 0; b < NREG; ++b)
 #pragma unroll
@@ -754,6 +777,24 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   // After product p's last stage of a fold segment: fold its FP32 partials into the int32
   // accumulators with the product's coefficient and restart them.
   auto fold_product = [&](int p) {
+    if constexpr (C::AP) {
+      // all pairs: every group's partial with its coefficient (fold_coef of the group index)
+#pragma unroll
+      for (int d = 0; d < C::NG; ++d) {
+        const int32_t l = fold_coef(d);
+#pragma unroll
+        for (int b = 0; b < NREG; ++b) {
+          const int i = b / C::AN, j = b % C::AN;
+#pragma unroll
+          for (int v = 0; v < C::AV; ++v) {
+            iacc[i][j][v] += __mul24(l, (int32_t)accg[d][i][j][v]);
+            accg[d][i][j][v] = 0.0f;
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      return;
+    }
     if ((g.fold_mask >> p) & 1u) {
       const int32_t l = fold_coef(p);
       // one 32x32 block at a time keeps the temporaries of the fold small
@@ -893,6 +934,17 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
                 for (int j = 0; j < C::AN; ++j)
                   acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(cur.a[i], cur.b[j], acc[i][j], 4, 4,
                                                                                0, kScale2, 0, kScale2);
+            } else if constexpr (C::AP) {
+              // every pair (pi, pj) of the stage's planes into accumulator group pi + pj
+#pragma unroll
+              for (int pi = 0; pi < C::NPA; ++pi)
+#pragma unroll
+                for (int pj = 0; pj < C::NPB; ++pj)
+#pragma unroll
+                  for (int i = 0; i < C::BMW; ++i)
+#pragma unroll
+                    for (int j = 0; j < C::BNW; ++j)
+                      mfma_block(accg[pi + pj][i][j], cur.a[pi * C::BMW + i], cur.b[pj * C::BNW + j]);
             } else if constexpr (C::NPL == 2) {
               // the four plane pairs, each block's MFMAs four apart in issue order
 #pragma unroll
@@ -921,7 +973,7 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
               // issue order: one MFMA, then one fragment read of a later k-step (measured
               // 1-3 % faster than all reads ahead of the MFMAs)
 #pragma unroll
-              for (int q = 0; q < C::NPL * C::NPL * C::AM * C::AN; ++q) {
+              for (int q = 0; q < (C::AP ? C::NPA * C::NPB : C::NPL * C::NPL) * C::AM * C::AN; ++q) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // an MFMA
                 __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // an LDS read
               }
@@ -1058,6 +1110,9 @@ using Cfg8w64x128lf = Cfg<4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3>;
 using Cfg8w64x128lf3 = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2>;
 // config 13 with the copies that refill a freed buffer issued after the first MFMAs of the next stage
 using Cfg8w64x128ci = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
+// all pairs of 3 planes per side (9 products, 5 accumulator groups): 128 x 128 on 8 waves of
+// 1 x 2 blocks, 2 k-steps per stage (48 KiB) in 3 stages, fragments read in place
+using Cfg8w32x64ap33 = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3>;
 // E2M3 operands (3 KiB units of two k-steps)
 using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
 using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
@@ -1179,8 +1234,9 @@ void fill_args(const GemmLaunch& L, GemmArgs& g) {
   for (int k = 0; k < L.r; ++k) {
     g.pidx_a |= (uint64_t)(L.pa[k] & 15) << (4 * k);
     g.pidx_b |= (uint64_t)(L.pb[k] & 15) << (4 * k);
-    g.fold_ell[k] = L.fold_ell[k];
   }
+  // (all pairs: one stream product, one coefficient per accumulator group)
+  for (int k = 0; k < kMaxProducts; ++k) g.fold_ell[k] = L.fold_ell[k];
   g.fold_mask = L.fold_mask;
   g.C = L.C;
   g.ldc = L.ldc;
@@ -1438,6 +1494,7 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   GemmArgs g{};
   fill_args(L, g);
   if (L.fmt == kFmtE4M3) return launch_tile<Cfg8w64x64e4m3>(g, L, stream);
+  if (L.allpairs_a == 3 && L.allpairs_b == 3) return launch_tile<Cfg8w32x64ap33>(g, L, stream);
   if (L.shared) {
     for (int k = 0; k < 2; ++k) {
       g.sa[k] = L.scale_a[k];
@@ -1484,7 +1541,8 @@ bool gemm_group_ok(const GemmLaunch* L, int n) {
   if (!group_cfg(choose_group_cfg(L, n))) return false;
   for (int j = 0; j < n; ++j) {
     const GemmLaunch& a = L[j];
-    if (a.fmt != kFmtE2M1 || a.shared || a.accumulate || a.r < 1 || a.r > kGroupProducts) return false;
+    if (a.fmt != kFmtE2M1 || a.shared || a.allpairs_a || a.accumulate || a.r < 1 || a.r > kGroupProducts)
+      return false;
     if (a.M != L[0].M || a.N != L[0].N || a.K != L[0].K || a.k_begin != L[0].k_begin ||
         a.k_end != L[0].k_end || a.k_end <= a.k_begin)
       return false;

@@ -243,6 +243,7 @@ def test_every_tile_configuration(monkeypatch, cfg, enc):
     # the int32 fold accumulators in LDS, copies issued before or after the first MFMAs of a
     # stage); every one must give the exact product
     monkeypatch.setenv("AWE_GEMM_CFG", cfg)
+    monkeypatch.setenv("AWE_GEMM_ALLPAIRS", "0")  # base-13 on the product-major stream here
     M, N, K = 300, 420, 1100
     A, B = _operands(enc, M, N, K, seed=int(cfg) + 40)
     C = _run_exact(enc, A, B)
@@ -388,3 +389,36 @@ def test_fp6p4_8192_sampled():
     for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=3):
         ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
         assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)
+
+
+@pytest.mark.parametrize("allpairs", ["1", "0"])
+@pytest.mark.parametrize("shape,out,kseg", [((1, 1, 1), torch.int32, 0), ((300, 420, 1100), torch.int32, 0),
+                                            ((129, 513, 3000), torch.int64, 256),
+                                            ((700, 300, 2100), torch.int64, 512)])
+def test_base13_all_pairs_stream(monkeypatch, allpairs, shape, out, kseg):
+    # base-13's nine limb pairs with one accumulator per coefficient 13^(i + j): each stage
+    # brings the three planes of each side once (default), or the product-major stream
+    # (AWE_GEMM_ALLPAIRS=0); ragged shapes, both outputs, forced fold segments
+    monkeypatch.setenv("AWE_GEMM_ALLPAIRS", allpairs)
+    M, N, K = shape
+    enc = awe.ENC_B13
+    A, B = _operands(enc, M, N, K, seed=M + N + K)
+    A[0, :] = -128
+    B[:, 0] = -128
+    pa, pb = _planes(enc, 0, A, B)
+    C = torch.empty((M, N), dtype=out, device="cuda")
+    awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I64 if out == torch.int64 else awe.I32, kseg)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy().astype(np.int64), og.gemm_i64(A, B))
+
+
+@pytest.mark.parametrize("cus", ["12", "16"])
+def test_base13_all_pairs_split_last_round(monkeypatch, cus):
+    # a ragged last round of 128 x 128 all-pairs tiles split along the reduction (atomics into C)
+    monkeypatch.setenv("AWE_GEMM_CUS", cus)
+    M, N, K = 1100, 700, 2100
+    A, B = _operands(awe.ENC_B13, M, N, K, seed=13)
+    C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_B13, torch.int32)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy().astype(np.int64), og.gemm_i64(A, B))
+

@@ -91,6 +91,35 @@ bool all_pairs_by_sum(const Scheme& s, int64_t* ell_d) {
   return true;
 }
 
+// Whether the scheme's products are (3k + t, 3l + t) for t < 3 and k, l < 2 with coefficient
+// inner[t] * outer[k + l], in launch group k + l of outer weight outer[k + l] (the 12-bit
+// significand scheme: two halves of three planes per side, App. A); then inner and outer receive
+// them.  Such a scheme runs as one launch: stream product t brings planes t and t + 3 of each
+// side, and its four pairs add into three accumulator groups, one per k + l.  AWE_GEMM_ALLPAIRS=0
+// keeps it on one launch per group.
+bool pairs_of_halves(const Scheme& s, int64_t* inner, int64_t* outer) {
+  const char* e = getenv("AWE_GEMM_ALLPAIRS");
+  if (e && atoi(e) == 0) return false;
+  if (s.n_lgroups != 3 || s.na != 6 || s.nb != 6 || s.r != 12 || s.scale_weights || s.modulus) return false;
+  for (int k = 0; k < 6; ++k)
+    if (s.fmt_a[k] != kFmtE2M1 || s.fmt_b[k] != kFmtE2M1) return false;
+  bool seen[3][2][2] = {}, have[3] = {};
+  for (int q = 0; q < s.r; ++q) {
+    const int t = s.pa[q] % 3, k = s.pa[q] / 3, l = s.pb[q] / 3;
+    if (s.pa[q] < 0 || s.pa[q] > 5 || s.pb[q] < 0 || s.pb[q] > 5 || s.pb[q] % 3 != t || seen[t][k][l] ||
+        s.lgroup[q] != k + l)
+      return false;
+    seen[t][k][l] = true;
+    const int64_t o = s.louter[k + l], in = s.ell[q] / o;
+    if (in * o != s.ell[q] || in >= (1 << 23) || in < -(1 << 23) || o > 0x7fffffff) return false;
+    if (have[t] && inner[t] != in) return false;
+    have[t] = true;
+    inner[t] = in;
+    outer[k + l] = o;
+  }
+  return true;
+}
+
 // The launches of one exact or mod-m GEMM on stored planes, in order (every launch after
 // the first adds into C); nothing is enqueued.
 awe_status plan_gemm(const Scheme& s, int64_t M, int64_t N, int64_t K, const void* pa, const void* pb,
@@ -136,6 +165,31 @@ awe_status plan_gemm(const Scheme& s, int64_t M, int64_t N, int64_t K, const voi
     L.k_begin = L.k_end = 0;
     L.accumulate = false;
     plan->push_back(L);
+    return AWE_OK;
+  }
+  int64_t inner[3] = {}, outer[3] = {};
+  if (pairs_of_halves(s, inner, outer)) {
+    // one launch per reduction range: stream product t = the four pairs of planes t and t + 3;
+    // an FP32 accumulator of group k + l covers at most two products per index
+    L.fmt = kFmtE2M1;
+    L.r = 3;
+    L.allpairs_a = L.allpairs_b = 2;
+    L.outer_groups = true;
+    for (int t = 0; t < 3; ++t) {
+      L.pa[t] = L.pb[t] = t;
+      L.fold_ell[t] = (int32_t)inner[t];
+      L.outer_g[t] = (int32_t)outer[t];
+    }
+    L.fold_mask = 7;
+    L.outer = 1;
+    const int64_t bound = ((int64_t(1) << 23) - 1) / (2 * (int64_t)s.c_a * s.c_b) / kKPad * kKPad;
+    L.k_seg = std::max<int64_t>(kKPad, std::min<int64_t>(own_seg ? s.k_seg : k_seg, bound));
+    for (int64_t k0 = 0; k0 < kp; k0 += step) {
+      L.k_begin = k0;
+      L.k_end = std::min(kp, k0 + step);
+      L.accumulate = k0 > 0;
+      plan->push_back(L);
+    }
     return AWE_OK;
   }
   // one launch per (reduction range, launch group); every launch after the first adds into C

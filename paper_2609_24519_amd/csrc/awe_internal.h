@@ -164,6 +164,11 @@ struct GemmLaunch {
   // (i, j) of the first allpairs_a A planes and allpairs_b B planes, each adding into
   // accumulator group i + j, folded with fold_ell[i + j].
   int allpairs_a, allpairs_b;
+  // With outer groups: pair (i, j) of the stream product's planes (stored planes k + 3 i and
+  // k + 3 j) adds into group i + j, which folds with the product's coefficient into its own
+  // int32 accumulator; C (+)= sum_d outer_g[d] (group d's sum / D).
+  bool outer_groups;
+  int32_t outer_g[3];
   int64_t k_seg;                   // fold segment length (multiple of kKPad)
   int64_t k_begin, k_end;          // reduction range of this launch (multiples of kKPad)
   void* C;

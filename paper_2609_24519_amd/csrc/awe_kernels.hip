@@ -293,7 +293,8 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
 template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0,
-          int NPL_ = 1, int MF_ = 32, int NLB_ = 0, int SCHED_ = 0, int NPA_ = 0, int NPB_ = 0>
+          int NPL_ = 1, int MF_ = 32, int NLB_ = 0, int SCHED_ = 0, int NPA_ = 0, int NPB_ = 0, int PSTEP_ = 1,
+          int OUTG_ = 0>
 struct Cfg {
   static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
   static constexpr int KST = KST_;        // bricks (64 reduction indices each) per row block and stage
@@ -342,6 +343,15 @@ struct Cfg {
   static constexpr int NPA = NPA_, NPB = NPB_;
   static constexpr bool AP = NPA_ > 0;
   static constexpr int NG = AP ? NPA + NPB - 1 : 1;
+  // A stage's plane pl is stored plane (first plane of the stream product) + pl * PSTEP.
+  static constexpr int PSTEP = PSTEP_;
+  // Outer groups (OUTG = 1, all pairs only): each group i + j has its own int32 accumulator,
+  // into which the stream product's coefficient folds it; the epilogue adds the groups with
+  // their outer weights (GemmArgs::outer_g) in int64.  Otherwise all groups fold into one int32
+  // accumulator with the group's coefficient.
+  static constexpr int OUTG = OUTG_;
+  static constexpr int NOUT = OUTG ? NG : 1;
+  static_assert(!OUTG || AP, "outer groups belong to the all-pairs stream");
   static_assert(!AP || (NPB > 0 && FMT == 0 && NPL == 1 && MF == 32 && NLB_ == 0 && SCHED_ == 0),
                 "all pairs: E2M1, 32x32x64 MFMAs, int32 accumulators in registers, schedule 0");
   static constexpr int PA_UNITS = (BM / kBrickRows) * KU;  // per plane and stage: row blocks x units
@@ -398,6 +408,7 @@ struct GemmArgs {
   // each computed by `split` workgroups over consecutive parts of the reduction range,
   // which add their exact partial results into C (zeroed beforehand) with atomics.
   int32_t n_full, split;
+  int32_t outer_g[4];  // outer weight of accumulator group d (all pairs with outer groups)
 };
 
 // Position in the reduction stream: product p, k-tile t, current fold segment [cs, ce).
@@ -471,7 +482,7 @@ __device__ __forceinline__ void load_stage_a(const GemmArgs& g, const Cursor& c,
     const int rb = min(tm * (C::BM / kBrickRows) + r / C::KU, g.rba - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pa + pl * g.stride_a + ((int64_t)(r % C::KU) * g.rba + rb) * UB + h * kBrickBytes, voff,
+      dma_brick(pa + (int64_t)pl * C::PSTEP * g.stride_a + ((int64_t)(r % C::KU) * g.rba + rb) * UB + h * kBrickBytes, voff,
                 stage_lds + id * UB + h * kBrickBytes);
   }
 }
@@ -491,7 +502,7 @@ __device__ __forceinline__ void load_stage_b(const GemmArgs& g, const Cursor& c,
     const int cb = min(tn * (C::BN / kBrickRows) + r / C::KU, g.rbb - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pb + pl * g.stride_b + ((int64_t)(r % C::KU) * g.rbb + cb) * UB + h * kBrickBytes, voff,
+      dma_brick(pb + (int64_t)pl * C::PSTEP * g.stride_b + ((int64_t)(r % C::KU) * g.rbb + cb) * UB + h * kBrickBytes, voff,
                 stage_lds + (C::A_UNITS + id) * UB + h * kBrickBytes);
   }
 }
@@ -653,10 +664,28 @@ __device__ __forceinline__ void tile_of_block(const GemmArgs& g, int bid, int& t
 // group of a wider scheme contributes outer * (its sum / D).  C is written with
 // non-temporal stores where it is not read back (C is not reused by the kernel,
 // and all tiles of a round write at once: measured 2 % faster at 8192^3).
-__device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col, int32_t val) {
+__device__ __forceinline__ void store_value(const GemmArgs& g, int row, int col, int64_t t) {
   if (row >= g.M || col >= g.N) return;
   const int64_t off = (int64_t)row * g.ldc + col;
+  if (g.c64) {
+    int64_t* Cp = reinterpret_cast<int64_t*>(g.C);
+    if (g.accumulate)
+      Cp[off] += t;
+    else
+      __builtin_nontemporal_store(t, Cp + off);
+  } else {
+    int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
+    if (g.accumulate)
+      Cp[off] = (int32_t)((uint32_t)Cp[off] + (uint32_t)t);
+    else
+      __builtin_nontemporal_store((int32_t)t, Cp + off);
+  }
+}
+
+__device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col, int32_t val) {
   if (g.modulus) {
+    if (row >= g.M || col >= g.N) return;
+    const int64_t off = (int64_t)row * g.ldc + col;
     const int32_t m = g.modulus;
     int32_t rr = val % m;
     if (rr < 0) rr += m;
@@ -665,35 +694,25 @@ __device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col
       Cp[off] = (Cp[off] + rr) % m;
     else
       __builtin_nontemporal_store(rr, Cp + off);
-  } else {
-    const int64_t t = (int64_t)(val >> g.log2D) * g.outer;
-    if (g.c64) {
-      int64_t* Cp = reinterpret_cast<int64_t*>(g.C);
-      if (g.accumulate)
-        Cp[off] += t;
-      else
-        __builtin_nontemporal_store(t, Cp + off);
-    } else {
-      int32_t* Cp = reinterpret_cast<int32_t*>(g.C);
-      if (g.accumulate)
-        Cp[off] = (int32_t)((uint32_t)Cp[off] + (uint32_t)t);
-      else
-        __builtin_nontemporal_store((int32_t)t, Cp + off);
-    }
+    return;
   }
+  store_value(g, row, col, (int64_t)(val >> g.log2D) * g.outer);
 }
 
 // A part of a split tile: its exact partial (a whole number of reduction
 // indices with all products, so a multiple of D) is added atomically into C,
 // which the host zeroed (or which holds an earlier launch's sum).
-__device__ __forceinline__ void add_output(const GemmArgs& g, int row, int col, int32_t val) {
+__device__ __forceinline__ void add_value(const GemmArgs& g, int row, int col, int64_t t) {
   if (row >= g.M || col >= g.N) return;
   const int64_t off = (int64_t)row * g.ldc + col;
-  const int64_t t = (int64_t)(val >> g.log2D) * g.outer;
   if (g.c64)
     atomicAdd(reinterpret_cast<unsigned long long*>(g.C) + off, (unsigned long long)t);
   else
     atomicAdd(reinterpret_cast<int32_t*>(g.C) + off, (int32_t)t);
+}
+
+__device__ __forceinline__ void add_output(const GemmArgs& g, int row, int col, int32_t val) {
+  add_value(g, row, col, (int64_t)(val >> g.log2D) * g.outer);
 }
 
 // Zeroes the C region of the split tiles before the parts add into it: block
@@ -741,6 +760,7 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   using AccT = std::conditional_t<C::MF == 16, v4f, v16f>;
   AccT acc[C::AM][C::AN];
   AccT accg[C::AP ? C::NG : 1][C::AM][C::AN];  // all pairs: one accumulator per group i + j
+  int32_t iaccg[C::NOUT][C::AM][C::AN][C::AV];   // outer groups: one int32 accumulator per group
   // Blocks b = i * AN + j < NREG keep their int32 fold accumulators in iacc; the others in this
   // wave's LDS fold area (int32 v of lane L of block b - NREG at ((b - NREG) * AV + v) * 64 + L).
   constexpr int NREG = C::AM * C::AN - C::NLB;
@@ -763,7 +783,10 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
 #pragma unroll
         for (int j = 0; j < C::AN; ++j)
 #pragma unroll
-          for (int v = 0; v < C::AV; ++v) accg[d][i][j][v] = 0.0f;
+          for (int v = 0; v < C::AV; ++v) {
+            accg[d][i][j][v] = 0.0f;
+            if constexpr (C::OUTG) iaccg[d][i][j][v] = 0;
+          }
   }
 #pragma unroll
   for (int b = 0; b < NREG; ++b)
@@ -777,7 +800,27 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   // After product p's last stage of a fold segment: fold its FP32 partials into the int32
   // accumulators with the product's coefficient and restart them.
   auto fold_product = [&](int p) {
-    if constexpr (C::AP) {
+    if constexpr (C::OUTG) {
+      // outer groups: every group's partial with the stream product's coefficient, into the
+      // group's own int32 accumulator
+      if ((g.fold_mask >> p) & 1u) {
+        const int32_t l = fold_coef(p);
+#pragma unroll
+        for (int d = 0; d < C::NG; ++d) {
+#pragma unroll
+          for (int i = 0; i < C::AM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::AN; ++j)
+#pragma unroll
+              for (int v = 0; v < C::AV; ++v) {
+                iaccg[d][i][j][v] += __mul24(l, (int32_t)accg[d][i][j][v]);
+                accg[d][i][j][v] = 0.0f;
+              }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      return;
+    } else if constexpr (C::AP) {
       // all pairs: every group's partial with its coefficient (fold_coef of the group index)
 #pragma unroll
       for (int d = 0; d < C::NG; ++d) {
@@ -1008,6 +1051,25 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
     else
       add_output(g, row, col, val);
   };
+  if constexpr (C::OUTG) {
+    // sum_d outer_d (group d's sum / D), exact in int64 (each group's sum is a multiple of D)
+#pragma unroll
+    for (int i = 0; i < C::AM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::AN; ++j)
+#pragma unroll
+        for (int v = 0; v < C::AV; ++v) {
+          int64_t t = 0;
+#pragma unroll
+          for (int d = 0; d < C::NG; ++d) t += (int64_t)(iaccg[d][i][j][v] >> g.log2D) * g.outer_g[d];
+          const int row = row0 + i * BS + 8 * (v >> 2) + (v & 3), col = col0 + j * BS;
+          if (part < 0)
+            store_value(g, row, col, t);
+          else
+            add_value(g, row, col, t);
+        }
+    return;
+  }
 #pragma unroll
   for (int b = 0; b < NREG; ++b)
 #pragma unroll
@@ -1113,6 +1175,10 @@ using Cfg8w64x128ci = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
 // all pairs of 3 planes per side (9 products, 5 accumulator groups): 128 x 128 on 8 waves of
 // 1 x 2 blocks, 2 k-steps per stage (48 KiB) in 3 stages, fragments read in place
 using Cfg8w32x64ap33 = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3>;
+// all pairs of 2 planes per side, 3 apart (the two halves of a 12-bit significand), each group
+// i + j with its own int32 accumulator and outer weight: 128 x 128 on 8 waves of 1 x 2 blocks,
+// 2 k-steps per stage (32 KiB) in 4 stages, fragments read one k-step ahead
+using Cfg8w32x64ap22o = Cfg<4, 2, 1, 2, 2, 4, 1, 0, 1, 32, 0, 0, 2, 2, 3, 1>;
 // E2M3 operands (3 KiB units of two k-steps)
 using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
 using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
@@ -1494,7 +1560,11 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   GemmArgs g{};
   fill_args(L, g);
   if (L.fmt == kFmtE4M3) return launch_tile<Cfg8w64x64e4m3>(g, L, stream);
-  if (L.allpairs_a == 3 && L.allpairs_b == 3) return launch_tile<Cfg8w32x64ap33>(g, L, stream);
+  if (L.allpairs_a == 3 && L.allpairs_b == 3 && !L.outer_groups) return launch_tile<Cfg8w32x64ap33>(g, L, stream);
+  if (L.allpairs_a == 2 && L.allpairs_b == 2 && L.outer_groups) {
+    for (int d = 0; d < 3; ++d) g.outer_g[d] = L.outer_g[d];
+    return launch_tile<Cfg8w32x64ap22o>(g, L, stream);
+  }
   if (L.shared) {
     for (int k = 0; k < 2; ++k) {
       g.sa[k] = L.scale_a[k];

@@ -270,11 +270,17 @@ def test_ternary_4096_sampled():
 
 
 
+@pytest.mark.parametrize("allpairs", ["1", "0"])
 @pytest.mark.parametrize("shape,out", [((70, 45, 500), torch.int32), ((130, 260, 2000), torch.int64),
-                                       ((33, 40, 16384), torch.int64), ((16, 24, 120_000), torch.int64)])
-def test_fp16_12_products(shape, out):
-    # App. A: 12-bit integers (FP16 significands) in 12 FP4 products, run as three launch
-    # groups with outer weights 71^(k+l); the last shape needs several reduction launches
+                                       ((33, 40, 16384), torch.int64), ((16, 24, 120_000), torch.int64),
+                                       ((300, 420, 70_000), torch.int64)])
+def test_fp16_12_products(monkeypatch, allpairs, shape, out):
+    # App. A: 12-bit integers (FP16 significands) in 12 FP4 products, by default one launch per
+    # reduction range in which each stage brings planes t and t + 3 of each side for the four
+    # products (t, k, l) into one accumulator per outer weight 71^(k+l); with
+    # AWE_GEMM_ALLPAIRS=0, one launch per outer weight; the last shapes need several reduction
+    # launches (and, the last, several fold segments)
+    monkeypatch.setenv("AWE_GEMM_ALLPAIRS", allpairs)
     M, N, K = shape
     rng = np.random.default_rng(M + N + K)
     A = inputs.uniform(rng, (M, K), -2048, 2047, np.int16)

@@ -11,6 +11,7 @@
 #include <type_traits>
 
 #include "awe_internal.h"
+#include "gemm_layout.h"
 
 namespace awe {
 
@@ -292,98 +293,6 @@ __global__ __launch_bounds__(256) void encode16_kernel(const int16_t* __restrict
 // ---------------------------------------------------------------------------
 constexpr uint32_t kScale2 = 0x80808080u;  // E8M0 2^1 in every byte
 
-template <int WM_, int WN_, int BMW_, int BNW_, int KST_, int NSTAGE_, int PD_ = 1, int FMT_ = 0,
-          int NPL_ = 1, int MF_ = 32, int NLB_ = 0, int SCHED_ = 0, int NPA_ = 0, int NPB_ = 0, int PSTEP_ = 1,
-          int OUTG_ = 0>
-struct Cfg {
-  static constexpr int WM = WM_, WN = WN_, BMW = BMW_, BNW = BNW_;
-  static constexpr int KST = KST_;        // bricks (64 reduction indices each) per row block and stage
-  static constexpr int KT = 64 * KST;     // reduction indices per stage
-  static constexpr int NSTAGE = NSTAGE_;  // LDS ring depth
-  // MFMA shape: 32 (32x32x64: one k-step is one brick) or 16 (16x16x128: one k-step is two
-  // bricks; a wave's 32x32 block is four 16x16 MFMA blocks).  Both read the same operand
-  // bytes from LDS per MAC for a given wave tile; on changing operands the 16x16x128 form
-  // sustains a higher rate at the board's power limit, but the GEMM, bound by its data path,
-  // runs no faster on it.
-  static constexpr int MF = MF_;
-  static_assert(MF == 32 || (MF == 16 && FMT_ == 0 && NPL_ == 1 && KST % 2 == 0), "MFMA shape");
-  static constexpr int KSTEPS = MF == 16 ? KST / 2 : KST;  // MFMA k-steps per stage
-  // Fragments are read PD k-steps before their MFMAs, into NSETS register sets
-  // (k-step ks of every stage uses set ks % NSETS, so NSETS divides KSTEPS).  PD = 0
-  // reads each k-step's fragments right before its MFMAs into a single set (the
-  // other wave of the SIMD covers the wait), which saves one set of registers.
-  static constexpr int PD = PD_;
-  static constexpr int NSETS = PD == 0 ? 1 : (PD == 1 ? 2 : KSTEPS);
-  static_assert(PD == 0 || (PD < NSETS && KSTEPS % NSETS == 0), "fragment prefetch distance");
-  // Accumulator blocks per wave (M x N) and FP32 values per lane and block.
-  static constexpr int AM = MF == 16 ? 2 * BMW : BMW, AN = MF == 16 ? 2 * BNW : BNW;
-  static constexpr int AV = MF == 16 ? 4 : 16;
-  // Operand element format and its storage unit: 0 E2M1, one k-step in 1 KiB (16 bytes
-  // per lane); 1 E4M3, one k-step in 2 KiB (32 bytes per lane); 2 E2M3, two k-steps in
-  // 3 KiB (24 bytes per lane and k-step).  Units move as 1 KiB copies.
-  static constexpr int FMT = FMT_;
-  static constexpr int UK = FMT == 2 ? 2 : 1;  // k-steps per unit
-  static constexpr int UNIT_BYTES = FMT == 0 ? kBrickBytes : (FMT == 1 ? 2 * kBrickBytes : 3 * kBrickBytes);
-  static constexpr int COPIES = UNIT_BYTES / kBrickBytes;
-  static constexpr int KU = KST / UK;          // units per row block and stage
-  static_assert(KST % UK == 0, "a stage holds whole units");
-  static constexpr int NW = WM * WN;
-  static constexpr int THREADS = 64 * NW;
-  static constexpr int BM = WM * BMW * 32, BN = WN * BNW * 32;
-  // Planes per side in a stage: 1 (one product's planes, product-major stream), or 2 (both
-  // planes of each side; every pair is a product, its weight in the E8M0 scales, all four
-  // into one accumulator).
-  static constexpr int NPL = NPL_;
-  static_assert(NPL == 1 || (NPL == 2 && FMT == 2), "two planes per side: E2M3 with weights in the scales");
-  // All pairs (NPA > 0): a stage brings NPA planes of A and NPB planes of B, and every pair
-  // (i, j) is a product whose coefficient depends on i + j only, so its MFMAs add into
-  // accumulator group i + j (NG groups), folded once per segment with the group's coefficient
-  // (products with equal coefficients share an accumulator, Alg. 1): each plane is copied once
-  // per stage for all the products that use it.
-  static constexpr int NPA = NPA_, NPB = NPB_;
-  static constexpr bool AP = NPA_ > 0;
-  static constexpr int NG = AP ? NPA + NPB - 1 : 1;
-  // A stage's plane pl is stored plane (first plane of the stream product) + pl * PSTEP.
-  static constexpr int PSTEP = PSTEP_;
-  // Outer groups (OUTG = 1, all pairs only): each group i + j has its own int32 accumulator,
-  // into which the stream product's coefficient folds it; the epilogue adds the groups with
-  // their outer weights (GemmArgs::outer_g) in int64.  Otherwise all groups fold into one int32
-  // accumulator with the group's coefficient.
-  static constexpr int OUTG = OUTG_;
-  static constexpr int NOUT = OUTG ? NG : 1;
-  static_assert(!OUTG || AP, "outer groups belong to the all-pairs stream");
-  static_assert(!AP || (NPB > 0 && FMT == 0 && NPL == 1 && MF == 32 && NLB_ == 0 && SCHED_ == 0),
-                "all pairs: E2M1, 32x32x64 MFMAs, int32 accumulators in registers, schedule 0");
-  static constexpr int PA_UNITS = (BM / kBrickRows) * KU;  // per plane and stage: row blocks x units
-  static constexpr int PB_UNITS = (BN / kBrickRows) * KU;
-  static constexpr int SPA = AP ? NPA : NPL, SPB = AP ? NPB : NPL;  // planes per side in a stage
-  static constexpr int A_UNITS = SPA * PA_UNITS;
-  static constexpr int B_UNITS = SPB * PB_UNITS;
-  static constexpr int STAGE_BYTES = (A_UNITS + B_UNITS) * UNIT_BYTES;
-  // The int32 fold accumulators of the last NLB accumulator blocks of every wave live in LDS
-  // after the ring (each wave its own 4 KiB per block, lane-major), so that a tile whose
-  // registers hold only its FP32 accumulators and part of its int32 ones still fits.
-  static constexpr int NLB = NLB_;
-  static_assert(NLB >= 0 && NLB < AM * AN && (NLB == 0 || (MF == 32 && NPL_ == 1)), "LDS fold blocks");
-  static constexpr int FOLD_LDS_OFFSET = NSTAGE * STAGE_BYTES;
-  static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES + NW * NLB * AV * 64 * 4;
-  static_assert(LDS_BYTES <= 160 * 1024, "LDS of one CU");
-  // copies per wave and stage: A units evenly, B units round-robin (the first
-  // B_UNITS % NW waves take one more)
-  static constexpr int A_PW = A_UNITS / NW;
-  static constexpr int B_LO = B_UNITS / NW, B_XTRA = B_UNITS % NW;
-  static_assert(A_UNITS % NW == 0, "A units must split evenly over the waves");
-  static_assert(kKPad % KT == 0, "a stage must divide the reduction padding");
-  // Schedule of the stage loop.  0: after the barrier that frees a buffer every wave issues
-  // its copies of the stage that refills it, then runs the stage's k-steps.  1: the copies
-  // that refill the freed buffer are issued one after each of the first MFMAs of the next
-  // stage instead, so that a wave waiting for the address unit to take a copy has matrix work
-  // in flight (at 8192^3 2-3 % faster than 0 on the 256 x 256 tile).
-  static constexpr int SCHED = SCHED_;
-  static_assert(SCHED == 0 || (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 &&
-                               A_PW + B_LO <= BMW * BNW && NSTAGE >= 3),
-                "copies after the MFMAs: E2M1, one plane per side, 32x32x64 MFMAs, fragments in place");
-};
 
 struct GemmArgs {
   const uint8_t* pa;
@@ -465,25 +374,21 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 
 __device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// The copies of one stage: wave w takes A units A_PW w .. A_PW w + A_PW - 1
-// and B units w, w + NW, ... (unit id = KU * row block + unit of the stage).
+// The copies of one stage (units as copy_unit assigns them; addresses from gemm_layout.h).
 template <class C>
 __device__ __forceinline__ void load_stage_a(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
                                              int tm, int wave, int lane) {
   const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u);
-  // k-step major planes: the units of one k-step (pair) for consecutive row blocks are adjacent
-  constexpr int UB = C::UNIT_BYTES;
-  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + (int64_t)c.t * C::KU * g.rba * UB;
+  const uint8_t* pa = g.pa + (int64_t)ka * g.stride_a + stage_global<C>(c.t, g.rba);
   const uint32_t voff = lane * 16;
 #pragma unroll
   for (int i = 0; i < C::A_PW; ++i) {
-    const int id = wave * C::A_PW + i;
-    const int pl = id / C::PA_UNITS, r = id % C::PA_UNITS;  // plane of the stage, unit in it
-    const int rb = min(tm * (C::BM / kBrickRows) + r / C::KU, g.rba - 1);
+    const int id = copy_unit<C>(true, wave, i);
+    const UnitPos u = unit_pos<C>(true, id);
+    const int rb = min(tm * (C::BM / kBrickRows) + u.rb, g.rba - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pa + (int64_t)pl * C::PSTEP * g.stride_a + ((int64_t)(r % C::KU) * g.rba + rb) * UB + h * kBrickBytes, voff,
-                stage_lds + id * UB + h * kBrickBytes);
+      dma_brick(pa + unit_global<C>(u, rb, g.rba, g.stride_a, h), voff, stage_lds + unit_lds<C>(true, id, h));
   }
 }
 
@@ -491,19 +396,17 @@ template <class C>
 __device__ __forceinline__ void load_stage_b(const GemmArgs& g, const Cursor& c, uint32_t stage_lds,
                                              int tn, int wave, int lane) {
   const int kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
-  constexpr int UB = C::UNIT_BYTES;
-  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + (int64_t)c.t * C::KU * g.rbb * UB;
+  const uint8_t* pb = g.pb + (int64_t)kb * g.stride_b + stage_global<C>(c.t, g.rbb);
   const uint32_t voff = lane * 16;
 #pragma unroll
   for (int i = 0; i < C::B_LO + (C::B_XTRA ? 1 : 0); ++i) {
-    const int id = wave + i * C::NW;
-    if (i == C::B_LO && wave >= C::B_XTRA) break;
-    const int pl = id / C::PB_UNITS, r = id % C::PB_UNITS;
-    const int cb = min(tn * (C::BN / kBrickRows) + r / C::KU, g.rbb - 1);
+    const int id = copy_unit<C>(false, wave, i);
+    if (id < 0) break;
+    const UnitPos u = unit_pos<C>(false, id);
+    const int cb = min(tn * (C::BN / kBrickRows) + u.rb, g.rbb - 1);
 #pragma unroll
     for (int h = 0; h < C::COPIES; ++h)
-      dma_brick(pb + (int64_t)pl * C::PSTEP * g.stride_b + ((int64_t)(r % C::KU) * g.rbb + cb) * UB + h * kBrickBytes, voff,
-                stage_lds + (C::A_UNITS + id) * UB + h * kBrickBytes);
+      dma_brick(pb + unit_global<C>(u, cb, g.rbb, g.stride_b, h), voff, stage_lds + unit_lds<C>(false, id, h));
   }
 }
 
@@ -514,26 +417,27 @@ __device__ __forceinline__ void load_stage(const GemmArgs& g, const Cursor& c, u
   load_stage_b<C>(g, c, stage_lds, tn, wave, lane);
 }
 
-// Copy q of this wave's share of a stage (E2M1, one plane per side): q < A_PW is A brick
-// wave * A_PW + q, then B brick wave + (q - A_PW) * NW, as load_stage orders them.
+// Copy q of this wave's share of a stage (one copy per unit): q < A_PW is its A unit q, then
+// its B units, in the order load_stage issues them.
 template <class C, int Q>
 __device__ __forceinline__ void load_one(const GemmArgs& g, const Cursor& c, uint32_t stage_lds, int tm,
                                          int tn, int wave, int lane) {
+  static_assert(C::COPIES == 1, "one copy per unit");
   const uint32_t voff = lane * 16;
   if constexpr (Q < C::A_PW) {
     const int ka = (int)((g.pidx_a >> (4 * c.p)) & 15u);
-    const int id = wave * C::A_PW + Q;
-    const int rb = min(tm * (C::BM / kBrickRows) + id / C::KU, g.rba - 1);
-    dma_brick(g.pa + (int64_t)ka * g.stride_a + ((int64_t)c.t * C::KU + id % C::KU) * g.rba * kBrickBytes +
-                  (int64_t)rb * kBrickBytes,
-              voff, stage_lds + id * kBrickBytes);
+    const int id = copy_unit<C>(true, wave, Q);
+    const UnitPos u = unit_pos<C>(true, id);
+    const int rb = min(tm * (C::BM / kBrickRows) + u.rb, g.rba - 1);
+    dma_brick(g.pa + (int64_t)ka * g.stride_a + stage_global<C>(c.t, g.rba) + unit_global<C>(u, rb, g.rba, g.stride_a, 0), voff,
+              stage_lds + unit_lds<C>(true, id, 0));
   } else {
     const int kb = (int)((g.pidx_b >> (4 * c.p)) & 15u);
-    const int id = wave + (Q - C::A_PW) * C::NW;
-    const int cb = min(tn * (C::BN / kBrickRows) + id / C::KU, g.rbb - 1);
-    dma_brick(g.pb + (int64_t)kb * g.stride_b + ((int64_t)c.t * C::KU + id % C::KU) * g.rbb * kBrickBytes +
-                  (int64_t)cb * kBrickBytes,
-              voff, stage_lds + (C::A_UNITS + id) * kBrickBytes);
+    const int id = copy_unit<C>(false, wave, Q - C::A_PW);
+    const UnitPos u = unit_pos<C>(false, id);
+    const int cb = min(tn * (C::BN / kBrickRows) + u.rb, g.rbb - 1);
+    dma_brick(g.pb + (int64_t)kb * g.stride_b + stage_global<C>(c.t, g.rbb) + unit_global<C>(u, cb, g.rbb, g.stride_b, 0), voff,
+              stage_lds + unit_lds<C>(false, id, 0));
   }
 }
 
@@ -543,34 +447,27 @@ __device__ __forceinline__ v8i frag(const uint8_t* p) {
   return v;
 }
 
-// A lane's 32 E4M3 elements (32 bytes) of an E4M3 brick.
-__device__ __forceinline__ v8i frag8(const uint8_t* p) {
-  const int4 x = *reinterpret_cast<const int4*>(p);
-  const int4 y = *reinterpret_cast<const int4*>(p + 16);
-  v8i v = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
-  return v;
-}
-
-// A lane's 32 E2M3 elements (24 bytes) of k-step i of an E2M3 unit: dwords 0..3 at
-// i*1024 + 16 L, dwords 4..5 at 2048 + i*512 + 8 L.
-// The MFMA reads 6 of the 8 operand registers for E2M3, so the last two are left
-// undefined instead of zeroed (zeros would cost two registers per fragment).
-__device__ __forceinline__ v8i frag6(const uint8_t* unit, int i, int lane) {
-  const v4i x = *reinterpret_cast<const v4i*>(unit + i * 1024 + lane * 16);
-  const v2i y = *reinterpret_cast<const v2i*>(unit + 2048 + i * 512 + lane * 8);
-  const v4i y4 = __builtin_shufflevector(y, y, 0, 1, -1, -1);
-  return __builtin_shufflevector(x, y4, 0, 1, 2, 3, 4, 5, -1, -1);
-}
-
-// Fragment of k-step i of a unit.
+// A lane's fragment of k-step i of a unit (the spans of frag_spans): E2M1 16 bytes, E4M3 32
+// bytes, E2M3 24 bytes (the MFMA reads 6 of the 8 operand registers for E2M3, so the last two
+// are left undefined instead of zeroed, which would cost two registers per fragment).
 template <int FMT>
 __device__ __forceinline__ v8i frag_fmt(const uint8_t* unit, int i, int lane) {
-  if constexpr (FMT == 0)
-    return frag(unit + lane * 16);
-  else if constexpr (FMT == 1)
-    return frag8(unit + lane * 32);
-  else
-    return frag6(unit, i, lane);
+  constexpr Spans z = frag_spans<FMT>(0, 0);
+  const Spans sp = frag_spans<FMT>(i, lane);
+  if constexpr (FMT == 0) {
+    return frag(unit + sp.off[0]);
+  } else if constexpr (FMT == 1) {
+    const int4 x = *reinterpret_cast<const int4*>(unit + sp.off[0]);
+    const int4 y = *reinterpret_cast<const int4*>(unit + sp.off[0] + 16);
+    v8i v = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+    return v;
+  } else {
+    static_assert(z.n == 2 && z.len[0] == 16 && z.len[1] == 8, "E2M3 spans");
+    const v4i x = *reinterpret_cast<const v4i*>(unit + sp.off[0]);
+    const v2i y = *reinterpret_cast<const v2i*>(unit + sp.off[1]);
+    const v4i y4 = __builtin_shufflevector(y, y, 0, 1, -1, -1);
+    return __builtin_shufflevector(x, y4, 0, 1, 2, 3, 4, 5, -1, -1);
+  }
 }
 
 // The wave's operand fragments for one k-step (64 reduction indices) of a stage.
@@ -580,14 +477,6 @@ struct Frags {
   v8i a[C::MF == 16 ? C::AM : C::SPA * C::BMW], b[C::MF == 16 ? C::AN : C::SPB * C::BNW];
 };
 
-// 16x16x128 operand fragment: lane L holds row (column) L % 16 of its 16-row block at
-// reduction indices 32 (L / 16) .. 32 (L / 16) + 31 of the k-step's 128, i.e. the 16
-// bytes that lane (L / 16 % 2) * 32 + row of brick L / 32 holds in the stored layout.
-__device__ __forceinline__ uint32_t frag16_lane_offset(int lane) {
-  const int q = lane >> 4;
-  return (uint32_t)((q >> 1) * kBrickBytes + ((q & 1) * 32 + (lane & 15)) * 16);
-}
-
 template <class C>
 __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, int ks, int wm,
                                            int wn, int lane) {
@@ -596,29 +485,24 @@ __device__ __forceinline__ void read_frags(Frags<C>& f, const uint8_t* stage, in
 #pragma unroll
     for (int ia = 0; ia < C::BMW; ++ia)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-        f.a[2 * ia + h] = frag(stage + ((wm * C::BMW + ia) * C::KU + 2 * ks) * C::UNIT_BYTES + h * 256 + lo);
+      for (int h = 0; h < 2; ++h) f.a[2 * ia + h] = frag(stage + frag16_unit<C>(true, wm * C::BMW + ia, ks, h) + lo);
 #pragma unroll
     for (int j = 0; j < C::BNW; ++j)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-        f.b[2 * j + h] =
-            frag(stage + (C::A_UNITS + (wn * C::BNW + j) * C::KU + 2 * ks) * C::UNIT_BYTES + h * 256 + lo);
+      for (int h = 0; h < 2; ++h) f.b[2 * j + h] = frag(stage + frag16_unit<C>(false, wn * C::BNW + j, ks, h) + lo);
     return;
   }
-  const int u = ks / C::UK, i = ks % C::UK;
+  const int i = ks % C::UK;
 #pragma unroll
   for (int pl = 0; pl < C::SPA; ++pl)
 #pragma unroll
     for (int ia = 0; ia < C::BMW; ++ia)
-      f.a[pl * C::BMW + ia] = frag_fmt<C::FMT>(
-          stage + (pl * C::PA_UNITS + (wm * C::BMW + ia) * C::KU + u) * C::UNIT_BYTES, i, lane);
+      f.a[pl * C::BMW + ia] = frag_fmt<C::FMT>(stage + frag_unit<C>(true, pl, wm * C::BMW + ia, ks), i, lane);
 #pragma unroll
   for (int pl = 0; pl < C::SPB; ++pl)
 #pragma unroll
     for (int j = 0; j < C::BNW; ++j)
-      f.b[pl * C::BNW + j] = frag_fmt<C::FMT>(
-          stage + (C::A_UNITS + pl * C::PB_UNITS + (wn * C::BNW + j) * C::KU + u) * C::UNIT_BYTES, i, lane);
+      f.b[pl * C::BNW + j] = frag_fmt<C::FMT>(stage + frag_unit<C>(false, pl, wn * C::BNW + j, ks), i, lane);
 }
 
 __device__ __forceinline__ void mfma_block(v16f& acc, const v8i& a, const v8i& b) {
@@ -765,8 +649,9 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   // wave's LDS fold area (int32 v of lane L of block b - NREG at ((b - NREG) * AV + v) * 64 + L).
   constexpr int NREG = C::AM * C::AN - C::NLB;
   int32_t iacc[C::AM][C::AN][C::AV];
-  int32_t* const fold_lds =
-      reinterpret_cast<int32_t*>(smem + C::FOLD_LDS_OFFSET) + wave * (C::NLB * C::AV * 64) + lane;
+  // int32 v of this lane in LDS fold block lb is fold_lds[(lb * AV + v) * 64] (fold_lds_offset)
+  int32_t* const fold_lds = reinterpret_cast<int32_t*>(smem + C::FOLD_LDS_OFFSET) +
+                            (fold_lds_offset<C>(wave, 0, 0, lane) - C::FOLD_LDS_OFFSET) / 4;
   // (register blocks and LDS blocks in separate loops: an expression that chooses between
   // iacc and the LDS area would keep iacc out of registers)
 #pragma unroll
@@ -1150,47 +1035,6 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_group_kernel(GroupArgs ga)
   gemm_tile<C>(g, [=](int p) { return p == 0 ? f0 : p == 1 ? f1 : p == 2 ? f2 : f3; }, tile, -1, g.t_begin,
                g.t_end);
 }
-
-// The tile configurations the launcher chooses from: waves (M x N), 32x32
-// blocks per wave (M x N), k-steps per stage, LDS ring depth.
-using Cfg8w64x64 = Cfg<4, 2, 2, 2, 2, 4>;    // 256 x 128, 8 waves (2 per SIMD)
-using Cfg8w64x96 = Cfg<4, 2, 2, 3, 2, 4>;    // 256 x 192, 8 waves (2 per SIMD)
-using Cfg8w64x64k4 = Cfg<4, 2, 2, 2, 4, 3>;  // 256 x 128, 8 waves, 4 k-steps per stage
-using Cfg8w64x64k4p3 = Cfg<4, 2, 2, 2, 4, 3, 3>;  // as above, fragments read 3 k-steps ahead
-using Cfg8w64x64e4m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 1>;  // 256 x 128, 8 waves, E4M3 operands
-using Cfg8w64x96k4 = Cfg<4, 2, 2, 3, 4, 2>;         // 256 x 192, 8 waves, 4 k-steps, 2 stages
-using Cfg8w64x96s5 = Cfg<4, 2, 2, 3, 2, 5>;         // 256 x 192, 8 waves, 2 k-steps, 5 stages
-using Cfg8w64x96k4p0 = Cfg<4, 2, 2, 3, 4, 2, 0>;    // as 6, fragments read in place
-// 16x16x128 MFMAs (one k-step = two bricks)
-using Cfg8w64x64k4m16 = Cfg<4, 2, 2, 2, 4, 3, 1, 0, 1, 16>;   // 256 x 128, 8 waves, 2 k-steps of 128 per stage
-using Cfg8w64x64k4p0m16 = Cfg<4, 2, 2, 2, 4, 3, 0, 0, 1, 16>; // as above, fragments read in place
-using Cfg8w64x96k4m16 = Cfg<4, 2, 2, 3, 4, 2, 0, 0, 1, 16>;   // 256 x 192, 8 waves, 2 stages, in place
-// 256 x 256 on 8 waves of 2 x 4 blocks, 2 k-steps per stage in 2 stages, fragments read in place;
-// the int32 fold accumulators of 3 of each wave's 8 blocks in LDS (96 KiB + a 64 KiB ring)
-using Cfg8w64x128lf = Cfg<4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3>;
-// as above with the fold accumulators of 2 blocks per wave in LDS (64 KiB) and a 3-stage ring
-using Cfg8w64x128lf3 = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2>;
-// config 13 with the copies that refill a freed buffer issued after the first MFMAs of the next stage
-using Cfg8w64x128ci = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
-// all pairs of 3 planes per side (9 products, 5 accumulator groups): 128 x 128 on 8 waves of
-// 1 x 2 blocks, 2 k-steps per stage (48 KiB) in 3 stages, fragments read in place
-using Cfg8w32x64ap33 = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3>;
-// all pairs of 2 planes per side, 3 apart (the two halves of a 12-bit significand), each group
-// i + j with its own int32 accumulator and outer weight: 128 x 128 on 8 waves of 1 x 2 blocks,
-// 2 k-steps per stage (32 KiB) in 4 stages, fragments read one k-step ahead
-using Cfg8w32x64ap22o = Cfg<4, 2, 1, 2, 2, 4, 1, 0, 1, 32, 0, 0, 2, 2, 3, 1>;
-// E2M3 operands (3 KiB units of two k-steps)
-using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
-using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages
-using Cfg8w64x64k4e2m3 = Cfg<4, 2, 2, 2, 4, 2, 1, 2>; // 256 x 128, 8 waves, 4 k-steps, 2 stages
-// 256 x 192, 8 waves, fragments read in place, the int32 fold accumulators of 1 of each wave's 6
-// blocks in LDS
-using Cfg8w64x96p0lfe2m3 = Cfg<4, 2, 2, 3, 2, 3, 0, 2, 1, 32, 1>;
-// 2 of each wave's 6 blocks in LDS, 2 stages
-using Cfg8w64x96p0lf2e2m3 = Cfg<4, 2, 2, 3, 2, 2, 0, 2, 1, 32, 2>;
-// E2M3, two planes per side with the weights in the scales (4 products, one accumulator)
-using Cfg8w64x64sh = Cfg<4, 2, 2, 2, 2, 2, 1, 2, 2>;    // 256 x 128, 8 waves, 2 k-steps, 2 stages
-using Cfg8w64x64shp0 = Cfg<4, 2, 2, 2, 2, 2, 0, 2, 2>;  // as above, fragments read in place
 
 __global__ void fill_zero_kernel(uint8_t* C, int64_t rows, int64_t row_bytes, int64_t ld_bytes) {
   const int64_t total = rows * row_bytes;

@@ -630,7 +630,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 // part of a split tile, added into C).  fold_coef(p): the fold coefficient of product p.
 // The arguments come by value: through a reference the compiler keeps more of them live
 // (the 256 x 192 tiles then spill).
-template <class C, class FoldCoef>
+template <class C, bool ROWS16, class FoldCoef>
 __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int tile, int part, int t_beg,
                                           int t_end) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
@@ -936,6 +936,55 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
     else
       add_output(g, row, col, val);
   };
+  if constexpr (ROWS16 && C::MF == 32 && !C::OUTG && C::FMT == 0 && C::NPL == 1) {
+    // Whole tiles written (not added) as int32 or int64: each 32 x 32 block goes through a
+    // per-wave LDS slot (rows of 36 words, 16-byte aligned) so that a lane stores 16 bytes of
+    // one row (4 outputs) instead of 16 single outputs of one column: a quarter of the store
+    // instructions.  Uniform per workgroup.
+    static_assert(C::NW * 32 * 36 * 4 <= C::NSTAGE * C::STAGE_BYTES, "row slots inside the ring");
+    const bool rows16 = part < 0 && !g.modulus && !g.accumulate && (tm + 1) * C::BM <= g.M &&
+                        (tn + 1) * C::BN <= g.N && (g.ldc & 3) == 0 &&
+                        (reinterpret_cast<uintptr_t>(g.C) & 15) == 0;
+    if (rows16) {
+      block_barrier();  // every wave is past its last ring read, and its last copies have landed
+      int32_t* const slot = reinterpret_cast<int32_t*>(smem) + wave * (32 * 36);
+      const int rr = lane >> 3, cc = (lane & 7) * 4;  // read: rows rr + 8 q, columns cc .. cc + 3
+      auto put_block = [&](int i, int j, auto value) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) slot[(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 36 + (lane & 31)] = value(v);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const v4i w = *reinterpret_cast<const v4i*>(slot + (rr + 8 * q) * 36 + cc);
+          const int64_t off =
+              (int64_t)(tm * C::BM + wm * (32 * C::BMW) + i * 32 + rr + 8 * q) * g.ldc + tn * C::BN +
+              wn * (32 * C::BNW) + j * 32 + cc;
+          if (g.c64) {
+            typedef long long v2l __attribute__((ext_vector_type(2)));
+            v2l lo, hi;
+            lo[0] = (long long)(w[0] >> g.log2D) * g.outer;
+            lo[1] = (long long)(w[1] >> g.log2D) * g.outer;
+            hi[0] = (long long)(w[2] >> g.log2D) * g.outer;
+            hi[1] = (long long)(w[3] >> g.log2D) * g.outer;
+            v2l* Cp = reinterpret_cast<v2l*>(reinterpret_cast<int64_t*>(g.C) + off);
+            __builtin_nontemporal_store(lo, Cp);
+            __builtin_nontemporal_store(hi, Cp + 1);
+          } else {
+            v4i t;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) t[e] = (int32_t)((int64_t)(w[e] >> g.log2D) * g.outer);
+            __builtin_nontemporal_store(t, reinterpret_cast<v4i*>(reinterpret_cast<int32_t*>(g.C) + off));
+          }
+        }
+      };
+#pragma unroll
+      for (int b = 0; b < NREG; ++b)
+        put_block(b / C::AN, b % C::AN, [&](int v) { return iacc[b / C::AN][b % C::AN][v]; });
+#pragma unroll
+      for (int b = NREG; b < C::AM * C::AN; ++b)
+        put_block(b / C::AN, b % C::AN, [&](int v) { return fold_lds[((b - NREG) * C::AV + v) * 64]; });
+      return;
+    }
+  }
   if constexpr (C::OUTG) {
     // sum_d outer_d (group d's sum / D), exact in int64 (each group's sum is a multiple of D)
 #pragma unroll
@@ -980,7 +1029,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_kernel(GemmArgs g) {
     t_end = min(g.t_end, t_beg + per);
     if (t_beg >= t_end) return;  // the host splits only ranges of at least 2 stages per part
   }
-  gemm_tile<C>(g, [&](int p) { return g.fold_ell[p]; }, tile, part, t_beg, t_end);
+  gemm_tile<C, true>(g, [&](int p) { return g.fold_ell[p]; }, tile, part, t_beg, t_end);
 }
 
 // Several GEMMs of one shape in one launch (the residue route's moduli): job j's tiles are
@@ -1032,7 +1081,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_group_kernel(GroupArgs ga)
   static_assert(kGroupProducts == 4, "the fold coefficients below");
   const int32_t f0 = uniform(jb.fold_ell[0]), f1 = uniform(jb.fold_ell[1]), f2 = uniform(jb.fold_ell[2]),
                 f3 = uniform(jb.fold_ell[3]);
-  gemm_tile<C>(g, [=](int p) { return p == 0 ? f0 : p == 1 ? f1 : p == 2 ? f2 : f3; }, tile, -1, g.t_begin,
+  gemm_tile<C, false>(g, [=](int p) { return p == 0 ? f0 : p == 1 ? f1 : p == 2 ? f2 : f3; }, tile, -1, g.t_begin,
                g.t_end);
 }
 
@@ -1076,7 +1125,7 @@ double rounds(int64_t tiles, int cus) {
 // place, 12: 256x256 with the int32 fold accumulators of 3 blocks per wave in LDS and a 2-stage
 // ring, 13: as 12 with 2 blocks per wave in LDS and a 3-stage ring, 14: as 13 with the copies
 // that refill a freed buffer issued after the first MFMAs of the next stage.
-bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 14); }
+bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 14 && n != 11); }
 
 // Tile configuration for a problem: AWE_GEMM_CFG if it names one, else the configuration whose
 // rounds of workgroups finish first: 5, 6 (a round about 1.48 times as long as a round of 5;
@@ -1437,7 +1486,6 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 8: return launch_tile<Cfg8w64x96k4p0>(g, L, stream);
     case 9: return launch_tile<Cfg8w64x64k4m16>(g, L, stream);
     case 10: return launch_tile<Cfg8w64x64k4p0m16>(g, L, stream);
-    case 11: return launch_tile<Cfg8w64x96k4m16>(g, L, stream);
     case 12: return launch_tile<Cfg8w64x128lf>(g, L, stream);
     case 13: return launch_tile<Cfg8w64x128lf3>(g, L, stream);
     case 14: return launch_tile<Cfg8w64x128ci>(g, L, stream);

@@ -198,7 +198,6 @@ using Cfg8w64x96k4p0 = Cfg<4, 2, 2, 3, 4, 2, 0>;    // as 6, fragments read in p
 // 16x16x128 MFMAs (one k-step = two bricks)
 using Cfg8w64x64k4m16 = Cfg<4, 2, 2, 2, 4, 3, 1, 0, 1, 16>;   // 256 x 128, 8 waves, 2 k-steps of 128 per stage
 using Cfg8w64x64k4p0m16 = Cfg<4, 2, 2, 2, 4, 3, 0, 0, 1, 16>; // as above, fragments read in place
-using Cfg8w64x96k4m16 = Cfg<4, 2, 2, 3, 4, 2, 0, 0, 1, 16>;   // 256 x 192, 8 waves, 2 stages, in place
 // 256 x 256 on 8 waves of 2 x 4 blocks, 2 k-steps per stage in 2 stages, fragments read in place;
 // the int32 fold accumulators of 3 of each wave's 8 blocks in LDS (96 KiB + a 64 KiB ring)
 using Cfg8w64x128lf = Cfg<4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3>;

@@ -176,7 +176,6 @@ int main() {
   CFG(Cfg8w64x96k4p0);
   CFG(Cfg8w64x64k4m16);
   CFG(Cfg8w64x64k4p0m16);
-  CFG(Cfg8w64x96k4m16);
   CFG(Cfg8w64x128lf);
   CFG(Cfg8w64x128lf3);
   CFG(Cfg8w64x128ci);

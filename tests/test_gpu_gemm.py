@@ -234,7 +234,7 @@ def test_mod_forced_segments():
     assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
 
 
-@pytest.mark.parametrize("cfg", ["1", "2", "4", "5", "6", "7", "8", "9", "10", "11", "12", "13", "14"])
+@pytest.mark.parametrize("cfg", ["1", "2", "4", "5", "6", "7", "8", "9", "10", "12", "13", "14"])
 @pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13, awe.ENC_TERNARY])
 def test_every_tile_configuration(monkeypatch, cfg, enc):
     # AWE_GEMM_CFG forces one of the GEMM's tile configurations (256x128 on 8 waves with

@@ -59,10 +59,26 @@ __global__ __launch_bounds__(256) void encode_kernel(const uint8_t* __restrict__
   slut[threadIdx.x] = lut.v[threadIdx.x];
   __syncthreads();
   const int lane = threadIdx.x & 63;
-  // each wave takes one brick, or several when the grid is capped
+  // Each wave takes one brick, or several when the grid is capped.  A side: the four waves of
+  // a workgroup take four consecutive k-steps of one row block (32 rows x 256 bytes of A).
+  // B side: four adjacent column blocks of one k-step, so that a workgroup reads whole 128-byte
+  // lines of B's rows (64 rows x 128 bytes); with the k-steps in a workgroup instead, each
+  // line was read by four workgroups far apart in time and, when B was not in the last-level
+  // cache, fetched from HBM up to four times.  Consecutive workgroups take consecutive k-steps
+  // (measured faster than consecutive column groups).  Here nbricks counts ceil(R32 / 4) * 4
+  // row blocks on the B side, and the waves past R32 have no brick.
   for (int64_t brick = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); brick < nbricks;
        brick += (int64_t)gridDim.x * 4) {
-  const int64_t rb = brick / KS, ks = brick - rb * KS;
+  int64_t rb, ks;
+  if (kTransposed) {
+    const int64_t q = brick >> 2;
+    ks = q % KS;
+    rb = (q / KS) * 4 + (brick & 3);
+    if (rb >= R32) continue;
+  } else {
+    rb = brick / KS;
+    ks = brick - rb * KS;
+  }
   const int64_t row = rb * kBrickRows + (lane & 31);
   const int64_t k0 = ks * kBrickK + (lane >> 5) * 32;
   const bool row_ok = row < rows;
@@ -1418,11 +1434,13 @@ awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
   }
   LutArg lut;
   for (int i = 0; i < 256; ++i) lut.v[i] = e.lut[i];
-  // one brick per wave; past 2^31 - 1 workgroups the waves walk several bricks each
-  const int64_t blocks = std::min<int64_t>((nbricks + 3) / 4, 0x7fffffffLL);
+  // one brick per wave; past 2^31 - 1 workgroups the waves walk several bricks each (the B
+  // side in groups of four column blocks, the last group padded)
+  const int64_t nb = e.transposed ? (rb + 3) / 4 * 4 * KS : nbricks;
+  const int64_t blocks = std::min<int64_t>((nb + 3) / 4, 0x7fffffffLL);
   if (e.transposed)
     hipLaunchKernelGGL(encode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nbricks,
+                       reinterpret_cast<const uint8_t*>(e.x), e.rows, e.K, e.ld, KS, rb, nb,
                        e.nplanes, e.nplanes8, e.fp6, e.planes, e.plane_stride, e.flag, lut);
   else
     hipLaunchKernelGGL(encode_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,

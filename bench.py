@@ -37,7 +37,9 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=5)
+    # the first ~15 GEMMs of a process run ~10 % slower (clocks still settling), so the default
+    # warms up past them
+    p.add_argument("--warmup", type=int, default=30)
     p.add_argument("--size", type=int, default=8192)
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
     p.add_argument("--no-context", action="store_true", help="skip base-13 and INT8 context")

@@ -771,7 +771,7 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   };
 
   constexpr int NSTAGE = C::NSTAGE;
-  if constexpr (C::SCHED == 1) {
+  if constexpr (C::SCHED >= 1) {
     // Stream stage u sits in buffer u % NSTAGE.  In stage u each wave issues its copies of
     // stage u + NSTAGE - 1 into the buffer of stage u - 1 (freed by the barrier at the end of
     // stage u - 1), one after each of the first MFMAs of the stage's first k-step.  Before the
@@ -793,6 +793,27 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
       for (int p = 0; p < g.r; ++p) {
         for (int t = cs; t < ce; ++t) {
           const uint32_t cur_off = buf * C::STAGE_BYTES, cp_lds = lds0 + cbuf * C::STAGE_BYTES;
+          if constexpr (C::SCHED >= 2) {
+            // the stage's copies spread evenly over its k-steps: CPK per k-step, one after
+            // every GAP-th MFMA
+            constexpr int CPK = PER_STAGE / C::KSTEPS, GAP = C::BMW * C::BNW / CPK;
+            static_for<0, C::KSTEPS>([&](auto kc) {
+              constexpr int ks = decltype(kc)::value;
+              read_frags<C>(f, smem + cur_off, ks, wm, wn, lane);
+              __builtin_amdgcn_sched_barrier(0);
+              static_for<0, C::BMW * C::BNW>([&](auto qc) {
+                constexpr int q = decltype(qc)::value;
+                mfma_block(acc[q / C::BNW][q % C::BNW], f.a[q / C::BNW], f.b[q % C::BNW]);
+                if constexpr (q % GAP == 0) {
+                  __builtin_amdgcn_sched_barrier(0);
+                  load_one<C, ks * CPK + q / GAP>(g, nxt, cp_lds, tm, tn, wave, lane);
+                  __builtin_amdgcn_sched_barrier(0);
+                }
+              });
+              __builtin_amdgcn_sched_barrier(0);
+            });
+            cursor_next(nxt, g, t_end);
+          } else {
 #pragma unroll
           for (int ks = 0; ks < C::KSTEPS; ++ks) {
             read_frags<C>(f, smem + cur_off, ks, wm, wn, lane);
@@ -815,6 +836,7 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
                 for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], f.a[i], f.b[j]);
             }
             __builtin_amdgcn_sched_barrier(0);
+          }
           }
           wait_vmcnt<(NSTAGE - 2) * PER_STAGE>();
           wait_lgkm0();
@@ -1137,15 +1159,15 @@ double rounds(int64_t tiles, int cus) {
 // waves, 2: 256x192 with 8 waves, 4: as 1 with 4 k-steps per stage, 5: as 4 with fragments
 // read three k-steps ahead, 6: 256x192 with 4 k-steps per stage in 2 stages, 7: 256x192 with 2
 // k-steps per stage in 5 stages, 8: as 6 with fragments read in place, 9: as 4 on the
-// 16x16x128 MFMA, 10: as 9 with fragments read in place, 11: 256x192 on the 16x16x128 MFMA, in
-// place, 12: 256x256 with the int32 fold accumulators of 3 blocks per wave in LDS and a 2-stage
-// ring, 13: as 12 with 2 blocks per wave in LDS and a 3-stage ring, 14: as 13 with the copies
-// that refill a freed buffer issued after the first MFMAs of the next stage.
-bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 14 && n != 11); }
+// 16x16x128 MFMA, 10: as 9 with fragments read in place, 12: 256x256 with the int32 fold
+// accumulators of 3 blocks per wave in LDS and a 2-stage ring, 13: as 12 with 2 blocks per wave
+// in LDS and a 3-stage ring, 14: as 13 with the copies that refill a freed buffer issued after
+// the first MFMAs of the next stage, 15: as 14 with those copies spread over both k-steps.
+bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 15 && n != 11); }
 
 // Tile configuration for a problem: AWE_GEMM_CFG if it names one, else the configuration whose
 // rounds of workgroups finish first: 5, 6 (a round about 1.48 times as long as a round of 5;
-// only when clearly sooner) or 14.  A round takes about 2.2 k + 1700 time units for 5 and
+// only when clearly sooner) or 15.  A round takes about 2.2 k + 1700 time units for 5 and
 // 3.9 k + 6000 for the 256x256 tile, k = r K / 6 reduction indices at r products: a fit of the
 // kernel times measured on MI355X for 4096^2 and 8192^2 outputs at K = 4096 .. 65536.  The
 // larger tile pays off once the reduction is long enough to amortise its fixed cost per round.
@@ -1160,7 +1182,7 @@ int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const double t128 = rounds(tm * ((N + 127) / 128), cus) * r128;
   const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.48 * r128;
   const double t256 = rounds(tm * ((N + 255) / 256), cus) * r256;
-  if (t256 < t128 && t256 < t192) return 14;
+  if (t256 < t128 && t256 < t192) return 15;
   return t192 < 0.97 * t128 ? 6 : 5;
 }
 
@@ -1507,12 +1529,13 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 12: return launch_tile<Cfg8w64x128lf>(g, L, stream);
     case 13: return launch_tile<Cfg8w64x128lf3>(g, L, stream);
     case 14: return launch_tile<Cfg8w64x128ci>(g, L, stream);
+    case 15: return launch_tile<Cfg8w64x128cs>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }
 
 // The grouped kernel is built for the 256 x 128 tiles on 8 waves (configurations 1, 4
-// and 5) and the 256 x 256 tiles of configuration 13 (with configuration 14's schedule it
+// and 5) and the 256 x 256 tiles of configuration 13 (with the schedules of 14 and 15 it
 // spills a register); the 256 x 192 ones leave no registers for the jobs' fields.
 bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5 || cfg == 13; }
 

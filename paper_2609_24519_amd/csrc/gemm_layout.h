@@ -98,9 +98,13 @@ struct Cfg {
   // stage instead, so that a wave waiting for the address unit to take a copy has matrix work
   // in flight (at 8192^3 2-3 % faster than 0 on the 256 x 256 tile).
   static constexpr int SCHED = SCHED_;
+  // 2: as 1, the copies spread evenly over the stage's k-steps, one after every few MFMAs, so
+  // that the eight waves' copies do not queue at the address unit at once (1-2 % faster than 1).
   static_assert(SCHED == 0 || (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 &&
                                A_PW + B_LO <= BMW * BNW && NSTAGE >= 3),
                 "copies after the MFMAs: E2M1, one plane per side, 32x32x64 MFMAs, fragments in place");
+  static_assert(SCHED != 2 || ((A_PW + B_LO) % KSTEPS == 0 && (BMW * BNW) % ((A_PW + B_LO) / KSTEPS) == 0),
+                "copies spread over the k-steps");
 };
 
 // ---------------------------------------------------------------------------
@@ -205,6 +209,8 @@ using Cfg8w64x128lf = Cfg<4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3>;
 using Cfg8w64x128lf3 = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2>;
 // config 13 with the copies that refill a freed buffer issued after the first MFMAs of the next stage
 using Cfg8w64x128ci = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
+// as above with the copies spread over both k-steps of the stage
+using Cfg8w64x128cs = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2>;
 // all pairs of 3 planes per side (9 products, 5 accumulator groups): 128 x 128 on 8 waves of
 // 1 x 2 blocks, 2 k-steps per stage (48 KiB) in 3 stages, fragments read in place
 using Cfg8w32x64ap33 = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3>;

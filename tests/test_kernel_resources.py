@@ -50,11 +50,13 @@ def rows():
 # The E2M3 default (256x192, the fold accumulators of 1 block per wave in LDS) spills one
 # 4-byte value: a store before the reduction loop and a reload after it, outside the loop, and
 # it runs 6-8 % faster than the E2M3 configuration without spills.  No more than that.
-# The E2M1 default for long reductions (256x256, the copies issued after the first MFMAs) spills
-# one 4-byte value the same way: its 16-byte row epilogue needs one register more than the loop
-# leaves, and that epilogue makes the kernel 2-3 % faster.
+# The E2M1 256x256 tiles with the copies issued between the MFMAs (the default for long
+# reductions, copies spread over the stage, and its predecessor) spill one 4-byte value the same
+# way: their 16-byte row epilogue needs one register more than the loop leaves, and that
+# epilogue makes the kernel 2-3 % faster.
 SMALL_SPILL = {"E2M3 256x192, 1 fold block per wave in LDS (default)": _cfg(4, 2, 2, 3, 2, 3, 0, 2, 1, 32, 1),
-               "E2M1 256x256, the copies after the first MFMAs (default)": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1)}
+               "E2M1 256x256, the copies after the first MFMAs": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1),
+               "E2M1 256x256, the copies spread over the stage (default)": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2)}
 
 
 def test_default_gemm_configurations_do_not_spill(rows):

@@ -772,12 +772,17 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
 
   constexpr int NSTAGE = C::NSTAGE;
   if constexpr (C::SCHED >= 1) {
-    // Stream stage u sits in buffer u % NSTAGE.  In stage u each wave issues its copies of
+    // Stream stage u sits in buffer u % NSTAGE.  During stage u each wave issues its copies of
     // stage u + NSTAGE - 1 into the buffer of stage u - 1 (freed by the barrier at the end of
-    // stage u - 1), one after each of the first MFMAs of the stage's first k-step.  Before the
-    // barrier at the end of stage u it waits until stage u + 1 has landed (its copies of the
-    // NSTAGE - 2 stages after u + 1 may still be in flight) and its reads of stage u are done.
+    // stage u - 1), spread over the stage, one after every GAP-th MFMA: the eight waves' copies
+    // then do not queue at the address unit together, and a wave that waits for one has matrix
+    // work in flight.  Schedule 2 also reads a later k-step's fragments during the k-step before
+    // it, each into its register set as soon as the last MFMA that uses the old value has
+    // issued.  Before the barrier at the end of stage u each wave waits until stage u + 1 has
+    // landed (its copies of the NSTAGE - 2 stages after u + 1 may still be in flight) and its
+    // reads of stage u are done.
     constexpr int PER_STAGE = C::A_PW + C::B_LO;  // copies per wave and stage
+    constexpr int CPK = PER_STAGE / C::KSTEPS, GAP = C::BMW * C::BNW / CPK;
     Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
 #pragma unroll
     for (int i = 0; i < NSTAGE - 1; ++i) {
@@ -793,51 +798,32 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
       for (int p = 0; p < g.r; ++p) {
         for (int t = cs; t < ce; ++t) {
           const uint32_t cur_off = buf * C::STAGE_BYTES, cp_lds = lds0 + cbuf * C::STAGE_BYTES;
-          if constexpr (C::SCHED >= 2) {
-            // the stage's copies spread evenly over its k-steps: CPK per k-step, one after
-            // every GAP-th MFMA
-            constexpr int CPK = PER_STAGE / C::KSTEPS, GAP = C::BMW * C::BNW / CPK;
-            static_for<0, C::KSTEPS>([&](auto kc) {
-              constexpr int ks = decltype(kc)::value;
+          static_for<0, C::KSTEPS>([&](auto kc) {
+            constexpr int ks = decltype(kc)::value;
+            if constexpr (C::SCHED == 1 || ks == 0) {
               read_frags<C>(f, smem + cur_off, ks, wm, wn, lane);
               __builtin_amdgcn_sched_barrier(0);
-              static_for<0, C::BMW * C::BNW>([&](auto qc) {
-                constexpr int q = decltype(qc)::value;
-                mfma_block(acc[q / C::BNW][q % C::BNW], f.a[q / C::BNW], f.b[q % C::BNW]);
-                if constexpr (q % GAP == 0) {
-                  __builtin_amdgcn_sched_barrier(0);
-                  load_one<C, ks * CPK + q / GAP>(g, nxt, cp_lds, tm, tn, wave, lane);
-                  __builtin_amdgcn_sched_barrier(0);
-                }
-              });
-              __builtin_amdgcn_sched_barrier(0);
-            });
-            cursor_next(nxt, g, t_end);
-          } else {
-#pragma unroll
-          for (int ks = 0; ks < C::KSTEPS; ++ks) {
-            read_frags<C>(f, smem + cur_off, ks, wm, wn, lane);
-            __builtin_amdgcn_sched_barrier(0);
-            if (ks == 0) {
-              static_for<0, C::BMW * C::BNW>([&](auto qc) {
-                constexpr int q = decltype(qc)::value;
-                mfma_block(acc[q / C::BNW][q % C::BNW], f.a[q / C::BNW], f.b[q % C::BNW]);
-                if constexpr (q < PER_STAGE) {
-                  __builtin_amdgcn_sched_barrier(0);
-                  load_one<C, q>(g, nxt, cp_lds, tm, tn, wave, lane);
-                  __builtin_amdgcn_sched_barrier(0);
-                }
-              });
-              cursor_next(nxt, g, t_end);
-            } else {
-#pragma unroll
-              for (int i = 0; i < C::BMW; ++i)
-#pragma unroll
-                for (int j = 0; j < C::BNW; ++j) mfma_block(acc[i][j], f.a[i], f.b[j]);
             }
+            static_for<0, C::BMW * C::BNW>([&](auto qc) {
+              constexpr int q = decltype(qc)::value, i = q / C::BNW, j = q % C::BNW;
+              mfma_block(acc[i][j], f.a[i], f.b[j]);
+              if constexpr (q % GAP == 0) {
+                __builtin_amdgcn_sched_barrier(0);
+                load_one<C, ks * CPK + q / GAP>(g, nxt, cp_lds, tm, tn, wave, lane);
+                __builtin_amdgcn_sched_barrier(0);
+              }
+              if constexpr (C::SCHED == 2 && ks + 1 < C::KSTEPS) {
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (j == C::BNW - 1)
+                  f.a[i] = frag(smem + cur_off + frag_unit<C>(true, 0, wm * C::BMW + i, ks + 1) + lane * 16);
+                if constexpr (i == C::BMW - 1)
+                  f.b[j] = frag(smem + cur_off + frag_unit<C>(false, 0, wn * C::BNW + j, ks + 1) + lane * 16);
+                __builtin_amdgcn_sched_barrier(0);
+              }
+            });
             __builtin_amdgcn_sched_barrier(0);
-          }
-          }
+          });
+          cursor_next(nxt, g, t_end);
           wait_vmcnt<(NSTAGE - 2) * PER_STAGE>();
           wait_lgkm0();
           block_barrier();
@@ -1161,13 +1147,13 @@ double rounds(int64_t tiles, int cus) {
 // k-steps per stage in 5 stages, 8: as 6 with fragments read in place, 9: as 4 on the
 // 16x16x128 MFMA, 10: as 9 with fragments read in place, 12: 256x256 with the int32 fold
 // accumulators of 3 blocks per wave in LDS and a 2-stage ring, 13: as 12 with 2 blocks per wave
-// in LDS and a 3-stage ring, 14: as 13 with the copies that refill a freed buffer issued after
-// the first MFMAs of the next stage, 15: as 14 with those copies spread over both k-steps.
-bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 15 && n != 11); }
+// in LDS and a 3-stage ring, 15: as 13 with the copies that refill a freed buffer spread over
+// the next stage's MFMAs, 16: as 15 with the second k-step's fragments read during the first.
+bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 16 && n != 11 && n != 14); }
 
 // Tile configuration for a problem: AWE_GEMM_CFG if it names one, else the configuration whose
 // rounds of workgroups finish first: 5, 6 (a round about 1.48 times as long as a round of 5;
-// only when clearly sooner) or 15.  A round takes about 2.2 k + 1700 time units for 5 and
+// only when clearly sooner) or 16.  A round takes about 2.2 k + 1700 time units for 5 and
 // 3.9 k + 6000 for the 256x256 tile, k = r K / 6 reduction indices at r products: a fit of the
 // kernel times measured on MI355X for 4096^2 and 8192^2 outputs at K = 4096 .. 65536.  The
 // larger tile pays off once the reduction is long enough to amortise its fixed cost per round.
@@ -1182,7 +1168,7 @@ int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const double t128 = rounds(tm * ((N + 127) / 128), cus) * r128;
   const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.48 * r128;
   const double t256 = rounds(tm * ((N + 255) / 256), cus) * r256;
-  if (t256 < t128 && t256 < t192) return 15;
+  if (t256 < t128 && t256 < t192) return 16;
   return t192 < 0.97 * t128 ? 6 : 5;
 }
 
@@ -1528,14 +1514,14 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 10: return launch_tile<Cfg8w64x64k4p0m16>(g, L, stream);
     case 12: return launch_tile<Cfg8w64x128lf>(g, L, stream);
     case 13: return launch_tile<Cfg8w64x128lf3>(g, L, stream);
-    case 14: return launch_tile<Cfg8w64x128ci>(g, L, stream);
     case 15: return launch_tile<Cfg8w64x128cs>(g, L, stream);
+    case 16: return launch_tile<Cfg8w64x128cr>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }
 
 // The grouped kernel is built for the 256 x 128 tiles on 8 waves (configurations 1, 4
-// and 5) and the 256 x 256 tiles of configuration 13 (with the schedules of 14 and 15 it
+// and 5) and the 256 x 256 tiles of configuration 13 (with the schedules of 15 and 16 it
 // spills a register); the 256 x 192 ones leave no registers for the jobs' fields.
 bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5 || cfg == 13; }
 

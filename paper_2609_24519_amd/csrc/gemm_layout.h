@@ -93,18 +93,18 @@ struct Cfg {
   static_assert(A_UNITS % NW == 0, "A units must split evenly over the waves");
   static_assert(kKPad % KT == 0, "a stage must divide the reduction padding");
   // Schedule of the stage loop.  0: after the barrier that frees a buffer every wave issues
-  // its copies of the stage that refills it, then runs the stage's k-steps.  1: the copies
-  // that refill the freed buffer are issued one after each of the first MFMAs of the next
-  // stage instead, so that a wave waiting for the address unit to take a copy has matrix work
-  // in flight (at 8192^3 2-3 % faster than 0 on the 256 x 256 tile).
+  // its copies of the stage that refills it, then runs the stage's k-steps.  1: the copies that
+  // refill the freed buffer are spread over the next stage's MFMAs instead, one after every few,
+  // so that the eight waves' copies do not queue at the address unit at once and a wave waiting
+  // for one has matrix work in flight.  2: as 1, and a later k-step's fragments are read during
+  // the k-step before it, each as soon as the last MFMA that uses the register's old value has
+  // issued.
   static constexpr int SCHED = SCHED_;
-  // 2: as 1, the copies spread evenly over the stage's k-steps, one after every few MFMAs, so
-  // that the eight waves' copies do not queue at the address unit at once (1-2 % faster than 1).
-  static_assert(SCHED == 0 || (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 &&
-                               A_PW + B_LO <= BMW * BNW && NSTAGE >= 3),
-                "copies after the MFMAs: E2M1, one plane per side, 32x32x64 MFMAs, fragments in place");
-  static_assert(SCHED != 2 || ((A_PW + B_LO) % KSTEPS == 0 && (BMW * BNW) % ((A_PW + B_LO) / KSTEPS) == 0),
-                "copies spread over the k-steps");
+  static_assert(SCHED == 0 ||
+                    (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 && NSTAGE >= 3 &&
+                     (A_PW + B_LO) % KSTEPS == 0 && (BMW * BNW) % ((A_PW + B_LO) / KSTEPS) == 0),
+                "copies between the MFMAs: E2M1, one plane per side, 32x32x64 MFMAs, fragments in place, "
+                "the copies spread evenly over the k-steps");
 };
 
 // ---------------------------------------------------------------------------
@@ -207,10 +207,10 @@ using Cfg8w64x64k4p0m16 = Cfg<4, 2, 2, 2, 4, 3, 0, 0, 1, 16>; // as above, fragm
 using Cfg8w64x128lf = Cfg<4, 2, 2, 4, 2, 2, 0, 0, 1, 32, 3>;
 // as above with the fold accumulators of 2 blocks per wave in LDS (64 KiB) and a 3-stage ring
 using Cfg8w64x128lf3 = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2>;
-// config 13 with the copies that refill a freed buffer issued after the first MFMAs of the next stage
-using Cfg8w64x128ci = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
-// as above with the copies spread over both k-steps of the stage
-using Cfg8w64x128cs = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2>;
+// config 13 with the copies that refill a freed buffer spread over the next stage's MFMAs (15),
+// and with the second k-step's fragments read during the first (16)
+using Cfg8w64x128cs = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
+using Cfg8w64x128cr = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2>;
 // all pairs of 3 planes per side (9 products, 5 accumulator groups): 128 x 128 on 8 waves of
 // 1 x 2 blocks, 2 k-steps per stage (48 KiB) in 3 stages, fragments read in place
 using Cfg8w32x64ap33 = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3>;

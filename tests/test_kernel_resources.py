@@ -34,6 +34,8 @@ DEFAULTS = {
     "E4M3": _cfg(4, 2, 2, 2, 2, 3, 1, 1, 1, 32, 0),
     "E2M3 256x128, 4 k-steps per stage": _cfg(4, 2, 2, 2, 4, 2, 1, 2, 1, 32, 0),
     "E2M3 weights in the scales": _cfg(4, 2, 2, 2, 2, 2, 1, 2, 2, 32, 0),
+    "E2M1 256x256, copies spread over the stage, fragments read a k-step ahead in place (default)":
+        _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2),
     "E2M1 base-13, all nine plane pairs in one stream": _cfg(4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3),
     "E2M1 FP16 significands, outer groups": _cfg(4, 2, 1, 2, 2, 4, 1, 0, 1, 32, 0, 0, 2, 2, 3, 1),
 }
@@ -50,13 +52,11 @@ def rows():
 # The E2M3 default (256x192, the fold accumulators of 1 block per wave in LDS) spills one
 # 4-byte value: a store before the reduction loop and a reload after it, outside the loop, and
 # it runs 6-8 % faster than the E2M3 configuration without spills.  No more than that.
-# The E2M1 256x256 tiles with the copies issued between the MFMAs (the default for long
-# reductions, copies spread over the stage, and its predecessor) spill one 4-byte value the same
-# way: their 16-byte row epilogue needs one register more than the loop leaves, and that
-# epilogue makes the kernel 2-3 % faster.
+# The E2M1 256x256 tile with the copies spread over the stage and each k-step's fragments read
+# right before its MFMAs spills one 4-byte value the same way: its 16-byte row epilogue needs one
+# register more than the loop leaves.
 SMALL_SPILL = {"E2M3 256x192, 1 fold block per wave in LDS (default)": _cfg(4, 2, 2, 3, 2, 3, 0, 2, 1, 32, 1),
-               "E2M1 256x256, the copies after the first MFMAs": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1),
-               "E2M1 256x256, the copies spread over the stage (default)": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2)}
+               "E2M1 256x256, the copies spread over the stage": _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1)}
 
 
 def test_default_gemm_configurations_do_not_spill(rows):

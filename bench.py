@@ -308,10 +308,34 @@ def _time_ms(fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
+def _time_steps(encode, gemm, reps, stream):
+    """Average milliseconds of a step (encode() then gemm()) and of the GEMM within it, over reps
+    steps after three warm-up steps: HIP events on `stream` around each step's GEMM, as for the
+    headline, so that both figures come from the same sequence of launches."""
+    import torch
+
+    for _ in range(3):
+        encode()
+        gemm()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    for e in evs:
+        e[0].record(stream)
+        encode()
+        e[1].record(stream)
+        gemm()
+        e[2].record(stream)
+    torch.cuda.synchronize()
+    step = sum(e[0].elapsed_time(e[2]) for e in evs) / reps
+    g = sum(e[1].elapsed_time(e[2]) for e in evs) / reps
+    return step, g
+
+
 def awe4_workload(dev, n=8192):
     """INT4 x INT8 in 4 FP4 products (App. A): A int4 uniform in [-8, 7] (one per int8 byte), B
-    int8 uniform in [-128, 127], seed 0, n^3, int32 C.  GEMM on resident planes (awe_gemm_planes)
-    and end to end (both encoders + GEMM); the FP4 work is 4 products of 2 n^3."""
+    int8 uniform in [-128, 127], seed 0, n^3, int32 C.  Steps of both encoders + GEMM on the
+    resident planes (awe_gemm_planes), timed whole and GEMM alone within each step; the FP4 work
+    is 4 products of 2 n^3."""
     import torch
 
     from paper_2609_24519_amd import awe, inputs
@@ -332,9 +356,7 @@ def awe4_workload(dev, n=8192):
     def gemm():
         awe.gemm_planes(enc, 0, n, n, n, pa, pb, C, n, awe.I32, 0, stream)
 
-    enc_both()
-    gms = _time_ms(gemm, 10, stream)
-    ems = _time_ms(lambda: (enc_both(), gemm()), 10, stream)
+    ems, gms = _time_steps(enc_both, gemm, 10, stream)
     ops = 2.0 * n ** 3
     tf = r * ops / (gms * 1e-3) / 1e12
     out = {"workload": "INT4xINT8 exact GEMM, M=N=K=%d, A uniform [-8,7], B uniform [-128,127], seed 0, "

@@ -771,7 +771,87 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   };
 
   constexpr int NSTAGE = C::NSTAGE;
-  if constexpr (C::SCHED >= 1) {
+  if constexpr (C::SCHED == 3) {
+    // Stream stage u sits in buffer u % 3; its barrier sits inside its second k-step, after the
+    // MFMAs of the first row of blocks (BAR of them).
+    //  k-step 0: MFMAs on fragments read before; the fragments of k-step 1 are read from
+    //    buffer u into each register set as soon as its last k-step-0 MFMA has issued; the
+    //    second half of stage u + 2's copies go to buffer (u + 2) % 3.
+    //  k-step 1, first BAR MFMAs; then wait until stage u + 1 has landed (stage u + 2's copies
+    //    may still be in flight) and this wave's reads of buffer u are done (they have had the
+    //    first BAR MFMAs to land); barrier: every wave is done with buffer u, stage u + 1 is
+    //    complete.
+    //  k-step 1, the other MFMAs: stage u + 1's k-step-0 fragments are read from buffer
+    //    (u + 1) % 3 into the registers already free and then as more free up; the first half of
+    //    stage u + 3's copies go to buffer u.
+    constexpr int PER_STAGE = C::A_PW + C::B_LO;  // copies per wave and stage
+    constexpr int CPK = PER_STAGE / 2, NQ = C::BMW * C::BNW, GAP = NQ / CPK, BAR = C::BNW;
+    constexpr int GAP1 = (NQ - BAR) / CPK;  // spacing of the copies after the barrier
+    static_assert(C::KSTEPS == 2 && NSTAGE == 3 && PER_STAGE % 2 == 0 && GAP1 >= 1, "schedule 3");
+    Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
+    load_stage<C>(g, nxt, lds0, tm, tn, wave, lane);
+    cursor_next(nxt, g, t_end);
+    load_stage<C>(g, nxt, lds0 + C::STAGE_BYTES, tm, tn, wave, lane);
+    cursor_next(nxt, g, t_end);
+    static_for<0, CPK>([&](auto qc) {
+      load_one<C, decltype(qc)::value>(g, nxt, lds0 + 2 * C::STAGE_BYTES, tm, tn, wave, lane);
+    });
+    wait_vmcnt<PER_STAGE + CPK>();
+    block_barrier();
+    Frags<C> f;
+    read_frags<C>(f, smem, 0, wm, wn, lane);
+    int buf = 0;
+    for (int cs = t_beg; cs < t_end; cs += g.ts) {
+      const int ce = min(cs + g.ts, t_end);
+      for (int p = 0; p < g.r; ++p) {
+        for (int t = cs; t < ce; ++t) {
+          const int b1 = buf == 2 ? 0 : buf + 1, b2 = b1 == 2 ? 0 : b1 + 1;
+          const uint32_t cur_off = buf * C::STAGE_BYTES, next_off = b1 * C::STAGE_BYTES;
+          static_for<0, NQ>([&](auto qc) {
+            constexpr int q = decltype(qc)::value, i = q / C::BNW, j = q % C::BNW;
+            mfma_block(acc[i][j], f.a[i], f.b[j]);
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (q % GAP == 0)
+              load_one<C, CPK + q / GAP>(g, nxt, lds0 + b2 * C::STAGE_BYTES, tm, tn, wave, lane);
+            if constexpr (j == C::BNW - 1)
+              f.a[i] = frag(smem + cur_off + frag_unit<C>(true, 0, wm * C::BMW + i, 1) + lane * 16);
+            if constexpr (i == C::BMW - 1)
+              f.b[j] = frag(smem + cur_off + frag_unit<C>(false, 0, wn * C::BNW + j, 1) + lane * 16);
+            __builtin_amdgcn_sched_barrier(0);
+          });
+          cursor_next(nxt, g, t_end);
+          static_for<0, NQ>([&](auto qc) {
+            constexpr int q = decltype(qc)::value, i = q / C::BNW, j = q % C::BNW;
+            mfma_block(acc[i][j], f.a[i], f.b[j]);
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (q == BAR - 1) {
+              wait_vmcnt<PER_STAGE>();
+              wait_lgkm0();
+              block_barrier();
+            }
+            if constexpr (q >= BAR - 1) {
+              // registers whose last use is MFMA q (at the barrier: MFMA BAR - 1 or earlier)
+              static_for<0, C::BMW>([&](auto ic) {
+                constexpr int ii = decltype(ic)::value, last = ii * C::BNW + C::BNW - 1;
+                if constexpr (last == q || (q == BAR - 1 && last < q))
+                  f.a[ii] = frag(smem + next_off + frag_unit<C>(true, 0, wm * C::BMW + ii, 0) + lane * 16);
+              });
+              static_for<0, C::BNW>([&](auto jc) {
+                constexpr int jj = decltype(jc)::value, last = (C::BMW - 1) * C::BNW + jj;
+                if constexpr (last == q || (q == BAR - 1 && last < q))
+                  f.b[jj] = frag(smem + next_off + frag_unit<C>(false, 0, wn * C::BNW + jj, 0) + lane * 16);
+              });
+            }
+            if constexpr (q >= BAR && (q - BAR) % GAP1 == 0 && (q - BAR) / GAP1 < CPK)
+              load_one<C, (q - BAR) / GAP1>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
+            __builtin_amdgcn_sched_barrier(0);
+          });
+          buf = b1;
+        }
+        fold_product(p);
+      }
+    }
+  } else if constexpr (C::SCHED >= 1) {
     // Stream stage u sits in buffer u % NSTAGE.  During stage u each wave issues its copies of
     // stage u + NSTAGE - 1 into the buffer of stage u - 1 (freed by the barrier at the end of
     // stage u - 1), spread over the stage, one after every GAP-th MFMA: the eight waves' copies
@@ -1148,12 +1228,14 @@ double rounds(int64_t tiles, int cus) {
 // 16x16x128 MFMA, 10: as 9 with fragments read in place, 12: 256x256 with the int32 fold
 // accumulators of 3 blocks per wave in LDS and a 2-stage ring, 13: as 12 with 2 blocks per wave
 // in LDS and a 3-stage ring, 15: as 13 with the copies that refill a freed buffer spread over
-// the next stage's MFMAs, 16: as 15 with the second k-step's fragments read during the first.
-bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 16 && n != 11 && n != 14); }
+// the next stage's MFMAs, 16: as 15 with the second k-step's fragments read during the first,
+// 17: as 16 with the barrier inside the second k-step and the next stage's first fragments read
+// during the rest of it.
+bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 17 && n != 11 && n != 14); }
 
 // Tile configuration for a problem: AWE_GEMM_CFG if it names one, else the configuration whose
 // rounds of workgroups finish first: 5, 6 (a round about 1.48 times as long as a round of 5;
-// only when clearly sooner) or 16.  A round takes about 2.2 k + 1700 time units for 5 and
+// only when clearly sooner) or 17.  A round takes about 2.2 k + 1700 time units for 5 and
 // 3.9 k + 6000 for the 256x256 tile, k = r K / 6 reduction indices at r products: a fit of the
 // kernel times measured on MI355X for 4096^2 and 8192^2 outputs at K = 4096 .. 65536.  The
 // larger tile pays off once the reduction is long enough to amortise its fixed cost per round.
@@ -1168,7 +1250,7 @@ int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const double t128 = rounds(tm * ((N + 127) / 128), cus) * r128;
   const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.48 * r128;
   const double t256 = rounds(tm * ((N + 255) / 256), cus) * r256;
-  if (t256 < t128 && t256 < t192) return 16;
+  if (t256 < t128 && t256 < t192) return 17;
   return t192 < 0.97 * t128 ? 6 : 5;
 }
 
@@ -1516,13 +1598,14 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
     case 13: return launch_tile<Cfg8w64x128lf3>(g, L, stream);
     case 15: return launch_tile<Cfg8w64x128cs>(g, L, stream);
     case 16: return launch_tile<Cfg8w64x128cr>(g, L, stream);
+    case 17: return launch_tile<Cfg8w64x128cm>(g, L, stream);
     default: return launch_tile<Cfg8w64x64>(g, L, stream);
   }
 }
 
 // The grouped kernel is built for the 256 x 128 tiles on 8 waves (configurations 1, 4
-// and 5) and the 256 x 256 tiles of configuration 13 (with the schedules of 15 and 16 it
-// spills a register); the 256 x 192 ones leave no registers for the jobs' fields.
+// and 5) and the 256 x 256 tiles of configuration 13 (with the schedules of 15 - 17 it spills
+// a register); the 256 x 192 ones leave no registers for the jobs' fields.
 bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5 || cfg == 13; }
 
 bool gemm_group_ok(const GemmLaunch* L, int n) {

@@ -98,7 +98,8 @@ struct Cfg {
   // so that the eight waves' copies do not queue at the address unit at once and a wave waiting
   // for one has matrix work in flight.  2: as 1, and a later k-step's fragments are read during
   // the k-step before it, each as soon as the last MFMA that uses the register's old value has
-  // issued.
+  // issued.  3: as 2, with the barrier inside the second k-step after its first row of MFMAs,
+  // so that the next stage's first fragments are read during the rest of that k-step.
   static constexpr int SCHED = SCHED_;
   static_assert(SCHED == 0 ||
                     (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 && NSTAGE >= 3 &&
@@ -211,6 +212,8 @@ using Cfg8w64x128lf3 = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2>;
 // and with the second k-step's fragments read during the first (16)
 using Cfg8w64x128cs = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 1>;
 using Cfg8w64x128cr = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2>;
+// as 16 with the barrier inside the second k-step, after its first row of MFMAs (17)
+using Cfg8w64x128cm = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 3>;
 // all pairs of 3 planes per side (9 products, 5 accumulator groups): 128 x 128 on 8 waves of
 // 1 x 2 blocks, 2 k-steps per stage (48 KiB) in 3 stages, fragments read in place
 using Cfg8w32x64ap33 = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3>;

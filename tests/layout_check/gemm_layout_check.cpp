@@ -180,6 +180,7 @@ int main() {
   CFG(Cfg8w64x128lf3);
   CFG(Cfg8w64x128cs);
   CFG(Cfg8w64x128cr);
+  CFG(Cfg8w64x128cm);
   CFG(Cfg8w32x64ap33);
   CFG(Cfg8w32x64ap22o);
   CFG(Cfg8w64x64e2m3);

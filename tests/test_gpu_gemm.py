@@ -234,7 +234,7 @@ def test_mod_forced_segments():
     assert np.array_equal(C.cpu().numpy(), og.gemm_mod(m, A, B))
 
 
-@pytest.mark.parametrize("cfg", ["1", "2", "4", "5", "6", "7", "8", "9", "10", "12", "13", "15", "16"])
+@pytest.mark.parametrize("cfg", ["1", "2", "4", "5", "6", "7", "8", "9", "10", "12", "13", "15", "16", "17"])
 @pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_AWE4, awe.ENC_B13, awe.ENC_TERNARY])
 def test_every_tile_configuration(monkeypatch, cfg, enc):
     # AWE_GEMM_CFG forces one of the GEMM's tile configurations (256x128 on 8 waves with
@@ -307,7 +307,7 @@ def test_fp8fp4_4096_sampled():
         assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)
 
 
-@pytest.mark.parametrize("cfg,cus", [("5", "12"), ("6", "16"), ("12", "12"), ("13", "12"), ("15", "12"), ("16", "12")])
+@pytest.mark.parametrize("cfg,cus", [("5", "12"), ("6", "16"), ("12", "12"), ("13", "12"), ("15", "12"), ("16", "12"), ("17", "12")])
 @pytest.mark.parametrize("enc,out", [(awe.ENC_AWE6, torch.int32), (awe.ENC_AWE4, torch.int64),
                                      (awe.ENC_FP8FP4, torch.int32), (awe.ENC_FP16, torch.int64),
                                      (awe.ENC_FP6K3, torch.int32), (awe.ENC_FP6P4, torch.int32)])

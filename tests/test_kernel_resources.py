@@ -34,8 +34,10 @@ DEFAULTS = {
     "E4M3": _cfg(4, 2, 2, 2, 2, 3, 1, 1, 1, 32, 0),
     "E2M3 256x128, 4 k-steps per stage": _cfg(4, 2, 2, 2, 4, 2, 1, 2, 1, 32, 0),
     "E2M3 weights in the scales": _cfg(4, 2, 2, 2, 2, 2, 1, 2, 2, 32, 0),
-    "E2M1 256x256, copies spread over the stage, fragments read a k-step ahead in place (default)":
+    "E2M1 256x256, copies spread over the stage, fragments read a k-step ahead in place":
         _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 2),
+    "E2M1 256x256, as above with the barrier inside the second k-step (default)":
+        _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 3),
     "E2M1 base-13, all nine plane pairs in one stream": _cfg(4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3),
     "E2M1 FP16 significands, outer groups": _cfg(4, 2, 1, 2, 2, 4, 1, 0, 1, 32, 0, 0, 2, 2, 3, 1),
 }

@@ -413,7 +413,9 @@ def residues_workload(dev, n=4096):
 
 def stress_workload(dev, M=4096, N=4096, K=65536):
     """Accumulation stress (every entry -128 or 127, structured rows and columns), AWE6, int64 C:
-    the GEMM on resident planes with the default fold segment and with a forced one of 4096."""
+    the GEMM on resident planes with the default fold segment and with a forced one of 4096, timed
+    alternately twice (the second pass is reported: the first GEMMs on freshly written planes run
+    slower)."""
     import torch
 
     from paper_2609_24519_amd import awe, inputs
@@ -432,11 +434,12 @@ def stress_workload(dev, M=4096, N=4096, K=65536):
     ops = 2.0 * M * N * K
     out = {"workload": "AWE6 exact GEMM, M=N=%d, K=%d, entries -128 or 127 (structured stress operands), "
                        "int64 C" % (M, K)}
-    for name, kseg in (("default_fold_segment", 0), ("fold_segment_4096", 4096)):
-        ms = _time_ms(lambda: awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I64, kseg, stream), 5, stream)
-        tf = r * ops / (ms * 1e-3) / 1e12
-        out[name] = {"gemm_ms": round(ms, 4), "gemm_exact_TOPS": round(ops / (ms * 1e-3) / 1e12, 1),
-                     "fp4_TFLOPs": round(tf, 1), "fp4_peak_frac": round(tf / FP4_PEAK_TFLOPS, 4)}
+    for _ in range(2):
+        for name, kseg in (("default_fold_segment", 0), ("fold_segment_4096", 4096)):
+            ms = _time_ms(lambda: awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I64, kseg, stream), 5, stream)
+            tf = r * ops / (ms * 1e-3) / 1e12
+            out[name] = {"gemm_ms": round(ms, 4), "gemm_exact_TOPS": round(ops / (ms * 1e-3) / 1e12, 1),
+                         "fp4_TFLOPs": round(tf, 1), "fp4_peak_frac": round(tf / FP4_PEAK_TFLOPS, 4)}
     del pa, pb, C
     torch.cuda.empty_cache()
     return out

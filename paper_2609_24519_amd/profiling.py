@@ -13,8 +13,9 @@ Markdown table.  ``traffic`` takes two ``--pmc`` runs (FETCH_SIZE, then
 WRITE_SIZE, each in KiB per dispatch) of a command that also ran a plain
 device copy of a known size (``bench.py --calibrate-copy``), scales every
 kernel's counters by what the counters read for that copy, and records the
-per-dispatch HBM bytes of the GEMM together with a hash of the kernel source
-they were taken on, so that a later change to the kernel makes them stale.
+per-dispatch HBM bytes of the GEMM together with a hash of the kernel sources
+they were taken on (the kernels and the GEMM's addressing header), so that a
+later change to either makes them stale.
 ``counters`` summarises one or more ``--pmc`` passes over the same command:
 per kernel the FP4 MFMA operation count (checked against the algorithmic
 r 2MNK), MFMA busy cycles, LDS bank conflicts and activity, L2 hit rate and
@@ -28,13 +29,17 @@ import os
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-KERNEL_SOURCE = os.path.join(HERE, "csrc", "awe_kernels.hip")
+# the GEMM's kernel code and its addressing (tile configurations, copy / LDS / fragment offsets)
+KERNEL_SOURCES = (os.path.join(HERE, "csrc", "awe_kernels.hip"), os.path.join(HERE, "csrc", "gemm_layout.h"))
 COPY_BYTES = 1 << 30  # bench.py --calibrate-copy copies 1 GiB
 
 
 def kernel_source_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 _LABELS = (  # first match wins
@@ -73,8 +78,12 @@ def stats(csv_path, out_md, command, skip=0):
         for r in rows:
             per.setdefault(r["Kernel_Name"], []).append(
                 (int(r["Start_Timestamp"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
-        lines += ["Per-dispatch durations from the kernel trace, the first %d dispatches of each kernel "
-                  "(the warm-up steps) left out." % skip, ""]
+        if skip:
+            lines += ["Per-dispatch durations from the kernel trace, the first %d dispatches of each kernel "
+                      "(the warm-up steps) left out." % skip, ""]
+        else:
+            lines += ["Per-dispatch durations from the kernel trace, every dispatch (the command's own warm-up "
+                      "calls included).", ""]
         table = []
         for name, d in per.items():
             d = [us for _, us in sorted(d)][skip:]

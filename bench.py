@@ -254,15 +254,8 @@ def main():
         tinfo, pta, ptb = setup(awe.ENC_TERNARY)
         awe.encode(awe.ENC_TERNARY, 0, awe.SIDE_A, At, M, K, K, pta, None, stream)
         awe.encode(awe.ENC_TERNARY, 0, awe.SIDE_B, B, N, K, N, ptb, None, stream)
-        awe.gemm_planes(awe.ENC_TERNARY, 0, M, N, K, pta, ptb, C, N, awe.I32, 0, stream)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(5):
-            awe.gemm_planes(awe.ENC_TERNARY, 0, M, N, K, pta, ptb, C, N, awe.I32, 0, stream)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        tms = e0.elapsed_time(e1) / 5
+        tms = _time_ms(lambda: awe.gemm_planes(awe.ENC_TERNARY, 0, M, N, K, pta, ptb, C, N, awe.I32, 0, stream),
+                       10, stream, warm=3)
         line["ternary_3_products"] = {
             "gemm_ms": round(tms, 4), "gemm_exact_TOPS": round(ops / (tms * 1e-3) / 1e12, 2),
             "fp4_peak_frac": round(tinfo["r"] * ops / (tms * 1e-3) / 1e12 / FP4_PEAK_TFLOPS, 4)}
@@ -293,11 +286,13 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def _time_ms(fn, reps, stream):
-    """Average milliseconds of fn() over reps calls, HIP events on `stream` after one warm-up call."""
+def _time_ms(fn, reps, stream, warm=1):
+    """Average milliseconds of fn() over reps calls, HIP events on `stream` after `warm` warm-up
+    calls."""
     import torch
 
-    fn()
+    for _ in range(warm):
+        fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
@@ -451,7 +446,8 @@ WORKLOAD_FNS = {"awe4_int4xint8": awe4_workload, "residues_per_modulus": residue
 
 def fp16_context(dev, n):
     """App. A's FP16-significand scheme: 12-bit integers (int16 in [-2048, 2047]) in 12 FP4
-    products (four launch groups), n^3, int64 C, awe_gemm_planes on resident planes."""
+    products (one launch), n^3, int64 C, awe_gemm_planes on resident planes: 10 calls timed after
+    3 warm-up calls (the first calls on freshly written planes run slower)."""
     import numpy as np
     import torch
 
@@ -468,15 +464,7 @@ def fp16_context(dev, n):
     stream = torch.cuda.current_stream()
     awe.encode(enc, 0, awe.SIDE_A, A, n, n, n, pa, None, stream)
     awe.encode(enc, 0, awe.SIDE_B, B, n, n, n, pb, None, stream)
-    awe.gemm_planes(enc, 0, n, n, n, pa, pb, C, n, awe.I64, 0, stream)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(3):
-        awe.gemm_planes(enc, 0, n, n, n, pa, pb, C, n, awe.I64, 0, stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / 3
+    ms = _time_ms(lambda: awe.gemm_planes(enc, 0, n, n, n, pa, pb, C, n, awe.I64, 0, stream), 10, stream, warm=3)
     ops = 2.0 * n * n * n
     out = {"workload": "M=N=K=%d, int16 entries uniform in [-2048, 2047], int64 C" % n,
            "gemm_ms": round(ms, 3), "gemm_exact_TOPS": round(ops / (ms * 1e-3) / 1e12, 1),

@@ -773,7 +773,10 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
   constexpr int NSTAGE = C::NSTAGE;
   if constexpr (C::SCHED == 3) {
     // Stream stage u sits in buffer u % 3; its barrier sits inside its second k-step, after the
-    // MFMAs of the first row of blocks (BAR of them).
+    // MFMAs of the first row of fragments (BAR of them).  A k-step's MFMAs run over the NR x NC
+    // pairs of the wave's A and B fragments, row by row (all pairs: row pi * BMW + i is block i
+    // of the stage's A plane pi, column pj * BNW + j block j of B plane pj, into accumulator
+    // group pi + pj).
     //  k-step 0: MFMAs on fragments read before; the fragments of k-step 1 are read from
     //    buffer u into each register set as soon as its last k-step-0 MFMA has issued; the
     //    second half of stage u + 2's copies go to buffer (u + 2) % 3.
@@ -785,8 +788,26 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
     //    (u + 1) % 3 into the registers already free and then as more free up; the first half of
     //    stage u + 3's copies go to buffer u.
     constexpr int PER_STAGE = C::A_PW + C::B_LO;  // copies per wave and stage
-    constexpr int CPK = PER_STAGE / 2, NQ = C::BMW * C::BNW, GAP = NQ / CPK, BAR = C::BNW;
+    constexpr int NR = C::SPA * C::BMW, NC = C::SPB * C::BNW;  // fragment rows and columns
+    constexpr int CPK = PER_STAGE / 2, NQ = NR * NC, GAP = NQ / CPK, BAR = NC;
     constexpr int GAP1 = (NQ - BAR) / CPK;  // spacing of the copies after the barrier
+    Frags<C> f;
+    // MFMA q of a k-step, and the reads of fragment row r / column c of k-step ks from a buffer
+    auto mfma_q = [&](auto qc) {
+      constexpr int q = decltype(qc)::value, r = q / NC, c = q % NC;
+      if constexpr (C::AP)
+        mfma_block(accg[r / C::BMW + c / C::BNW][r % C::BMW][c % C::BNW], f.a[r], f.b[c]);
+      else
+        mfma_block(acc[r][c], f.a[r], f.b[c]);
+    };
+    auto read_a = [&](auto rc, uint32_t off, int ks) {
+      constexpr int r = decltype(rc)::value;
+      f.a[r] = frag(smem + off + frag_unit<C>(true, r / C::BMW, wm * C::BMW + r % C::BMW, ks) + lane * 16);
+    };
+    auto read_b = [&](auto cc, uint32_t off, int ks) {
+      constexpr int c = decltype(cc)::value;
+      f.b[c] = frag(smem + off + frag_unit<C>(false, c / C::BNW, wn * C::BNW + c % C::BNW, ks) + lane * 16);
+    };
     static_assert(C::KSTEPS == 2 && NSTAGE == 3 && PER_STAGE % 2 == 0 && GAP1 >= 1, "schedule 3");
     Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
     load_stage<C>(g, nxt, lds0, tm, tn, wave, lane);
@@ -798,7 +819,6 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
     });
     wait_vmcnt<PER_STAGE + CPK>();
     block_barrier();
-    Frags<C> f;
     read_frags<C>(f, smem, 0, wm, wn, lane);
     int buf = 0;
     for (int cs = t_beg; cs < t_end; cs += g.ts) {
@@ -808,21 +828,19 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
           const int b1 = buf == 2 ? 0 : buf + 1, b2 = b1 == 2 ? 0 : b1 + 1;
           const uint32_t cur_off = buf * C::STAGE_BYTES, next_off = b1 * C::STAGE_BYTES;
           static_for<0, NQ>([&](auto qc) {
-            constexpr int q = decltype(qc)::value, i = q / C::BNW, j = q % C::BNW;
-            mfma_block(acc[i][j], f.a[i], f.b[j]);
+            constexpr int q = decltype(qc)::value, r = q / NC, c = q % NC;
+            mfma_q(qc);
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (q % GAP == 0)
               load_one<C, CPK + q / GAP>(g, nxt, lds0 + b2 * C::STAGE_BYTES, tm, tn, wave, lane);
-            if constexpr (j == C::BNW - 1)
-              f.a[i] = frag(smem + cur_off + frag_unit<C>(true, 0, wm * C::BMW + i, 1) + lane * 16);
-            if constexpr (i == C::BMW - 1)
-              f.b[j] = frag(smem + cur_off + frag_unit<C>(false, 0, wn * C::BNW + j, 1) + lane * 16);
+            if constexpr (c == NC - 1) read_a(std::integral_constant<int, r>{}, cur_off, 1);
+            if constexpr (r == NR - 1) read_b(std::integral_constant<int, c>{}, cur_off, 1);
             __builtin_amdgcn_sched_barrier(0);
           });
           cursor_next(nxt, g, t_end);
           static_for<0, NQ>([&](auto qc) {
-            constexpr int q = decltype(qc)::value, i = q / C::BNW, j = q % C::BNW;
-            mfma_block(acc[i][j], f.a[i], f.b[j]);
+            constexpr int q = decltype(qc)::value;
+            mfma_q(qc);
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (q == BAR - 1) {
               wait_vmcnt<PER_STAGE>();
@@ -831,15 +849,13 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
             }
             if constexpr (q >= BAR - 1) {
               // registers whose last use is MFMA q (at the barrier: MFMA BAR - 1 or earlier)
-              static_for<0, C::BMW>([&](auto ic) {
-                constexpr int ii = decltype(ic)::value, last = ii * C::BNW + C::BNW - 1;
-                if constexpr (last == q || (q == BAR - 1 && last < q))
-                  f.a[ii] = frag(smem + next_off + frag_unit<C>(true, 0, wm * C::BMW + ii, 0) + lane * 16);
+              static_for<0, NR>([&](auto rc) {
+                constexpr int last = decltype(rc)::value * NC + NC - 1;
+                if constexpr (last == q || (q == BAR - 1 && last < q)) read_a(rc, next_off, 0);
               });
-              static_for<0, C::BNW>([&](auto jc) {
-                constexpr int jj = decltype(jc)::value, last = (C::BMW - 1) * C::BNW + jj;
-                if constexpr (last == q || (q == BAR - 1 && last < q))
-                  f.b[jj] = frag(smem + next_off + frag_unit<C>(false, 0, wn * C::BNW + jj, 0) + lane * 16);
+              static_for<0, NC>([&](auto cc) {
+                constexpr int last = (NR - 1) * NC + decltype(cc)::value;
+                if constexpr (last == q || (q == BAR - 1 && last < q)) read_b(cc, next_off, 0);
               });
             }
             if constexpr (q >= BAR && (q - BAR) % GAP1 == 0 && (q - BAR) / GAP1 < CPK)

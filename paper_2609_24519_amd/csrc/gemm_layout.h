@@ -70,8 +70,8 @@ struct Cfg {
   static constexpr int OUTG = OUTG_;
   static constexpr int NOUT = OUTG ? NG : 1;
   static_assert(!OUTG || AP, "outer groups belong to the all-pairs stream");
-  static_assert(!AP || (NPB > 0 && FMT == 0 && NPL == 1 && MF == 32 && NLB_ == 0 && SCHED_ == 0),
-                "all pairs: E2M1, 32x32x64 MFMAs, int32 accumulators in registers, schedule 0");
+  static_assert(!AP || (NPB > 0 && FMT == 0 && NPL == 1 && MF == 32 && NLB_ == 0 && (SCHED_ == 0 || SCHED_ == 3)),
+                "all pairs: E2M1, 32x32x64 MFMAs, int32 accumulators in registers, schedule 0 or 3");
   static constexpr int PA_UNITS = (BM / kBrickRows) * KU;  // per plane and stage: row blocks x units
   static constexpr int PB_UNITS = (BN / kBrickRows) * KU;
   static constexpr int SPA = AP ? NPA : NPL, SPB = AP ? NPB : NPL;  // planes per side in a stage
@@ -103,7 +103,7 @@ struct Cfg {
   static constexpr int SCHED = SCHED_;
   static_assert(SCHED == 0 ||
                     (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 && NSTAGE >= 3 &&
-                     (A_PW + B_LO) % KSTEPS == 0 && (BMW * BNW) % ((A_PW + B_LO) / KSTEPS) == 0),
+                     (A_PW + B_LO) % KSTEPS == 0 && (SPA * BMW * SPB * BNW) % ((A_PW + B_LO) / KSTEPS) == 0),
                 "copies between the MFMAs: E2M1, one plane per side, 32x32x64 MFMAs, fragments in place, "
                 "the copies spread evenly over the k-steps");
 };
@@ -219,8 +219,9 @@ using Cfg8w64x128cm = Cfg<4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 3>;
 using Cfg8w32x64ap33 = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3>;
 // all pairs of 2 planes per side, 3 apart (the two halves of a 12-bit significand), each group
 // i + j with its own int32 accumulator and outer weight: 128 x 128 on 8 waves of 1 x 2 blocks,
-// 2 k-steps per stage (32 KiB) in 4 stages, fragments read one k-step ahead
-using Cfg8w32x64ap22o = Cfg<4, 2, 1, 2, 2, 4, 1, 0, 1, 32, 0, 0, 2, 2, 3, 1>;
+// 2 k-steps per stage (32 KiB) in 3 stages, on schedule 3 (fragments read in place during the
+// k-step before, the barrier inside the second k-step)
+using Cfg8w32x64ap22o = Cfg<4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 3, 2, 2, 3, 1>;
 // E2M3 operands (3 KiB units of two k-steps)
 using Cfg8w64x64e2m3 = Cfg<4, 2, 2, 2, 2, 3, 1, 2>;   // 256 x 128, 8 waves, 2 k-steps, 3 stages
 using Cfg8w64x64s4e2m3 = Cfg<4, 2, 2, 2, 2, 4, 1, 2>; // 256 x 128, 8 waves, 2 k-steps, 4 stages

@@ -39,7 +39,7 @@ DEFAULTS = {
     "E2M1 256x256, as above with the barrier inside the second k-step (default)":
         _cfg(4, 2, 2, 4, 2, 3, 0, 0, 1, 32, 2, 3),
     "E2M1 base-13, all nine plane pairs in one stream": _cfg(4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 0, 3, 3),
-    "E2M1 FP16 significands, outer groups": _cfg(4, 2, 1, 2, 2, 4, 1, 0, 1, 32, 0, 0, 2, 2, 3, 1),
+    "E2M1 FP16 significands, outer groups": _cfg(4, 2, 1, 2, 2, 3, 0, 0, 1, 32, 0, 3, 2, 2, 3, 1),
 }
 
 

@@ -1251,10 +1251,12 @@ bool e2m1_cfg(int n) { return n == 1 || n == 2 || (n >= 4 && n <= 17 && n != 11 
 
 // Tile configuration for a problem: AWE_GEMM_CFG if it names one, else the configuration whose
 // rounds of workgroups finish first: 5, 6 (a round about 1.48 times as long as a round of 5;
-// only when clearly sooner) or 17.  A round takes about 2.2 k + 1700 time units for 5 and
-// 3.9 k + 6000 for the 256x256 tile, k = r K / 6 reduction indices at r products: a fit of the
-// kernel times measured on MI355X for 4096^2 and 8192^2 outputs at K = 4096 .. 65536.  The
-// larger tile pays off once the reduction is long enough to amortise its fixed cost per round.
+// only when clearly sooner) or 17.  A round takes about 2.05 k + 1090 time units (10 ns) for 5
+// and 3.76 k + 1800 for 17, k = r K / 6 reduction indices at r products: a fit of the kernel
+// times measured on one MI355X for 8192^2 outputs at K = 2048 .. 8192 (r = 6); it also orders
+// 4096^2 outputs at K = 4096 .. 16384 with 1 to 6 products, 6144^3 and 2048^2 x 8192 as
+// measured.  The larger tile moves fewer bytes per MAC but fills the chip only with enough
+// tiles: at 2048^2 x 8192 its 64 tiles leave most CUs idle and 5 wins.
 int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
@@ -1262,7 +1264,7 @@ int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
   const int cus = compute_units();
   const int64_t tm = (M + 255) / 256;
   const double k = (double)r * (double)K / 6.0;
-  const double r128 = 2.2 * k + 1700.0, r256 = 3.9 * k + 6000.0;
+  const double r128 = 2.05 * k + 1090.0, r256 = 3.76 * k + 1800.0;
   const double t128 = rounds(tm * ((N + 127) / 128), cus) * r128;
   const double t192 = rounds(tm * ((N + 191) / 192), cus) * 1.48 * r128;
   const double t256 = rounds(tm * ((N + 255) / 256), cus) * r256;

@@ -1273,9 +1273,10 @@ int choose_cfg(int64_t M, int64_t N, int r, int64_t K) {
 }
 
 // Tile configuration of a grouped launch of n jobs of one shape: AWE_GEMM_CFG if set, else 5
-// or 13 (the configurations the grouped kernel is built for), whichever the per-round model of
-// choose_cfg gives less time summed over the jobs' tiles (many jobs fill the rounds, so the
-// rounds are not quantised).
+// or 16 (256 x 128 or 256 x 256, the latter on config 16's schedule), whichever a per-round model
+// fitted to configs 5 and 13 gives less time summed over the jobs' tiles (many jobs fill the
+// rounds, so the rounds are not quantised); config 16 runs the residue route's grouped GEMM at
+// 4096 x 4096 x 16384 about 4 % faster than 13.
 int choose_group_cfg(const GemmLaunch* L, int n) {
   const char* e = getenv("AWE_GEMM_CFG");
   const int forced = e ? atoi(e) : -1;
@@ -1288,7 +1289,7 @@ int choose_group_cfg(const GemmLaunch* L, int n) {
     s128 += t128 * (2.2 * k + 1700.0);
     s256 += t256 * (3.9 * k + 6000.0);
   }
-  return s256 < s128 ? 13 : 5;
+  return s256 < s128 ? 16 : 5;
 }
 
 // Tile configuration for E2M3 operands: AWE_GEMM_CFG_E2M3 (0: 256x128 with 8 waves in
@@ -1622,9 +1623,9 @@ awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
 }
 
 // The grouped kernel is built for the 256 x 128 tiles on 8 waves (configurations 1, 4
-// and 5) and the 256 x 256 tiles of configuration 13 (with the schedules of 15 - 17 it spills
-// a register); the 256 x 192 ones leave no registers for the jobs' fields.
-bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5 || cfg == 13; }
+// and 5) and the 256 x 256 tiles of configurations 13 and 16 (with config 17's schedule it
+// spills 23 registers); the 256 x 192 ones leave no registers for the jobs' fields.
+bool group_cfg(int cfg) { return cfg == 1 || cfg == 4 || cfg == 5 || cfg == 13 || cfg == 16; }
 
 bool gemm_group_ok(const GemmLaunch* L, int n) {
   if (n < 1 || n > kMaxModuli) return false;
@@ -1657,6 +1658,7 @@ awe_status launch_gemm_group(const GemmLaunch* L, int n, hipStream_t stream) {
     case 4: return launch_group_tile<Cfg8w64x64k4>(L, order, n, stream);
     case 5: return launch_group_tile<Cfg8w64x64k4p3>(L, order, n, stream);
     case 13: return launch_group_tile<Cfg8w64x128lf3>(L, order, n, stream);
+    case 16: return launch_group_tile<Cfg8w64x128cr>(L, order, n, stream);
     default: return launch_group_tile<Cfg8w64x64>(L, order, n, stream);
   }
 }

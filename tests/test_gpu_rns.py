@@ -144,10 +144,10 @@ def test_gemm_crt_full(shape):
 
 
 @pytest.mark.parametrize("grouped,cfg", [("1", None), ("0", None), ("1", "4"), ("1", "1"), ("1", "6"), ("1", "13"),
-                                          ("1", "16")])
+                                          ("1", "16"), ("1", "17")])
 def test_gemm_crt_grouped_launch(monkeypatch, grouped, cfg):
     # the moduli's GEMMs run as one grouped launch (jobs with the most products first) or,
-    # with AWE_GEMM_GROUPED=0 or a tile configuration the grouped kernel lacks (6, 16), one launch
+    # with AWE_GEMM_GROUPED=0 or a tile configuration the grouped kernel lacks (6, 17), one launch
     # per modulus; 9 tiles per modulus (256 x 128) are not a multiple of the 8 XCDs
     monkeypatch.setenv("AWE_GEMM_GROUPED", grouped)
     if cfg is not None:

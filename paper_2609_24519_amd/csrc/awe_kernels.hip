@@ -778,19 +778,20 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
     // of the stage's A plane pi, column pj * BNW + j block j of B plane pj, into accumulator
     // group pi + pj).
     //  k-step 0: MFMAs on fragments read before; the fragments of k-step 1 are read from
-    //    buffer u into each register set as soon as its last k-step-0 MFMA has issued; the
-    //    second half of stage u + 2's copies go to buffer (u + 2) % 3.
+    //    buffer u into each register set as soon as its last k-step-0 MFMA has issued; stage
+    //    u + 2's copies go to buffer (u + 2) % 3 (freed by the barrier of stage u - 1), one after
+    //    every other MFMA (after the odd ones: 1-2 % faster than right after that barrier, where
+    //    they meet every wave's reads of the next fragments, or after the even MFMAs).
     //  k-step 1, first BAR MFMAs; then wait until stage u + 1 has landed (stage u + 2's copies
     //    may still be in flight) and this wave's reads of buffer u are done (they have had the
     //    first BAR MFMAs to land); barrier: every wave is done with buffer u, stage u + 1 is
     //    complete.
     //  k-step 1, the other MFMAs: stage u + 1's k-step-0 fragments are read from buffer
-    //    (u + 1) % 3 into the registers already free and then as more free up; the first half of
-    //    stage u + 3's copies go to buffer u.
+    //    (u + 1) % 3 into the registers already free and then as more free up.
     constexpr int PER_STAGE = C::A_PW + C::B_LO;  // copies per wave and stage
     constexpr int NR = C::SPA * C::BMW, NC = C::SPB * C::BNW;  // fragment rows and columns
-    constexpr int CPK = PER_STAGE / 2, NQ = NR * NC, GAP = NQ / CPK, BAR = NC;
-    constexpr int GAP1 = (NQ - BAR) / CPK;  // spacing of the copies after the barrier
+    constexpr int NQ = NR * NC, BAR = NC;
+    constexpr int GAP = NQ / PER_STAGE;  // MFMAs per copy in k-step 0
     Frags<C> f;
     // MFMA q of a k-step, and the reads of fragment row r / column c of k-step ks from a buffer
     auto mfma_q = [&](auto qc) {
@@ -808,16 +809,13 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
       constexpr int c = decltype(cc)::value;
       f.b[c] = frag(smem + off + frag_unit<C>(false, c / C::BNW, wn * C::BNW + c % C::BNW, ks) + lane * 16);
     };
-    static_assert(C::KSTEPS == 2 && NSTAGE == 3 && PER_STAGE % 2 == 0 && GAP1 >= 1, "schedule 3");
+    static_assert(C::KSTEPS == 2 && NSTAGE == 3 && NQ % PER_STAGE == 0, "schedule 3");
     Cursor nxt{0, t_beg, t_beg, min(t_beg + g.ts, t_end)};
     load_stage<C>(g, nxt, lds0, tm, tn, wave, lane);
     cursor_next(nxt, g, t_end);
     load_stage<C>(g, nxt, lds0 + C::STAGE_BYTES, tm, tn, wave, lane);
     cursor_next(nxt, g, t_end);
-    static_for<0, CPK>([&](auto qc) {
-      load_one<C, decltype(qc)::value>(g, nxt, lds0 + 2 * C::STAGE_BYTES, tm, tn, wave, lane);
-    });
-    wait_vmcnt<PER_STAGE + CPK>();
+    wait_vmcnt<PER_STAGE>();
     block_barrier();
     read_frags<C>(f, smem, 0, wm, wn, lane);
     int buf = 0;
@@ -831,8 +829,8 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
             constexpr int q = decltype(qc)::value, r = q / NC, c = q % NC;
             mfma_q(qc);
             __builtin_amdgcn_sched_barrier(0);
-            if constexpr (q % GAP == 0)
-              load_one<C, CPK + q / GAP>(g, nxt, lds0 + b2 * C::STAGE_BYTES, tm, tn, wave, lane);
+            if constexpr (q % GAP == GAP / 2)
+              load_one<C, q / GAP>(g, nxt, lds0 + b2 * C::STAGE_BYTES, tm, tn, wave, lane);
             if constexpr (c == NC - 1) read_a(std::integral_constant<int, r>{}, cur_off, 1);
             if constexpr (r == NR - 1) read_b(std::integral_constant<int, c>{}, cur_off, 1);
             __builtin_amdgcn_sched_barrier(0);
@@ -858,8 +856,6 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
                 if constexpr (last == q || (q == BAR - 1 && last < q)) read_b(cc, next_off, 0);
               });
             }
-            if constexpr (q >= BAR && (q - BAR) % GAP1 == 0 && (q - BAR) / GAP1 < CPK)
-              load_one<C, (q - BAR) / GAP1>(g, nxt, lds0 + cur_off, tm, tn, wave, lane);
             __builtin_amdgcn_sched_barrier(0);
           });
           buf = b1;

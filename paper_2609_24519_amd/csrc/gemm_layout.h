@@ -99,7 +99,8 @@ struct Cfg {
   // for one has matrix work in flight.  2: as 1, and a later k-step's fragments are read during
   // the k-step before it, each as soon as the last MFMA that uses the register's old value has
   // issued.  3: as 2, with the barrier inside the second k-step after its first row of MFMAs,
-  // so that the next stage's first fragments are read during the rest of that k-step.
+  // so that the next stage's first fragments are read during the rest of that k-step, and each
+  // refill issued during the first k-step of the stage after its buffer was freed.
   static constexpr int SCHED = SCHED_;
   static_assert(SCHED == 0 ||
                     (NPL == 1 && MF == 32 && B_XTRA == 0 && COPIES == 1 && PD == 0 && NSTAGE >= 3 &&

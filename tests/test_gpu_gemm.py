@@ -256,6 +256,29 @@ def test_every_tile_configuration(monkeypatch, cfg, enc):
 
 
 
+@pytest.mark.parametrize("cfg", ["16", "17"])
+@pytest.mark.parametrize("shape,kseg,out", [
+    ((256, 256, 1), 0, torch.int32),        # the whole reduction in 2 stages: copies past its end
+    ((300, 420, 257), 0, torch.int32),      # 4 stages, ragged tiles
+    ((512, 512, 1024), 0, torch.int32),     # whole 256 x 256 tiles (16-byte row epilogue)
+    ((512, 256, 3000), 256, torch.int32),   # a fold every 2 stages, whole tiles
+    ((260, 520, 1500), 512, torch.int64),   # int64 C, ragged, a fold every 4 stages
+])
+def test_long_reduction_schedules_edges(monkeypatch, cfg, shape, kseg, out):
+    # configs 16 and 17 (256 x 256, copies between the MFMAs, fragments read during the k-step
+    # before, config 17's barrier inside the second k-step; 17 is the default for long
+    # reductions): reductions of a few stages, forced fold segments, whole and ragged tiles
+    monkeypatch.setenv("AWE_GEMM_CFG", cfg)
+    M, N, K = shape
+    enc = awe.ENC_AWE6
+    A, B = _operands(enc, M, N, K, seed=K % 97 + int(cfg))
+    pa, pb = _planes(enc, 0, A, B)
+    C = torch.empty((M, N), dtype=out, device="cuda")
+    awe.gemm_planes(enc, 0, M, N, K, pa, pb, C, N, awe.I64 if out == torch.int64 else awe.I32, kseg)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy().astype(np.int64), og.gemm_i64(A, B))
+
+
 def test_ternary_4096_sampled():
     # {0, +-1} x INT8 (Sec. 6.2) at 4096 x 4096 x 8192, int32 C, sampled tiles
     M = N = 4096

@@ -81,3 +81,12 @@ def test_other_kernels_use_no_scratch(rows):
         if "gemm" in r[0]:
             continue
         assert r[7] == 0, r
+
+
+def test_encoders_keep_four_waves_per_simd(rows):
+    # The byte encoders are HBM-bound and need four waves per SIMD (at most 128 registers) to keep
+    # enough loads in flight: at 148 registers (three waves) the B side took 15 % longer.
+    enc = [r for r in rows if "13encode_kernel" in r[0]]
+    assert len(enc) == 2, enc
+    for r in enc:
+        assert r[1] + r[2] <= 128, r

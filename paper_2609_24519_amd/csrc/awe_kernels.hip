@@ -12,6 +12,7 @@
 
 #include "awe_internal.h"
 #include "gemm_layout.h"
+#include "plane_pack.h"
 
 namespace awe {
 
@@ -177,42 +178,14 @@ __global__ __launch_bounds__(256, 4) void encode_kernel(const uint8_t* __restric
   }
   uint8_t* dst = planes + 2 * nplanes8 * plane_stride + (ks * R32 + rb) * kBrickBytes + lane * 16;
   if (nplanes8 == 0) {
-    // All planes E2M1, plane p's code in bits 4p .. 4p + 3 of e[j]: a nibble transpose.  Byte q
-    // of x[i] (y[i]) holds the codes of plane 2q (2q + 1) for elements 2i (low nibble) and 2i + 1;
-    // a 4 x 4 byte transpose of x[4w .. 4w + 3] gives dword w of planes 0, 2, 4, 6, which holds
-    // elements 8w .. 8w + 7, as the stored layout wants.  (About a third of the VALU work of
-    // packing each plane nibble by nibble, which bounded the encoder's rate.)
-    uint32_t x[16], y[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint32_t lo = e[2 * i], hi = e[2 * i + 1];
-      x[i] = (lo & 0x0f0f0f0fu) | ((hi & 0x0f0f0f0fu) << 4);
-      y[i] = ((lo >> 4) & 0x0f0f0f0fu) | (hi & 0xf0f0f0f0u);
-    }
-    uint32_t px[4][4], py[4][4];  // [dword w][plane pair q]
-    auto transpose4 = [](const uint32_t* v, uint32_t* out) {
-      // v_perm_b32: result byte k = byte sel_k of {first operand : second operand}, the second
-      // operand being bytes 0..3
-      const uint32_t t0 = __builtin_amdgcn_perm(v[1], v[0], 0x05010400u);
-      const uint32_t t1 = __builtin_amdgcn_perm(v[1], v[0], 0x07030602u);
-      const uint32_t t2 = __builtin_amdgcn_perm(v[3], v[2], 0x05010400u);
-      const uint32_t t3 = __builtin_amdgcn_perm(v[3], v[2], 0x07030602u);
-      out[0] = __builtin_amdgcn_perm(t2, t0, 0x05040100u);
-      out[1] = __builtin_amdgcn_perm(t2, t0, 0x07060302u);
-      out[2] = __builtin_amdgcn_perm(t3, t1, 0x05040100u);
-      out[3] = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
-    };
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      transpose4(x + 4 * w, px[w]);
-      transpose4(y + 4 * w, py[w]);
-    }
+    // All planes E2M1: the nibble transpose of pack_e2m1_planes (about a third of the VALU work
+    // of packing each plane nibble by nibble, which bounded the encoder's rate).
+    uint32_t d[8][4];
+    pack_e2m1_planes<8>(e, d);
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       if (p >= nplanes) break;
-      const uint32_t(*src)[4] = (p & 1) ? py : px;
-      *reinterpret_cast<uint4*>(dst + p * plane_stride) =
-          make_uint4(src[0][p >> 1], src[1][p >> 1], src[2][p >> 1], src[3][p >> 1]);
+      *reinterpret_cast<uint4*>(dst + p * plane_stride) = make_uint4(d[p][0], d[p][1], d[p][2], d[p][3]);
     }
     continue;
   }

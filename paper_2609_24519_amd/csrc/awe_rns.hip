@@ -6,8 +6,10 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <type_traits>
 
 #include "awe_internal.h"
+#include "plane_pack.h"
 
 namespace awe {
 namespace {
@@ -213,12 +215,27 @@ __global__ __launch_bounds__(256) void residue_encode_kernel(ResidueEncodeArgs a
 #pragma unroll
       for (int e = 0; e < 32; ++e) code[e] = ((ok >> e) & 1u) ? slut[j * 256 + r[e]] : 0u;
       uint8_t* dst = a.planes + a.off[j] + (ks * a.R32 + rb) * kBrickBytes + lane * 16;
-      for (int pl = 0; pl < a.np[j]; ++pl) {
-        uint32_t d[4] = {0, 0, 0, 0};
+      // the nibble transpose for exactly the planes the modulus has (1 to 3 for the mod-m
+      // schemes; up to 8 fit a code word)
+      auto store = [&](auto npc) {
+        constexpr int NP = decltype(npc)::value;
+        uint32_t d[NP][4];
+        pack_e2m1_planes<NP>(code, d);
 #pragma unroll
-        for (int e = 0; e < 32; ++e) d[e >> 3] |= ((code[e] >> (4 * pl)) & 0xfu) << (4 * (e & 7));
-        *reinterpret_cast<uint4*>(dst + pl * a.plane_stride) = make_uint4(d[0], d[1], d[2], d[3]);
-      }
+        for (int pl = 0; pl < NP; ++pl) {
+          if (pl >= a.np[j]) break;
+          *reinterpret_cast<uint4*>(dst + pl * a.plane_stride) = make_uint4(d[pl][0], d[pl][1], d[pl][2], d[pl][3]);
+        }
+      };
+      const int np = a.np[j];
+      if (np == 1)
+        store(std::integral_constant<int, 1>{});
+      else if (np == 2)
+        store(std::integral_constant<int, 2>{});
+      else if (np == 3)
+        store(std::integral_constant<int, 3>{});
+      else
+        store(std::integral_constant<int, 8>{});
     };
     // one route for the whole wave (a per-entry choice would run both); the double route
     // keeps only the converted entries live across the moduli

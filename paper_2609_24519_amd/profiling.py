@@ -14,7 +14,8 @@ WRITE_SIZE, each in KiB per dispatch) of a command that also ran a plain
 device copy of a known size (``bench.py --calibrate-copy``), scales every
 kernel's counters by what the counters read for that copy, and records the
 per-dispatch HBM bytes of the GEMM together with a hash of the kernel sources
-they were taken on (the kernels and the GEMM's addressing header), so that a
+they were taken on (the kernels, the GEMM's addressing header and the encoders'
+plane packing), so that a
 later change to either makes them stale.
 ``counters`` summarises one or more ``--pmc`` passes over the same command:
 per kernel the FP4 MFMA operation count (checked against the algorithmic
@@ -30,7 +31,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 # the GEMM's kernel code and its addressing (tile configurations, copy / LDS / fragment offsets)
-KERNEL_SOURCES = (os.path.join(HERE, "csrc", "awe_kernels.hip"), os.path.join(HERE, "csrc", "gemm_layout.h"))
+KERNEL_SOURCES = tuple(os.path.join(HERE, "csrc", f) for f in ("awe_kernels.hip", "gemm_layout.h", "plane_pack.h"))
 COPY_BYTES = 1 << 30  # bench.py --calibrate-copy copies 1 GiB
 
 

@@ -265,8 +265,8 @@ awe_status awe_crt_workspace_bytes(const int32_t* moduli, int32_t n, int64_t M, 
    allows it), awe_crt into c128 and/or c64 (as for awe_crt, leading dimension ldc).  Requires M_prod > 2 K bound_a bound_b (AWE_ERR_OVERFLOW otherwise) and every
    modulus to have a scheme (AWE_ERR_UNSUPPORTED).  Entries beyond their bound set
    *d_range_flag.  The workspace (caller-owned device memory, awe_crt_workspace_bytes) holds the
-   moduli's code tables, all their planes and the n int32 residue products; it is uploaded to
-   and written on `stream`. */
+   moduli's code tables, all their planes and the n residue products (one byte per output each:
+   every modulus is at most 256); it is uploaded to and written on `stream`. */
 awe_status awe_gemm_crt(int64_t M, int64_t N, int64_t K, const int64_t* A, int64_t lda,
                         const int64_t* B, int64_t ldb, int64_t bound_a, int64_t bound_b,
                         const int32_t* moduli, int32_t n, int64_t* c128, double* c64, int64_t ldc,

@@ -393,7 +393,7 @@ struct CrtLayout {  // workspace of awe_gemm_crt
   size_t luts;                   // the moduli's code tables, A side then B side (n x 1 KiB each)
   size_t planes_a, planes_b;     // every modulus's stored planes of A, then of B
   int64_t off_a[kMaxModuli], off_b[kMaxModuli];
-  size_t res_c;                  // the n int32 residue products
+  size_t res_c;                  // the n residue products, one byte each (m <= 256)
   size_t total;
 };
 
@@ -412,7 +412,7 @@ CrtLayout crt_layout(const int32_t* moduli, int32_t n, int64_t M, int64_t N, int
   }
   L.planes_a = (size_t)round_up(pa, 256);
   L.planes_b = (size_t)round_up(pb, 256);
-  L.res_c = (size_t)round_up((int64_t)n * M * N * 4, 256);
+  L.res_c = (size_t)round_up((int64_t)n * M * N, 256);
   L.total = L.luts + L.planes_a + L.planes_b + L.res_c;
   return L;
 }
@@ -672,7 +672,7 @@ awe_status awe_gemm_crt(int64_t M, int64_t N, int64_t K, const int64_t* A, int64
   uint32_t* luts = reinterpret_cast<uint32_t*>(ws);
   uint8_t* pla = ws + L.luts;
   uint8_t* plb = pla + L.planes_a;
-  int32_t* rc = reinterpret_cast<int32_t*>(plb + L.planes_b);
+  uint8_t* rc = plb + L.planes_b;
   if (K > 0) {
     // every modulus's planes of A and of B straight from the int64 operands
     const std::vector<uint32_t>* tab = crt_tables(moduli, n, &st);
@@ -715,6 +715,7 @@ awe_status awe_gemm_crt(int64_t M, int64_t N, int64_t K, const int64_t* A, int64
     if (!s) return st;
     st = plan_gemm(*s, M, N, K, pla + L.off_a[j], plb + L.off_b[j], rc + (size_t)j * M * N, N, AWE_I32, 0, &plan);
     if (st != AWE_OK) return st;
+    for (GemmLaunch& gl : plan) gl.c_u8 = true;  // residues below 256: bytes, a quarter of the traffic
     single = single && plan.size() == 1;
     all.insert(all.end(), plan.begin(), plan.end());
   }

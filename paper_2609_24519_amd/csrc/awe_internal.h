@@ -174,6 +174,7 @@ struct GemmLaunch {
   void* C;
   int64_t ldc;
   awe_dtype c_type;
+  bool c_u8;                       // residues (modulus set) written as bytes instead of c_type
   bool accumulate;
   int log2D;
   int32_t modulus;
@@ -233,7 +234,11 @@ struct alignas(16) CrtParams {
   uint64_t half_lo, half_hi;    // floor(M / 2)
   int32_t n;
 };
+// Residues as int32 (awe_crt) or as bytes (awe_gemm_crt's own products, a quarter of the bytes).
 awe_status launch_crt(const int32_t* res, int64_t res_stride, int64_t rows, int64_t cols,
+                      int64_t ld_res, const CrtParams& P, int64_t* c128, double* c64, int64_t ldc,
+                      hipStream_t stream);
+awe_status launch_crt(const uint8_t* res, int64_t res_stride, int64_t rows, int64_t cols,
                       int64_t ld_res, const CrtParams& P, int64_t* c128, double* c64, int64_t ldc,
                       hipStream_t stream);
 

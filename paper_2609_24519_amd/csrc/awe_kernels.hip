@@ -301,7 +301,8 @@ struct GemmArgs {
   void* C;
   int64_t ldc;
   int32_t M, N;
-  int32_t c64, accumulate, log2D, modulus;
+  int32_t c64;  // C's elements: 0 int32, 1 int64, 2 bytes (residues only, modulus set)
+  int32_t accumulate, log2D, modulus;
   int32_t tiles_m, tiles_n;
   int64_t outer;  // C (+)= outer * (sum / D)
   uint32_t sa[2], sb[2];  // two planes per side: E8M0 scale word of plane 0 / 1 of A and B
@@ -573,6 +574,23 @@ __device__ __forceinline__ void store_output(const GemmArgs& g, int row, int col
     return;
   }
   store_value(g, row, col, (int64_t)(val >> g.log2D) * g.outer);
+}
+
+// A residue written as a byte (C's elements are bytes: m <= 256).  Its own epilogue loop, so
+// that the int32 / int64 one keeps its size (a larger loop body stopped its unrolling).
+__device__ __forceinline__ void store_residue_u8(const GemmArgs& g, int row, int col, int32_t val) {
+  if (row >= g.M || col >= g.N) return;
+  const int64_t off = (int64_t)row * g.ldc + col;
+  const int32_t m = g.modulus;
+  int32_t rr = val % m;
+  if (rr < 0) rr += m;
+  uint8_t* Cb = reinterpret_cast<uint8_t*>(g.C);
+  if (g.accumulate) {
+    const int32_t s = Cb[off] + rr;
+    Cb[off] = (uint8_t)(s >= m ? s - m : s);
+  } else {
+    __builtin_nontemporal_store((uint8_t)rr, Cb + off);
+  }
 }
 
 // A part of a split tile: its exact partial (a whole number of reduction
@@ -1096,6 +1114,20 @@ __device__ __forceinline__ void gemm_tile(GemmArgs g, FoldCoef fold_coef, int ti
         }
     return;
   }
+  if (g.c64 == 2) {  // residues as bytes (only with a modulus, whose tiles are never split)
+    auto emit8 = [&](int i, int j, int v, int32_t val) {
+      store_residue_u8(g, row0 + i * BS + (BS == 16 ? v : 8 * (v >> 2) + (v & 3)), col0 + j * BS, val);
+    };
+#pragma unroll
+    for (int b = 0; b < NREG; ++b)
+#pragma unroll
+      for (int v = 0; v < C::AV; ++v) emit8(b / C::AN, b % C::AN, v, iacc[b / C::AN][b % C::AN][v]);
+#pragma unroll
+    for (int b = NREG; b < C::AM * C::AN; ++b)
+#pragma unroll
+      for (int v = 0; v < C::AV; ++v) emit8(b / C::AN, b % C::AN, v, fold_lds[((b - NREG) * C::AV + v) * 64]);
+    return;
+  }
 #pragma unroll
   for (int b = 0; b < NREG; ++b)
 #pragma unroll
@@ -1298,7 +1330,7 @@ void fill_args(const GemmLaunch& L, GemmArgs& g) {
   g.ldc = L.ldc;
   g.M = (int32_t)L.M;
   g.N = (int32_t)L.N;
-  g.c64 = L.c_type == AWE_I64;
+  g.c64 = L.c_u8 && L.modulus ? 2 : (L.c_type == AWE_I64 ? 1 : 0);
   g.accumulate = L.accumulate;
   g.log2D = L.log2D;
   g.modulus = L.modulus;
@@ -1537,7 +1569,7 @@ awe_status launch_encode(const EncodeLaunch& e, hipStream_t stream) {
 
 awe_status launch_gemm(const GemmLaunch& L, hipStream_t stream) {
   if (L.M == 0 || L.N == 0) return AWE_OK;
-  const int64_t esize = L.c_type == AWE_I64 ? 8 : 4;
+  const int64_t esize = L.c_u8 && L.modulus ? 1 : (L.c_type == AWE_I64 ? 8 : 4);
   if (L.k_end <= L.k_begin) {
     if (L.accumulate) return AWE_OK;
     hipLaunchKernelGGL(fill_zero_kernel, dim3(1024), dim3(256), 0, stream,
@@ -1609,8 +1641,8 @@ bool gemm_group_ok(const GemmLaunch* L, int n) {
     if (a.M != L[0].M || a.N != L[0].N || a.K != L[0].K || a.k_begin != L[0].k_begin ||
         a.k_end != L[0].k_end || a.k_end <= a.k_begin)
       return false;
-    if (a.c_type != L[0].c_type || a.log2D != L[0].log2D || a.outer != L[0].outer || a.ldc != L[0].ldc ||
-        a.stride_a != L[0].stride_a || a.stride_b != L[0].stride_b)
+    if (a.c_type != L[0].c_type || a.c_u8 != L[0].c_u8 || (a.c_u8 && !a.modulus) || a.log2D != L[0].log2D ||
+        a.outer != L[0].outer || a.ldc != L[0].ldc || a.stride_a != L[0].stride_a || a.stride_b != L[0].stride_b)
       return false;
   }
   return true;

@@ -292,9 +292,10 @@ __device__ __forceinline__ double wide_to_double(uint64_t lo, uint64_t hi) {
 
 // The reconstruction's constants (about 1.6 KiB: the digit coefficients alone are
 // n(n-1)/2 bytes) are staged once per workgroup in LDS and read there as uniform
-// 16-byte words; held in scalar registers they would not fit.
-template <int NMAX>
-__global__ __launch_bounds__(256) void crt_kernel(const int32_t* __restrict__ res, int64_t res_stride,
+// 16-byte words; held in scalar registers they would not fit.  Residues come as int32 or as
+// bytes (RT).
+template <int NMAX, class RT>
+__global__ __launch_bounds__(256) void crt_kernel(const RT* __restrict__ res, int64_t res_stride,
                                                   int64_t rows, int64_t cols, int64_t ld_res,
                                                   CrtParams P, int64_t* __restrict__ c128,
                                                   double* __restrict__ c64, int64_t ldc) {
@@ -309,13 +310,13 @@ __global__ __launch_bounds__(256) void crt_kernel(const int32_t* __restrict__ re
        i += (int64_t)gridDim.x * blockDim.x) {
     asm volatile("" ::: "memory");  // read the constants from LDS where used, not hoisted into registers
     const int64_t r = i / cols, c = i - r * cols;
-    const int32_t* src = res + r * ld_res + c;
+    const RT* src = res + r * ld_res + c;
     // Mixed-radix digits: X = v_0 + v_1 P_1 + ... + v_{n-1} P_{n-1}, P_j = m_0 ... m_{j-1},
     // v_j = (r_j - sum_{i<j} v_i (P_i mod m_j)) (P_j^-1 mod m_j)  mod m_j.  The subtracted
     // sum stays below off_j < 2^22, so both reductions are mod_f's.
     int32_t rj[NMAX];
 #pragma unroll
-    for (int j = 0; j < NMAX; ++j) rj[j] = j < n ? src[j * res_stride] : 0;
+    for (int j = 0; j < NMAX; ++j) rj[j] = j < n ? (int32_t)src[j * res_stride] : 0;
     uint32_t v[NMAX];
 #pragma unroll
     for (int j = 0; j < NMAX; ++j) {
@@ -422,19 +423,19 @@ awe_status launch_residue_encode(const ResidueEncodeArgs& a, const ResidueParams
   return AWE_OK;
 }
 
-awe_status launch_crt(const int32_t* res, int64_t res_stride, int64_t rows, int64_t cols,
-                      int64_t ld_res, const CrtParams& P, int64_t* c128, double* c64, int64_t ldc,
-                      hipStream_t stream) {
+template <class RT>
+awe_status launch_crt_t(const RT* res, int64_t res_stride, int64_t rows, int64_t cols, int64_t ld_res,
+                        const CrtParams& P, int64_t* c128, double* c64, int64_t ldc, hipStream_t stream) {
   if (rows == 0 || cols == 0) return AWE_OK;
   const dim3 grid(grid_for(rows * cols)), block(256);
   if (P.n <= 8)
-    hipLaunchKernelGGL(crt_kernel<8>, grid, block, 0, stream, res, res_stride, rows, cols, ld_res, P,
+    hipLaunchKernelGGL((crt_kernel<8, RT>), grid, block, 0, stream, res, res_stride, rows, cols, ld_res, P,
                        c128, c64, ldc);
   else if (P.n <= 16)
-    hipLaunchKernelGGL(crt_kernel<16>, grid, block, 0, stream, res, res_stride, rows, cols, ld_res, P,
+    hipLaunchKernelGGL((crt_kernel<16, RT>), grid, block, 0, stream, res, res_stride, rows, cols, ld_res, P,
                        c128, c64, ldc);
   else
-    hipLaunchKernelGGL(crt_kernel<32>, grid, block, 0, stream, res, res_stride, rows, cols, ld_res, P,
+    hipLaunchKernelGGL((crt_kernel<32, RT>), grid, block, 0, stream, res, res_stride, rows, cols, ld_res, P,
                        c128, c64, ldc);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) {
@@ -442,6 +443,18 @@ awe_status launch_crt(const int32_t* res, int64_t res_stride, int64_t rows, int6
     return AWE_ERR_HIP;
   }
   return AWE_OK;
+}
+
+awe_status launch_crt(const int32_t* res, int64_t res_stride, int64_t rows, int64_t cols,
+                      int64_t ld_res, const CrtParams& P, int64_t* c128, double* c64, int64_t ldc,
+                      hipStream_t stream) {
+  return launch_crt_t(res, res_stride, rows, cols, ld_res, P, c128, c64, ldc, stream);
+}
+
+awe_status launch_crt(const uint8_t* res, int64_t res_stride, int64_t rows, int64_t cols,
+                      int64_t ld_res, const CrtParams& P, int64_t* c128, double* c64, int64_t ldc,
+                      hipStream_t stream) {
+  return launch_crt_t(res, res_stride, rows, cols, ld_res, P, c128, c64, ldc, stream);
 }
 
 }  // namespace awe

@@ -25,6 +25,11 @@ awe_status launch_crt(const int32_t*, int64_t, int64_t, int64_t, int64_t, const 
   ++g_launches;
   return AWE_OK;
 }
+awe_status launch_crt(const uint8_t*, int64_t, int64_t, int64_t, int64_t, const CrtParams&, int64_t*, double*,
+                      int64_t, hipStream_t) {
+  ++g_launches;
+  return AWE_OK;
+}
 // a host buffer stands in for the device planes array (the stubbed launchers never touch it)
 awe_status noalloc_planes(void** out) {
   static unsigned char planes[256];

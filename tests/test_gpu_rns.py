@@ -162,6 +162,22 @@ def test_gemm_crt_grouped_launch(monkeypatch, grouped, cfg):
     assert np.array_equal(c64.cpu().numpy(), ocrt.to_double(ref))
 
 
+def test_gemm_crt_split_reduction():
+    # K beyond what one launch of modulus 147's scheme may reduce (about 165,000 indices for its
+    # int32 partial sums): its residue product takes two launches, the second adding mod 147 into
+    # the byte residues of the first; the other moduli take one launch each, so nothing is grouped
+    ms = [147, 149, 151, 157, 139]
+    M, N, K, bound = 32, 40, 200_000, 100
+    rng = np.random.default_rng(7)
+    A = rng.integers(-bound, bound, size=(M, K), dtype=np.int64, endpoint=True)
+    B = rng.integers(-bound, bound, size=(K, N), dtype=np.int64, endpoint=True)
+    c128, c64 = awe.matmul_crt(to_dev(A), to_dev(B), ms, bound, bound)
+    torch.cuda.synchronize()
+    ref = og.gemm_i128(A, B)
+    assert (_words_to_ints(c128) == ref).all()
+    assert np.array_equal(c64.cpu().numpy(), ocrt.to_double(ref))
+
+
 def test_gemm_crt_extremes():
     # every product at the bound: C = -K B^2 needs 120 bits and the top of the range
     ms = _moduli()

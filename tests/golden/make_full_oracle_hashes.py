@@ -1,5 +1,9 @@
-"""Writes full_oracle_sha256.txt: the SHA-256 of the oracle's whole C for the two workloads
-whose full product is too slow to recompute inside a GPU test.
+"""Writes full_oracle_sha256.txt: the SHA-256 of the oracle's whole C for the workloads whose
+full product is too slow to recompute inside a GPU test.
+
+* The headline product at 8192^3: operands ``inputs.int8_pair(8192, 8192, 8192, seed=0)``, C = A B
+  exactly as int32 (Alg. 1, its postcondition; |C| <= 8192 * 128^2 fits), and the INT4 x INT8
+  product on ``inputs.int8_pair(8192, 8192, 8192, seed=0, a_range=(-8, 7))`` (Sec. 5.2).
 
 * Residue products at 4096^3, one per modulus of moduli_fp64_k16384.txt: operands
   ``inputs.residue_pair(4096, 4096, 4096, m)`` (seed m), C = (A B) mod m as int32 in [0, m)
@@ -40,6 +44,15 @@ def main():
     lines = ["# SHA-256 of the oracle's full C (C-contiguous little-endian bytes), written by",
              "# make_full_oracle_hashes.py from oracle/ and the seeded inputs only.",
              "# workload | M N K | dtype | sha256"]
+    for name, a_range in (("int8 8192", None), ("int4xint8 8192", (-8, 7))):
+        t0 = time.time()
+        A, B = (inputs.int8_pair(8192, 8192, 8192, seed=0) if a_range is None else
+                inputs.int8_pair(8192, 8192, 8192, seed=0, a_range=a_range))
+        C = og.gemm_i64(A, B)
+        assert np.abs(C).max() < 2**31
+        lines.append("%s | 8192 8192 8192 | int32 | %s" % (name, digest(C.astype(np.int32))))
+        print(lines[-1], "(%.0f s)" % (time.time() - t0), flush=True)
+        del A, B, C
     for m in moduli():
         t0 = time.time()
         A, B = inputs.residue_pair(4096, 4096, 4096, m)

@@ -5,7 +5,31 @@ bricks of 32 rows x 64 reduction indices, stored k-step major, K padded to
 a multiple of awe.K_PAD, lane L = 32 h + t owning row t and
 indices 32 h .. 32 h + 31, two E2M1 codes per byte, low nibble first).
 """
+import hashlib
+import os
+
 import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _full_hashes():
+    out = {}
+    with open(os.path.join(GOLDEN, "full_oracle_sha256.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                name, dims, dtype, digest = [x.strip() for x in line.split("|")]
+                out[name] = (tuple(int(v) for v in dims.split()), dtype, digest)
+    return out
+
+
+def full_oracle_match(C, name, shape, dtype):
+    """Whether C (host array) equals the oracle's whole C for workload `name`, by the SHA-256 that
+    tests/golden/make_full_oracle_hashes.py wrote from the oracle."""
+    dims, want_dtype, digest = _full_hashes()[name]
+    assert C.shape == shape and str(C.dtype) == want_dtype == dtype, (C.shape, C.dtype)
+    return hashlib.sha256(np.ascontiguousarray(C).tobytes()).hexdigest() == digest
+
 
 E2M1_MAG = np.array([0, 1, 2, 3, 4, 6, 8, 12], dtype=np.int64)
 

@@ -2,9 +2,10 @@
 benchmark times, against the oracle (bit-exact).
 
 * 256^3 int8, base-13 and AWE6 (in test_gpu_gemm.py).
-* 8192^3 int8, AWE6 and base-13, int32 C: 64 random 128 x 128 output tiles plus the
-  4 corner tiles against the oracle restricted to those tiles, and a full 2048^3
-  product against the full oracle.
+* 8192^3 int8, AWE6 and base-13, int32 C: the whole C against the oracle's (its SHA-256 in
+  tests/golden/full_oracle_sha256.txt, written from the oracle by make_full_oracle_hashes.py),
+  64 random 128 x 128 output tiles plus the 4 corner tiles against the oracle restricted to
+  those tiles (which locate a difference), and a full 2048^3 product against the full oracle.
 * 8192^3 int4 x int8, AWE4: the same checks.
 * 4096^3 residues for every modulus of the FP64-significand residue set
   (tests/golden/moduli_fp64_k16384.txt): the whole C against the oracle's (its SHA-256 in
@@ -14,7 +15,6 @@ benchmark times, against the oracle (bit-exact).
   segment: the whole C against the oracle's (SHA-256 as above), closed forms over the whole
   of C where they exist, plus sampled tiles.
 """
-import hashlib
 import os
 
 import numpy as np
@@ -23,7 +23,7 @@ import torch
 
 from oracle import gemm as og
 from paper_2609_24519_amd import awe, inputs
-from tests.gpu_helpers import to_dev
+from tests.gpu_helpers import full_oracle_match, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -34,23 +34,6 @@ def _moduli():
     with open(os.path.join(GOLDEN, "moduli_fp64_k16384.txt")) as f:
         lines = [l for l in f if l.strip() and not l.startswith("#")]
     return [int(x) for x in lines[0].split()]
-
-
-def _full_hashes():
-    out = {}
-    with open(os.path.join(GOLDEN, "full_oracle_sha256.txt")) as f:
-        for line in f:
-            if line.strip() and not line.startswith("#"):
-                name, dims, dtype, digest = [x.strip() for x in line.split("|")]
-                out[name] = (tuple(int(v) for v in dims.split()), dtype, digest)
-    return out
-
-
-def _check_full(C, name, shape, dtype):
-    """C (host array) against the SHA-256 of the oracle's whole C for workload `name`."""
-    dims, want_dtype, digest = _full_hashes()[name]
-    assert C.shape == shape and str(C.dtype) == want_dtype == dtype, (C.shape, C.dtype)
-    return hashlib.sha256(np.ascontiguousarray(C).tobytes()).hexdigest() == digest
 
 
 def _check_tiles(C, A, B, tiles, mod=None):
@@ -77,10 +60,12 @@ def int8_8192():
 
 
 @pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_B13])
-def test_config2_int8_8192_sampled(int8_8192, enc):
+def test_config2_int8_8192(int8_8192, enc):
     A, B = int8_8192
     C = _exact_on_gpu(enc, A, B)
+    full_ok = full_oracle_match(C, "int8 8192", (8192, 8192), "int32")
     _check_tiles(C, A, B, inputs.sample_tiles(8192, 8192, 64, 128, seed=1))
+    assert full_ok, "whole C differs from the oracle's (sampled tiles agree)"
 
 
 @pytest.mark.parametrize("enc", [awe.ENC_AWE6, awe.ENC_B13])
@@ -90,10 +75,12 @@ def test_config2_full_2048(enc):
     assert np.array_equal(C.astype(np.int64), og.gemm_i64(A, B))
 
 
-def test_config3_int4_int8_8192_sampled():
+def test_config3_int4_int8_8192():
     A, B = inputs.int8_pair(8192, 8192, 8192, seed=0, a_range=(-8, 7))
     C = _exact_on_gpu(awe.ENC_AWE4, A, B)
+    full_ok = full_oracle_match(C, "int4xint8 8192", (8192, 8192), "int32")
     _check_tiles(C, A, B, inputs.sample_tiles(8192, 8192, 64, 128, seed=1))
+    assert full_ok, "whole C differs from the oracle's (sampled tiles agree)"
 
 
 def test_config3_full_2048():
@@ -110,7 +97,7 @@ def test_config4_residues_4096(m):
     Ch = C.cpu().numpy()
     del C
     assert Ch.min() >= 0 and Ch.max() < m
-    full_ok = _check_full(Ch, "residues mod %d" % m, (4096, 4096), "int32")
+    full_ok = full_oracle_match(Ch, "residues mod %d" % m, (4096, 4096), "int32")
     # sampled tiles locate a difference; the whole C must match the oracle's in any case
     _check_tiles(Ch, A, B, inputs.sample_tiles(4096, 4096, 12, 128, seed=m), mod=m)
     assert full_ok, "C mod %d differs from the oracle's full product" % m
@@ -163,7 +150,7 @@ def test_config5_stress_65536(stress, kseg):
     Ch = C.cpu().numpy()
     del C, pa, pb
     torch.cuda.empty_cache()
-    full_ok = _check_full(Ch, "stress", (4096, 4096), "int64")
+    full_ok = full_oracle_match(Ch, "stress", (4096, 4096), "int64")
     _stress_closed_forms(Ch, A, B, K)
     _check_tiles(Ch, A, B, inputs.sample_tiles(M, N, 4, 64, seed=5))
     assert full_ok, "the stress product differs from the oracle's full product"

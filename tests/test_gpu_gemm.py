@@ -11,7 +11,7 @@ import torch
 
 from oracle import gemm as og
 from paper_2609_24519_amd import awe, inputs
-from tests.gpu_helpers import to_dev
+from tests.gpu_helpers import full_oracle_match, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -373,17 +373,20 @@ def test_every_e2m3_tile_configuration(monkeypatch, cfg):
     assert np.array_equal(C.cpu().numpy(), ref)
 
 
-def test_fp6k3_8192_sampled():
-    # INT8 x INT8 in 3 E2M3 products at 8192^3 (the benchmark's shape and launch), int32 C,
-    # sampled 128 x 128 tiles plus the four corner tiles
+def test_fp6k3_8192():
+    # INT8 x INT8 in 3 E2M3 products at 8192^3 (the benchmark's shape and launch), int32 C: the
+    # whole C against the oracle's (by its SHA-256), sampled 128 x 128 tiles plus the four corner
+    # tiles to locate a difference
     M = N = K = 8192
     A, B = inputs.int8_pair(M, N, K, seed=0)
     C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_FP6K3, torch.int32)
     torch.cuda.synchronize()
     Ch = C.cpu().numpy()
+    full_ok = full_oracle_match(Ch, "int8 8192", (M, N), "int32")
     for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=1):
         ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
         assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)
+    assert full_ok, "whole C differs from the oracle's (sampled tiles agree)"
 
 
 @pytest.mark.parametrize("cfg", ["0", "1"])
@@ -407,17 +410,19 @@ def test_shared_accumulator_configurations(monkeypatch, cfg):
     assert np.array_equal(C.cpu().numpy(), ref)
 
 
-def test_fp6p4_8192_sampled():
-    # the weights-in-scales scheme at 8192^3 (the benchmark's shape and launch), int32 C,
-    # sampled 128 x 128 tiles plus the four corner tiles
+def test_fp6p4_8192():
+    # the weights-in-scales scheme at 8192^3 (the benchmark's shape and launch), int32 C: the
+    # whole C against the oracle's (by its SHA-256), sampled tiles to locate a difference
     M = N = K = 8192
     A, B = inputs.int8_pair(M, N, K, seed=0)
     C = awe.matmul_exact(to_dev(A), to_dev(B), awe.ENC_FP6P4, torch.int32)
     torch.cuda.synchronize()
     Ch = C.cpu().numpy()
+    full_ok = full_oracle_match(Ch, "int8 8192", (M, N), "int32")
     for rows, cols in inputs.sample_tiles(M, N, 16, 128, seed=3):
         ref = og.gemm_i64(np.ascontiguousarray(A[rows]), np.ascontiguousarray(B[:, cols]))
         assert np.array_equal(Ch[rows][:, cols].astype(np.int64), ref)
+    assert full_ok, "whole C differs from the oracle's (sampled tiles agree)"
 
 
 @pytest.mark.parametrize("allpairs", ["1", "0"])

@@ -156,9 +156,9 @@ def test_wide_product_int64_boundaries():
 
 
 def test_full_oracle_hash_file_matches_oracle():
-    """tests/golden/full_oracle_sha256.txt (used by the GPU tests of the residue and stress
-    workloads) lists every modulus of the residue set and the stress workload, and its entry for
-    m = 5 is the SHA-256 of the oracle's C recomputed here (8 s on a few cores)."""
+    """tests/golden/full_oracle_sha256.txt (used by the GPU tests of the large workloads) lists
+    the two 8192^3 products, every modulus of the residue set and the stress workload, and its
+    entry for m = 5 is the SHA-256 of the oracle's C recomputed here (8 s on a few cores)."""
     import hashlib
     import os
 
@@ -171,8 +171,9 @@ def test_full_oracle_hash_file_matches_oracle():
             if line.strip() and not line.startswith("#"):
                 name, dims, dtype, digest = [x.strip() for x in line.split("|")]
                 rows[name] = (dims, dtype, digest)
-    assert set(rows) == {"residues mod %d" % m for m in moduli} | {"stress"}
+    assert set(rows) == {"residues mod %d" % m for m in moduli} | {"stress", "int8 8192", "int4xint8 8192"}
     assert rows["stress"][:2] == ("4096 4096 65536", "int64")
+    assert rows["int8 8192"][:2] == rows["int4xint8 8192"][:2] == ("8192 8192 8192", "int32")
     A, B = inputs.residue_pair(4096, 4096, 4096, 5)
     C = og.gemm_mod(5, A, B)
     assert rows["residues mod 5"][:2] == ("4096 4096 4096", "int32")
